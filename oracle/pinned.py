@@ -1,0 +1,73 @@
+"""ctypes loader for the oracle's fixed-order fp32 routines (``pinned.c``).
+
+TEST INFRASTRUCTURE ONLY: the product path never imports this module.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pinned.c")
+_LIB = os.path.join(_HERE, "_pinned.so")
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile pinned.c with gcc (contraction off, so only the written fmaf fuse)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O3", "-mavx2", "-mfma", "-ffp-contract=off", "-fno-fast-math",
+                               "-fopenmp", "-fPIC", "-shared", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            lib = ctypes.CDLL(build())
+            f = ctypes.POINTER(ctypes.c_float)
+            i32 = ctypes.c_int32
+            lib.oracle_embed_f32.argtypes = [f, f, f, f, i32, i32, i32, f]
+            lib.oracle_embed_f32.restype = None
+            lib.oracle_cosine_f32.argtypes = [f, f, i32, i32, f]
+            lib.oracle_cosine_f32.restype = None
+            _lib = lib
+    return _lib
+
+
+def _fp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def embed_f32(patches: np.ndarray, w_pe: np.ndarray, b_pe: np.ndarray, pos: np.ndarray) -> np.ndarray:
+    """T0 = patch embedding + Pos in the fixed fp32 fmaf order; [N][D] float32."""
+    lib = _load()
+    patches = np.ascontiguousarray(patches, dtype=np.float32)
+    w_pe = np.ascontiguousarray(w_pe, dtype=np.float32)
+    b_pe = np.ascontiguousarray(b_pe, dtype=np.float32)
+    pos = np.ascontiguousarray(pos, dtype=np.float32)
+    n, p = patches.shape
+    d = w_pe.shape[1]
+    assert w_pe.shape == (p, d) and b_pe.shape == (d,) and pos.shape == (n, d)
+    out = np.empty((n, d), dtype=np.float32)
+    lib.oracle_embed_f32(_fp(patches), _fp(w_pe), _fp(b_pe), _fp(pos), n, p, d, _fp(out))
+    return out
+
+
+def cosine_f32(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Row-wise cosine in the fixed fp32 order; [N] float32."""
+    lib = _load()
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    assert a.shape == b.shape and a.ndim == 2
+    out = np.empty((a.shape[0],), dtype=np.float32)
+    lib.oracle_cosine_f32(_fp(a), _fp(b), a.shape[0], a.shape[1], _fp(out))
+    return out

@@ -1,0 +1,237 @@
+"""CPU oracle of incremental ViT encoding with temporal token reuse.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package; the product path
+never does, and this package imports nothing from the product.
+
+What it computes (paper §III-B, "Temporal Token Reuse"):
+
+* every frame is patch-embedded and each token is scored by the cosine of its
+  current and cached representation (eq. 3); the least similar tokens are the
+  updated set U, the rest R reuse their cache (the top-rho*N rule, here a
+  threshold tau followed by a cap);
+* the index set is chosen once, before the first layer, and reused by every
+  layer;
+* in every layer, Q, K and V are recomputed only for the rows in U (eq. 4);
+  the new K/V rows are scattered into the cached full K/V (eq. 5);
+* attention is computed only for the updated queries, over all N keys;
+  reused tokens keep their cached outputs; the updated rows then go through the
+  residual add and the MLP.
+
+The model is a pre-LN ViT (the paper's vision encoder is a SigLIP/ViT, §III-A):
+no CLS token, learned positions added after the patch embedding, biased
+linear layers, LayerNorm with biased variance, tanh-form GELU, softmax
+attention scaled by 1/sqrt(d_h), and a final LayerNorm.  These details are not
+in the paper; they are the readings this build takes.
+
+Arithmetic: everything is float64 except the patch embedding and the cosine,
+which follow a fixed fp32 order (``pinned.c``) so that the selection is
+reproducible bit for bit.  ``S(.)`` rounds to the storage precision (bf16 with
+ties to even, fp32, or nothing for the "f64" mode used by the pins) at the
+points where a stored or GEMM-operand value is formed: Q/K/V, the LN outputs
+fed to a GEMM, the attention output, the GELU output, each layer's output rows,
+the final output and the layer-0 input rows.  The residual H stays unrounded.
+
+Parity: pinned (see tests/test_oracle_*.py) by library routines (torch fp64
+functional ops), closed forms, brute-force selection, and the invariants the
+method fixes.  No intermediate value printed in the paper exists to pin against.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import pinned
+
+# ----------------------------------------------------------------------------
+# Elementary operations
+# ----------------------------------------------------------------------------
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bf16 number (8 significant bits),
+    ties to even, directly from float64.  Normal range only."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)              # x = m * 2**e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
+
+
+def S(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round to the storage precision; returns float64."""
+    if dtype == "bf16":
+        return round_bf16(x)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+    if dtype == "f64":
+        return np.asarray(x, dtype=np.float64)
+    raise ValueError(dtype)
+
+
+def layer_norm(x: np.ndarray, g: np.ndarray, b: np.ndarray, eps: float) -> np.ndarray:
+    """LayerNorm over the last axis with the biased variance."""
+    mean = x.mean(axis=-1, keepdims=True)
+    var = ((x - mean) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mean) / np.sqrt(var + eps) * g + b
+
+
+def gelu_tanh(x: np.ndarray) -> np.ndarray:
+    """GELU, tanh form: 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))."""
+    return 0.5 * x * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (x + 0.044715 * x ** 3)))
+
+
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, heads: int) -> np.ndarray:
+    """Multi-head softmax attention of the rows of q over all rows of k, v.
+
+    q: [m][D], k, v: [N][D]; head j uses columns [j*dh, (j+1)*dh)."""
+    m, d = q.shape
+    dh = d // heads
+    out = np.empty((m, d), dtype=np.float64)
+    for j in range(heads):
+        c = slice(j * dh, (j + 1) * dh)
+        s = q[:, c] @ k[:, c].T / math.sqrt(dh)
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        out[:, c] = (p @ v[:, c]) / p.sum(axis=1, keepdims=True)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Token selection (eq. 3 and the top-rho*N rule)
+# ----------------------------------------------------------------------------
+
+
+def select(sim: np.ndarray, tau: float, cap: int) -> np.ndarray:
+    """U = {i : sim_i < tau} (fp32 compare); if |U| > cap keep the cap lowest
+    similarities, equal similarities going to the lower index.  Ascending."""
+    sim = np.asarray(sim, dtype=np.float32)
+    if np.isnan(sim).any():
+        raise ValueError("non-finite similarity: the frame holds NaN or Inf")
+    n = sim.shape[0]
+    cap = max(0, min(int(cap), n))
+    cand = np.nonzero(sim < np.float32(tau))[0]
+    if cand.size > cap:
+        order = np.lexsort((cand, sim[cand]))   # by sim, then by index
+        cand = np.sort(cand[order[:cap]])
+    return cand.astype(np.int32)
+
+
+# ----------------------------------------------------------------------------
+# Model and per-view cache
+# ----------------------------------------------------------------------------
+
+
+class Model:
+    """Weights of the encoder as float64 arrays (values as stored)."""
+
+    def __init__(self, shape, weights: Dict[str, np.ndarray], dtype: Optional[str] = None):
+        self.shape = shape
+        self.dtype = dtype or shape.dtype
+        self.eps = float(shape.ln_eps)
+        self.w = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
+        self.w32 = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in
+                    (("w_pe", weights["w_pe"]), ("b_pe", weights["b_pe"]), ("pos", weights["pos"]))}
+
+    def p(self, l: int, name: str) -> np.ndarray:
+        return self.w[f"l{l}.{name}"]
+
+
+@dataclasses.dataclass
+class ViewCache:
+    """Everything one stream keeps between frames, canonical layout.
+
+    ref: [N][D] fp32, each token's embedding at its last refresh (the
+    reference the cosine is taken against);
+    X: [L+1][N][D] layer inputs (X[0] = embedded tokens, X[l+1] = layer l out);
+    K, V: [L][N][D] per-layer keys and values;  Y: [N][D] final output."""
+
+    ref: np.ndarray
+    X: np.ndarray
+    K: np.ndarray
+    V: np.ndarray
+    Y: np.ndarray
+
+    def copy(self) -> "ViewCache":
+        return ViewCache(self.ref.copy(), self.X.copy(), self.K.copy(), self.V.copy(), self.Y.copy())
+
+
+@dataclasses.dataclass
+class StepResult:
+    idx: np.ndarray        # int32 [k], ascending
+    sim: np.ndarray        # float32 [N], fixed-order cosine
+    refreshed: np.ndarray  # [k][D] = Y[idx]
+    t0: np.ndarray         # float32 [N][D] embedded tokens of this frame
+
+    @property
+    def count(self) -> int:
+        return int(self.idx.shape[0])
+
+
+def embed(model: Model, patches: np.ndarray) -> np.ndarray:
+    """Patch embedding + Pos for all tokens, fixed fp32 order; [N][D] fp32."""
+    w = model.w32
+    return pinned.embed_f32(patches, w["w_pe"], w["b_pe"], w["pos"])
+
+
+def _encode_rows(model: Model, cache: ViewCache, U: np.ndarray, t0: np.ndarray,
+                 trace: Optional[dict] = None) -> None:
+    """Recompute rows U through every layer against the cached rows R.
+
+    The caller has already decided U.  K/V rows of U are written before the
+    attention of the layer, so the updated queries see the new keys of U and
+    the cached keys of R.  `trace`, if given, collects the per-layer attention
+    outputs and residuals of the rows U (for tests)."""
+    m, dt = model.shape, model.dtype
+    D, H = m.dim, m.heads
+    cache.ref[U] = t0[U]
+    Z = S(t0[U].astype(np.float64), dt)
+    cache.X[0][U] = Z
+    for l in range(m.depth):
+        A = S(layer_norm(Z, model.p(l, "ln1_g"), model.p(l, "ln1_b"), model.eps), dt)
+        qkv = S(A @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)
+        q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
+        cache.K[l][U] = k
+        cache.V[l][U] = v
+        O = S(attention(q, cache.K[l], cache.V[l], H), dt)
+        Hres = Z + (O @ model.p(l, "w_o") + model.p(l, "b_o"))
+        if trace is not None:
+            trace.setdefault("O", []).append(O)
+            trace.setdefault("H", []).append(Hres)
+        A2 = S(layer_norm(Hres, model.p(l, "ln2_g"), model.p(l, "ln2_b"), model.eps), dt)
+        G = S(gelu_tanh(A2 @ model.p(l, "w_1") + model.p(l, "b_1")), dt)
+        Z = S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
+        cache.X[l + 1][U] = Z
+    cache.Y[U] = S(layer_norm(Z, model.w["lnf_g"], model.w["lnf_b"], model.eps), dt)
+
+
+def empty_cache(model: Model) -> ViewCache:
+    m = model.shape
+    N, D, L = m.n_tokens, m.dim, m.depth
+    return ViewCache(ref=np.zeros((N, D), np.float32), X=np.zeros((L + 1, N, D)),
+                     K=np.zeros((L, N, D)), V=np.zeros((L, N, D)), Y=np.zeros((N, D)))
+
+
+def full_encode(model: Model, patches: np.ndarray) -> ViewCache:
+    """Full forward of one frame; fills every cache row (the paper's odd chunk)."""
+    cache = empty_cache(model)
+    t0 = embed(model, patches)
+    _encode_rows(model, cache, np.arange(model.shape.n_tokens), t0)
+    return cache
+
+
+def step(model: Model, patches: np.ndarray, cache: ViewCache, tau: float, cap: int,
+         trace: Optional[dict] = None) -> StepResult:
+    """Incremental encode of one frame; updates `cache` in place."""
+    t0 = embed(model, patches)
+    sim = pinned.cosine_f32(t0, cache.ref)
+    U = select(sim, tau, cap)
+    if U.size:
+        _encode_rows(model, cache, U, t0, trace)
+    return StepResult(idx=U, sim=sim, refreshed=cache.Y[U].copy(), t0=t0)
+
+
+def full_forward_dense(model: Model, patches: np.ndarray) -> np.ndarray:
+    """Y of a plain full forward (no cache); same as full_encode(...).Y."""
+    return full_encode(model, patches).Y
