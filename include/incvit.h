@@ -1,0 +1,190 @@
+/*
+ * incvit: incremental ViT encoding of streaming camera frames on MI355X (gfx950).
+ *
+ * The method (paper §III-B, "Temporal Token Reuse"): for each new frame every
+ * token is scored by the cosine similarity of its current and cached
+ * representation (eq. 3); the least similar tokens form the updated set U and
+ * are recomputed through every layer -- Q, K, V only for U (eq. 4), the new K/V
+ * rows scattered into the cached full K/V (eq. 5), attention only for the
+ * updated queries over all N keys, then the residual and the MLP -- while the
+ * other tokens reuse their cached outputs.  The index set is chosen once,
+ * before the first layer, and reused by every layer.
+ *
+ * Readings taken where the paper is silent (each is an argument of this API or
+ * fixed here):
+ *   - the score is the cosine of the layer-1 input token (patch embedding +
+ *     position) against that token's value at its last refresh, computed in a
+ *     fixed fp32 order so that selection is reproducible bit for bit;
+ *   - "top rho*N lowest similarities" is generalised to: U = {i : sim_i < tau}
+ *     (strict), and if |U| > cap only the cap lowest similarities are kept,
+ *     equal similarities going to the lower token index.  tau = +INFINITY with
+ *     cap = round(rho*N) is the paper's top-rho*N rule;
+ *   - the encoder is a pre-LN ViT without CLS token: learned positions added
+ *     after the patch embedding, biased linear layers, LayerNorm with biased
+ *     variance, tanh GELU, attention scaled by 1/sqrt(d_h), final LayerNorm.
+ *
+ * Conventions for every entry point:
+ *   - every buffer argument is DEVICE memory owned by the caller, except
+ *     `cap` of incvit_step and the config / handle structs, which are host;
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream); work
+ *     is enqueued asynchronously on it and results are valid after the caller
+ *     synchronises it; no entry point below synchronises unless it says so;
+ *   - argument and shape errors are returned before anything is enqueued;
+ *     HIP launch errors return INCVIT_ERR_HIP; incvit_last_error() gives text;
+ *   - a handle is not thread-safe; handles are independent of each other;
+ *   - the library allocates no device memory: weights, caches, workspace,
+ *     inputs and outputs are all passed in.
+ */
+#ifndef INCVIT_H_
+#define INCVIT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  INCVIT_OK = 0,
+  INCVIT_ERR_ARG = -1,         /* null pointer, bad count, NaN tau, ...          */
+  INCVIT_ERR_SHAPE = -2,       /* inconsistent model shape                        */
+  INCVIT_ERR_UNSUPPORTED = -3, /* shape valid but outside what the kernels cover  */
+  INCVIT_ERR_STATE = -4,       /* cache not initialised or from another model     */
+  INCVIT_ERR_HIP = -5          /* a HIP call failed                               */
+} incvit_status;
+
+typedef enum { INCVIT_F32 = 0, INCVIT_BF16 = 1 } incvit_dtype;
+
+/* Model and limits.  N = (img_h/patch)*(img_w/patch) tokens, P = channels*patch^2
+ * patch features, D = dim, L = depth, h = heads, d_h = D/h, F = mlp_dim.
+ * Supported: img_h, img_w multiples of patch; D % 32 == 0; D % h == 0;
+ * d_h % 8 == 0 and d_h <= 128; N <= 4096; D <= 2048; F >= 1;
+ * 1 <= max_streams <= 64.  dtype is the storage type of weights, caches and
+ * activations (GEMMs accumulate in fp32; LayerNorm, softmax, GELU in fp32). */
+typedef struct {
+  int32_t img_h, img_w, channels, patch;
+  int32_t dim, depth, heads, mlp_dim;
+  int32_t dtype;       /* incvit_dtype */
+  float ln_eps;        /* e.g. 1e-6 */
+  int32_t max_streams; /* largest B accepted by a call */
+} incvit_config;
+
+typedef struct incvit_handle incvit_handle;
+
+/* ---------------------------------------------------------------- weights -- */
+
+/* Bytes of the canonical weight buffer: the parameters below, in this order,
+ * each row-major, each element of the storage dtype:
+ *   W_pe [P][D] (row (c*p + dy)*p + dx), b_pe [D], Pos [N][D],
+ *   per layer l = 0..L-1: ln1_g [D], ln1_b [D], W_qkv [D][3D] (columns
+ *     [0,D) Q, [D,2D) K, [2D,3D) V; head j owns columns [j*d_h,(j+1)*d_h) of
+ *     each block), b_qkv [3D], W_o [D][D], b_o [D], ln2_g [D], ln2_b [D],
+ *     W_1 [D][F], b_1 [F], W_2 [F][D], b_2 [D],
+ *   lnf_g [D], lnf_b [D].
+ * Every linear layer computes y = x W + b.  Returns 0 for an invalid config. */
+size_t incvit_canonical_weights_bytes(const incvit_config* cfg);
+
+/* Bytes of the packed (device-layout) weight buffer.  0 for an invalid config. */
+size_t incvit_packed_weights_bytes(const incvit_config* cfg);
+
+/* Repack canonical weights (device) into the kernels' layout (device):
+ * GEMM weights in 16-column x 32-row MFMA operand chunks, vectors in fp32.
+ * The two buffers must not overlap.  Asynchronous on `stream`. */
+incvit_status incvit_pack_weights(const incvit_config* cfg, const void* canonical,
+                                  void* packed, void* stream);
+
+/* ----------------------------------------------------------------- handle -- */
+
+/* Validate cfg and bind the packed weights (which must outlive the handle and
+ * not change while it is used).  No device allocation.  On failure *out is
+ * NULL and incvit_last_error(NULL) describes the problem. */
+incvit_status incvit_create(const incvit_config* cfg, const void* packed_weights,
+                            incvit_handle** out);
+
+void incvit_destroy(incvit_handle* h);
+
+/* Bytes of one stream's cache (device layout, 256-byte aligned parts): a header
+ * (magic, config hash, status word), ref [N][D] fp32 (each token's embedding
+ * at its last refresh), X [L+1][N][D] (layer inputs), K and V of every layer,
+ * Y [N][D] (final output).  Base addresses must be 256-byte aligned. */
+size_t incvit_cache_bytes(const incvit_handle* h);
+
+/* Bytes of one stream's cache in the canonical (export) layout:
+ * ref [N][D] fp32, then in the storage dtype X [L+1][N][D], K [L][N][D],
+ * V [L][N][D], Y [N][D]. */
+size_t incvit_cache_canonical_bytes(const incvit_handle* h);
+
+/* Bytes of workspace a call with B streams needs (256-byte aligned base). */
+size_t incvit_workspace_bytes(const incvit_handle* h, int32_t B);
+
+/* ----------------------------------------------------------------- encode -- */
+
+/* Full forward of B frames (the paper's full pass on odd chunks, §III-B):
+ * patches [B][N][P] fp32 (frame pixels, token-major, features (c, dy, dx));
+ * caches: host array of B device pointers, one cache per stream; every cache
+ * row is (re)written and the cache header is initialised for this model.
+ * workspace: incvit_workspace_bytes(h, B) bytes, device. */
+incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patches,
+                                 void* const* caches, void* workspace, void* stream);
+
+/* Incremental encode of B frames (§III-B, eqs. 3-5).  For each stream v:
+ * U_v is selected from this frame's patches against the cache (tau, cap[v]),
+ * rows U_v are recomputed through every layer and written into the cache
+ * (ref, X, K, V, Y); all other rows are left untouched.
+ *   tau: threshold (not NaN; +INFINITY disables it);
+ *   cap: HOST int32[B], each clamped to [0, N];
+ *   idx: device int32 [B][N]; idx[v][0..count[v]) = U_v ascending;
+ *   count: device int32 [B];
+ *   refreshed: device [B][N][D] storage dtype; rows 0..count[v] of stream v
+ *     receive Y[U_v] (the new outputs of the refreshed tokens); may be NULL.
+ * No host synchronisation inside.  A cache that was never full-encoded, or was
+ * encoded by a different model, or a frame whose similarity is NaN, makes that
+ * stream's step a no-op (count = 0) and sets the cache's status word; read it
+ * with incvit_cache_status. */
+incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches,
+                          void* const* caches, float tau, const int32_t* cap,
+                          int32_t* idx, int32_t* count, void* refreshed,
+                          void* workspace, void* stream);
+
+/* ----------------------------------------------------------- cache state -- */
+
+/* Copy a cache into the canonical layout (incvit_cache_canonical_bytes). */
+incvit_status incvit_cache_export(const incvit_handle* h, const void* cache,
+                                  void* canonical_dst, void* stream);
+
+/* Fill a cache from the canonical layout and mark it valid for this model. */
+incvit_status incvit_cache_import(const incvit_handle* h, const void* canonical_src,
+                                  void* cache, void* stream);
+
+/* Synchronises `stream`, then returns the cache's status: INCVIT_OK,
+ * INCVIT_ERR_STATE (never encoded / other model) or INCVIT_ERR_ARG (a step saw
+ * a non-finite similarity). */
+incvit_status incvit_cache_status(const incvit_handle* h, const void* cache, void* stream);
+
+/* Text of the last error on h (or of the last failed create/size query when
+ * h is NULL).  Valid until the next call on h. */
+const char* incvit_last_error(const incvit_handle* h);
+
+/* ------------------------------------------------------------- profiling -- */
+
+/* Kernel kinds for the per-kernel timers. */
+typedef enum {
+  INCVIT_K_EMBED = 0, INCVIT_K_SIM, INCVIT_K_SELECT, INCVIT_K_COMMIT,
+  INCVIT_K_QKV, INCVIT_K_ATTN, INCVIT_K_OPROJ, INCVIT_K_FC1, INCVIT_K_FC2,
+  INCVIT_K_FINAL, INCVIT_K_COUNT
+} incvit_kernel_kind;
+
+/* When enabled, every kernel launch of the encode calls is bracketed by a pair
+ * of hipEvents on the call's stream; incvit_profile_read synchronises those
+ * events and returns, per kind, the summed duration (ms) and the number of
+ * launches since the last reset.  Timing adds event records between kernels,
+ * so measure throughput with profiling off. */
+incvit_status incvit_profile_enable(incvit_handle* h, int32_t enable);
+incvit_status incvit_profile_read(incvit_handle* h, double* total_ms /* [INCVIT_K_COUNT] */,
+                                  int64_t* launches /* [INCVIT_K_COUNT] */, int32_t reset);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* INCVIT_H_ */

@@ -175,35 +175,48 @@ def embed(model: Model, patches: np.ndarray) -> np.ndarray:
     return pinned.embed_f32(patches, w["w_pe"], w["b_pe"], w["pos"])
 
 
+def layer_rows(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
+               trace: Optional[dict] = None) -> np.ndarray:
+    """Layer l for the rows U, whose inputs are Z ([|U|][D]); K, V are the
+    layer's full [N][D] key/value caches.  The new K/V rows of U are written
+    into K, V before the attention, so the updated queries see the new keys of
+    U and the cached keys of the other rows.  Returns the layer's output rows."""
+    m, dt = model.shape, model.dtype
+    D = m.dim
+    A = S(layer_norm(Z, model.p(l, "ln1_g"), model.p(l, "ln1_b"), model.eps), dt)
+    qkv = S(A @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)
+    q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
+    K[U] = k
+    V[U] = v
+    O = S(attention(q, K, V, m.heads), dt)
+    Hres = Z + (O @ model.p(l, "w_o") + model.p(l, "b_o"))
+    if trace is not None:
+        trace.setdefault("O", []).append(O)
+        trace.setdefault("H", []).append(Hres)
+    A2 = S(layer_norm(Hres, model.p(l, "ln2_g"), model.p(l, "ln2_b"), model.eps), dt)
+    G = S(gelu_tanh(A2 @ model.p(l, "w_1") + model.p(l, "b_1")), dt)
+    return S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
+
+
+def final_rows(model: Model, Z: np.ndarray) -> np.ndarray:
+    """Final LayerNorm of the last layer's output rows."""
+    return S(layer_norm(Z, model.w["lnf_g"], model.w["lnf_b"], model.eps), model.dtype)
+
+
 def _encode_rows(model: Model, cache: ViewCache, U: np.ndarray, t0: np.ndarray,
                  trace: Optional[dict] = None) -> None:
     """Recompute rows U through every layer against the cached rows R.
 
-    The caller has already decided U.  K/V rows of U are written before the
-    attention of the layer, so the updated queries see the new keys of U and
-    the cached keys of R.  `trace`, if given, collects the per-layer attention
-    outputs and residuals of the rows U (for tests)."""
-    m, dt = model.shape, model.dtype
-    D, H = m.dim, m.heads
+    The caller has already decided U; the same rows are recomputed in every
+    layer.  `trace`, if given, collects the per-layer attention outputs and
+    residuals of the rows U (for tests)."""
     cache.ref[U] = t0[U]
-    Z = S(t0[U].astype(np.float64), dt)
+    Z = S(t0[U].astype(np.float64), model.dtype)
     cache.X[0][U] = Z
-    for l in range(m.depth):
-        A = S(layer_norm(Z, model.p(l, "ln1_g"), model.p(l, "ln1_b"), model.eps), dt)
-        qkv = S(A @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)
-        q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
-        cache.K[l][U] = k
-        cache.V[l][U] = v
-        O = S(attention(q, cache.K[l], cache.V[l], H), dt)
-        Hres = Z + (O @ model.p(l, "w_o") + model.p(l, "b_o"))
-        if trace is not None:
-            trace.setdefault("O", []).append(O)
-            trace.setdefault("H", []).append(Hres)
-        A2 = S(layer_norm(Hres, model.p(l, "ln2_g"), model.p(l, "ln2_b"), model.eps), dt)
-        G = S(gelu_tanh(A2 @ model.p(l, "w_1") + model.p(l, "b_1")), dt)
-        Z = S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
+    for l in range(model.shape.depth):
+        Z = layer_rows(model, l, Z, U, cache.K[l], cache.V[l], trace)
         cache.X[l + 1][U] = Z
-    cache.Y[U] = S(layer_norm(Z, model.w["lnf_g"], model.w["lnf_b"], model.eps), dt)
+    cache.Y[U] = final_rows(model, Z)
 
 
 def empty_cache(model: Model) -> ViewCache:

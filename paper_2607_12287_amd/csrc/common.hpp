@@ -1,0 +1,303 @@
+// Shared definitions of the incvit HIP library: device layouts, kernel argument
+// structs, launchers and small device helpers.  gfx950 (CDNA4) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace incvit {
+
+constexpr int kMaxViews = 64;
+constexpr int kMaxTokens = 4096;
+constexpr int kMaxDim = 2048;
+constexpr int kMaxHeadDim = 128;
+constexpr uint32_t kCacheMagic = 0x31435649u;  // "IVC1"
+constexpr int kStatusNonFinite = -1;           // a step saw a NaN similarity
+
+// GEMM tiling: a workgroup of 4 waves owns 64 rows x 16 columns; each wave
+// takes every 4th 32-deep K chunk; the 4 partial tiles are summed in a fixed
+// order.  Weights are packed so that one chunk is one 16-byte (bf16) or
+// 32-byte (fp32) load per lane, already in MFMA operand order.
+constexpr int kGemmRows = 64;
+constexpr int kGemmWaves = 4;
+constexpr int kChunkElems = 512;  // 64 lanes x 8 elements
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+struct Shape {
+  int N, P, D, L, H, dh, F, Fpad, Npad;
+  int dtype;  // 0 = fp32, 1 = bf16
+  int eb;     // element bytes of the storage dtype
+  float eps;
+};
+
+// Byte offsets inside one stream's cache.
+struct CacheLayout {
+  size_t ref, x, k, v, y, total;
+  size_t x_layer;   // N*D*eb
+  size_t kv_layer;  // H*Npad*dh*eb
+};
+
+struct CacheHeader {
+  uint32_t magic;
+  uint32_t hash;
+  int32_t status;
+  uint32_t frames;
+  uint32_t pad[60];
+};
+static_assert(sizeof(CacheHeader) == 256, "header is 256 bytes");
+
+struct Views {
+  char* p[kMaxViews];
+};
+
+// Rows of a call: row r of the compact M rows belongs to the view v with
+// off[v] <= r < off[v+1] (off = prefix sum of count) and is token
+// idx[v*N + r - off[v]].
+struct RowMap {
+  const int* count;
+  const int* idx;
+  int B, N;
+};
+
+struct LayerW {
+  const float* ln1_g;
+  const float* ln1_b;
+  const void* w_qkv;
+  const float* b_qkv;
+  const void* w_o;
+  const float* b_o;
+  const float* ln2_g;
+  const float* ln2_b;
+  const void* w_1;
+  const float* b_1;
+  const void* w_2;
+  const float* b_2;
+};
+
+// ---------------------------------------------------------------- kernels --
+
+struct EmbedArgs {
+  const float* patches;  // [B][N][P]
+  const void* w_pe;      // [P][D] storage dtype
+  const float* b_pe;     // [D]
+  const float* pos;      // [N][D]
+  float* t0;             // [B][N][D]
+  int B, N, P, D, dtype;
+  int* zero;             // counters to clear (may be null)
+  int nzero;
+  int* ident_idx;        // if set: idx[v][i] = i, count[v] = N
+  int* ident_count;
+};
+
+struct SimArgs {
+  const float* t0;
+  Views caches;
+  size_t ref_off;
+  float* sim;  // [B][N]
+  int B, N, D;
+};
+
+struct SelectArgs {
+  const float* sim;
+  Views caches;
+  int B, N;
+  float tau;
+  uint32_t hash;
+  int cap[kMaxViews];
+  int* idx;    // [B][N]
+  int* count;  // [B]
+};
+
+struct RowsArgs {  // commit (ref/X0 of refreshed rows) and final LayerNorm
+  RowMap rm;
+  Views caches;
+  CacheLayout cl;
+  Shape sh;
+  const float* t0;
+  const float* g;
+  const float* b;
+  void* refreshed;   // final: optional [B][N][D]
+  int init_header;   // commit of a full encode: write header
+  uint32_t hash;
+};
+
+enum Epi { EPI_QKV = 0, EPI_OPROJ = 1, EPI_FC1 = 2, EPI_FC2 = 3 };
+
+struct GemmArgs {
+  RowMap rm;
+  Views caches;
+  CacheLayout cl;
+  Shape sh;
+  int layer;
+  const void* A;      // OPROJ: O [Mpad][D]; FC1: H f32 [Mpad][D]; FC2: G [Mpad][Fpad]
+  int lda;
+  const float* ln_g;
+  const float* ln_b;
+  const void* W;      // packed [Nout/16][kchunks][512]
+  const float* bias;  // [Nout]
+  int K, kchunks, Nout;
+  int ksplit;
+  int Mpad;
+  float* partial;     // [ksplit][Mpad][Nout] when ksplit > 1
+  int* counters;      // [gridDim.y][gridDim.x]
+  void* out;          // QKV: Q [Mpad][D]; OPROJ: H f32 [Mpad][D]; FC1: G [Mpad][Fpad]
+  int ldo;
+  const float* hres;  // FC2: H f32 [Mpad][D]
+};
+
+struct AttnArgs {
+  RowMap rm;
+  Views caches;
+  CacheLayout cl;
+  Shape sh;
+  int layer;
+  const void* q;  // [Mpad][D]
+  void* o;        // [Mpad][D]
+  float scale_log2;
+  int split;      // 4: one 16-query tile per workgroup, keys split over 4 waves;
+                  // 1: four 16-query tiles per workgroup, one per wave
+};
+
+struct PackArgs {
+  const void* src;  // canonical [K][Ncols] storage dtype
+  void* dst;        // packed
+  int K, Ncols, kchunks, nblocks, dtype;
+};
+
+struct ConvArgs {  // storage dtype vector -> fp32 (with zero padding)
+  const void* src;
+  float* dst;
+  long n, npad;
+  int dtype;
+};
+
+struct ExportArgs {
+  const char* cache;
+  char* canon;
+  CacheLayout cl;
+  Shape sh;
+  int to_canonical;  // 1 export, 0 import
+  uint32_t hash;
+};
+
+// launchers (return the launch error)
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+hipError_t launch_sim(const SimArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
+hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s);
+hipError_t launch_gemm(int epi, const GemmArgs& a, int mmax, size_t lds_bytes, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s);
+hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+hipError_t launch_conv(const ConvArgs& a, hipStream_t s);
+hipError_t launch_export(const ExportArgs& a, hipStream_t s);
+hipError_t gemm_set_lds_limits(size_t bytes);
+
+}  // namespace incvit
+
+// ------------------------------------------------------------ device side --
+#if defined(__HIPCC__)
+namespace incvit {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (inputs are finite here; NaN kept NaN).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <class T> struct Elem;
+template <> struct Elem<uint16_t> {
+  __device__ static float ld(const uint16_t* p, long i) { return bf2f(p[i]); }
+  __device__ static uint16_t cv(float f) { return f2bf(f); }
+  __device__ static float rnd(float f) { return bf2f(f2bf(f)); }
+};
+template <> struct Elem<float> {
+  __device__ static float ld(const float* p, long i) { return p[i]; }
+  __device__ static float cv(float f) { return f; }
+  __device__ static float rnd(float f) { return f; }
+};
+
+// 8 consecutive elements of one lane: one MFMA operand for a 32-deep chunk.
+template <class T> struct V8;
+template <> struct V8<uint16_t> {
+  uint4 v;
+  __device__ void load(const uint16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ void zero() { v = make_uint4(0, 0, 0, 0); }
+};
+template <> struct V8<float> {
+  float4 a, b;
+  __device__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ void zero() { a = make_float4(0, 0, 0, 0); b = a; }
+};
+
+// acc(16x16) += A(16x32) * B(32x16) where lane l holds A[l%16][8*(l/16)+j] and
+// B[8*(l/16)+j][l%16], j = 0..7.  Output lane l holds rows 4*(l/16)+i, col l%16.
+__device__ __forceinline__ void mma(f32x4_t& acc, const V8<uint16_t>& a, const V8<uint16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v),
+                                                __builtin_bit_cast(bf16x8_t, b.v), acc, 0, 0, 0);
+}
+// fp32: eight 16x16x4 products; product j pairs element j of every lane, so
+// the chunk's k = 8*(l/16)+j assignment is the same as for bf16.
+__device__ __forceinline__ void mma(f32x4_t& acc, const V8<float>& a, const V8<float>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.x, b.a.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.y, b.a.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.z, b.a.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.w, b.a.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.x, b.b.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.y, b.b.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.z, b.b.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.b.w, b.b.w, acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+  return x;
+}
+
+// Per-view row offsets (prefix sums of count) into shared memory; returns M.
+__device__ __forceinline__ int row_offsets(const RowMap& rm, int* s_off) {
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int v = 0; v < rm.B; ++v) {
+      s_off[v] = acc;
+      acc += rm.count[v];
+    }
+    s_off[rm.B] = acc;
+  }
+  __syncthreads();
+  return s_off[rm.B];
+}
+
+// Compact row r -> (view, token).
+__device__ __forceinline__ void row_token(const RowMap& rm, const int* s_off, int r, int& v, int& tok) {
+  int vv = 0;
+  while (vv + 1 < rm.B && s_off[vv + 1] <= r) ++vv;
+  v = vv;
+  tok = rm.idx[vv * rm.N + (r - s_off[vv])];
+}
+
+template <class T>
+__device__ __forceinline__ T* x_row(const Views& c, const CacheLayout& cl, const Shape& sh, int v, int layer, int tok) {
+  return reinterpret_cast<T*>(c.p[v] + cl.x + (size_t)layer * cl.x_layer) + (size_t)tok * sh.D;
+}
+
+}  // namespace incvit
+#endif

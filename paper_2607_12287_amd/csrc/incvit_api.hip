@@ -1,0 +1,671 @@
+// C ABI of the incremental ViT encoder: validation, buffer layouts and the
+// launch sequence of one encode call.  The host only enqueues; it never waits
+// for the device inside incvit_full_encode / incvit_step.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+#include "incvit.h"
+
+using namespace incvit;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr size_t kLdsLimit = 160 * 1024;
+constexpr size_t kLdsStatic = 2048;  // static __shared__ of the GEMM kernel (upper bound)
+constexpr int kMaxSplit = 8;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+thread_local std::string g_error;
+
+struct PackedLayer {
+  size_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_1, b_1, w_2, b_2;
+};
+
+struct PackedLayout {
+  size_t w_pe, b_pe, pos, lnf_g, lnf_b, total;
+  std::vector<PackedLayer> layers;
+};
+
+struct CanonLayout {  // element offsets into the canonical buffer
+  size_t w_pe, b_pe, pos, lnf_g, lnf_b, total;
+  std::vector<PackedLayer> layers;
+};
+
+struct WsLayout {
+  size_t counters, count, idx, sim, t0, q, o, h, g, partial, total;
+  int Mpad, ncounters;
+};
+
+enum GemmKind { G_QKV = 0, G_OPROJ = 1, G_FC1 = 2, G_FC2 = 3 };
+
+bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::string& err) {
+  char buf[256];
+  st = INCVIT_ERR_SHAPE;
+  if (!c) { st = INCVIT_ERR_ARG; err = "null config"; return false; }
+  if (c->img_h <= 0 || c->img_w <= 0 || c->channels <= 0 || c->patch <= 0 || c->dim <= 0 ||
+      c->depth <= 0 || c->heads <= 0 || c->mlp_dim <= 0) {
+    err = "config sizes must be positive";
+    return false;
+  }
+  if (c->img_h % c->patch || c->img_w % c->patch) { err = "image size is not a multiple of the patch size"; return false; }
+  if (c->dim % c->heads) { err = "dim is not a multiple of heads"; return false; }
+  if (!(c->ln_eps > 0.0f) || !std::isfinite(c->ln_eps)) { err = "ln_eps must be positive and finite"; return false; }
+  if (c->dtype != INCVIT_F32 && c->dtype != INCVIT_BF16) { st = INCVIT_ERR_UNSUPPORTED; err = "dtype must be INCVIT_F32 or INCVIT_BF16"; return false; }
+  sh.N = (c->img_h / c->patch) * (c->img_w / c->patch);
+  sh.P = c->channels * c->patch * c->patch;
+  sh.D = c->dim;
+  sh.L = c->depth;
+  sh.H = c->heads;
+  sh.dh = c->dim / c->heads;
+  sh.F = c->mlp_dim;
+  sh.Fpad = round_up(c->mlp_dim, 32);
+  sh.Npad = round_up(sh.N, 32);
+  sh.dtype = c->dtype;
+  sh.eb = c->dtype == INCVIT_BF16 ? 2 : 4;
+  sh.eps = c->ln_eps;
+  st = INCVIT_ERR_UNSUPPORTED;
+  if (sh.D % 32) { err = "dim must be a multiple of 32"; return false; }
+  if (sh.D > kMaxDim) { snprintf(buf, sizeof buf, "dim must be <= %d", kMaxDim); err = buf; return false; }
+  if (sh.dh % 8 || sh.dh > kMaxHeadDim) { err = "head dim must be a multiple of 8 and <= 128"; return false; }
+  if (sh.N > kMaxTokens) { snprintf(buf, sizeof buf, "at most %d tokens", kMaxTokens); err = buf; return false; }
+  if (c->max_streams < 1 || c->max_streams > kMaxViews) { snprintf(buf, sizeof buf, "max_streams must be in [1, %d]", kMaxViews); err = buf; return false; }
+  st = INCVIT_OK;
+  return true;
+}
+
+size_t packed_gemm_bytes(int K, int Ncols, int eb) {
+  return (size_t)(round_up(Ncols, 16) / 16) * (size_t)(round_up(K, 32) / 32) * kChunkElems * eb;
+}
+
+PackedLayout packed_layout(const Shape& sh) {
+  PackedLayout p;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+  const int D = sh.D, eb = sh.eb;
+  p.w_pe = take((size_t)sh.P * D * eb);
+  p.b_pe = take((size_t)D * 4);
+  p.pos = take((size_t)sh.N * D * 4);
+  for (int l = 0; l < sh.L; ++l) {
+    PackedLayer L;
+    L.ln1_g = take(D * 4);
+    L.ln1_b = take(D * 4);
+    L.w_qkv = take(packed_gemm_bytes(D, 3 * D, eb));
+    L.b_qkv = take(3 * D * 4);
+    L.w_o = take(packed_gemm_bytes(D, D, eb));
+    L.b_o = take(D * 4);
+    L.ln2_g = take(D * 4);
+    L.ln2_b = take(D * 4);
+    L.w_1 = take(packed_gemm_bytes(D, sh.Fpad, eb));
+    L.b_1 = take((size_t)sh.Fpad * 4);
+    L.w_2 = take(packed_gemm_bytes(sh.Fpad, D, eb));
+    L.b_2 = take(D * 4);
+    p.layers.push_back(L);
+  }
+  p.lnf_g = take(D * 4);
+  p.lnf_b = take(D * 4);
+  p.total = off;
+  return p;
+}
+
+CanonLayout canon_layout(const Shape& sh) {
+  CanonLayout c;
+  size_t off = 0;
+  auto take = [&](size_t n) { size_t o = off; off += n; return o; };
+  const size_t D = sh.D, F = sh.F;
+  c.w_pe = take((size_t)sh.P * D);
+  c.b_pe = take(D);
+  c.pos = take((size_t)sh.N * D);
+  for (int l = 0; l < sh.L; ++l) {
+    PackedLayer L;
+    L.ln1_g = take(D);
+    L.ln1_b = take(D);
+    L.w_qkv = take(D * 3 * D);
+    L.b_qkv = take(3 * D);
+    L.w_o = take(D * D);
+    L.b_o = take(D);
+    L.ln2_g = take(D);
+    L.ln2_b = take(D);
+    L.w_1 = take(D * F);
+    L.b_1 = take(F);
+    L.w_2 = take(F * D);
+    L.b_2 = take(D);
+    c.layers.push_back(L);
+  }
+  c.lnf_g = take(D);
+  c.lnf_b = take(D);
+  c.total = off;
+  return c;
+}
+
+CacheLayout cache_layout(const Shape& sh) {
+  CacheLayout cl;
+  size_t off = kAlign;  // header
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+  cl.x_layer = (size_t)sh.N * sh.D * sh.eb;
+  cl.kv_layer = (size_t)sh.H * sh.Npad * sh.dh * sh.eb;
+  cl.ref = take((size_t)sh.N * sh.D * 4);
+  cl.x = take(cl.x_layer * (sh.L + 1));
+  cl.k = take(cl.kv_layer * sh.L);
+  cl.v = take(cl.kv_layer * sh.L);
+  cl.y = take(cl.x_layer);
+  cl.total = off;
+  return cl;
+}
+
+uint32_t config_hash(const incvit_config& c) {
+  const int32_t f[10] = {c.img_h, c.img_w, c.channels, c.patch, c.dim, c.depth, c.heads, c.mlp_dim, c.dtype, 0};
+  uint32_t h = 2166136261u;
+  auto mix = [&](uint32_t x) {
+    for (int i = 0; i < 4; ++i) {
+      h ^= (x >> (8 * i)) & 0xffu;
+      h *= 16777619u;
+    }
+  };
+  for (int i = 0; i < 9; ++i) mix((uint32_t)f[i]);
+  uint32_t e;
+  memcpy(&e, &c.ln_eps, 4);
+  mix(e);
+  return h == 0 ? 1u : h;
+}
+
+struct GemmGeom {
+  int K, kchunks, Nout, nblocks;
+};
+
+GemmGeom gemm_geom(const Shape& sh, int kind) {
+  GemmGeom g;
+  switch (kind) {
+    case G_QKV: g.K = sh.D; g.Nout = 3 * sh.D; break;
+    case G_OPROJ: g.K = sh.D; g.Nout = sh.D; break;
+    case G_FC1: g.K = sh.D; g.Nout = sh.Fpad; break;
+    default: g.K = sh.Fpad; g.Nout = sh.D; break;
+  }
+  g.kchunks = round_up(g.K, 32) / 32;
+  g.nblocks = g.Nout / 16;
+  return g;
+}
+
+// Split of K over workgroups: enough to fit the A block in LDS, and enough
+// workgroups to keep the chip busy when there are few rows.
+int choose_ksplit(const Shape& sh, const GemmGeom& g, int mmax) {
+  const size_t per_row = (kLdsLimit - kLdsStatic) / kGemmRows;
+  const int max_chunks = (int)((per_row - 16) / sh.eb / 32);
+  const int ks_lds = (g.kchunks + max_chunks - 1) / max_chunks;
+  const int gy = std::max(1, (mmax + kGemmRows - 1) / kGemmRows);
+  const int ks_occ = (200 + g.nblocks * gy - 1) / (g.nblocks * gy);
+  int ks = std::min(ks_occ, std::max(1, g.kchunks / 4));
+  ks = std::max(ks, ks_lds);
+  return std::min(std::max(ks, 1), std::max(kMaxSplit, ks_lds));
+}
+
+size_t gemm_lds(const Shape& sh, const GemmGeom& g, int ks) {
+  const int chunks = (g.kchunks + ks - 1) / ks;
+  const size_t a = (size_t)kGemmRows * ((size_t)chunks * 32 * sh.eb + 16);
+  return std::max(a, (size_t)kGemmWaves * 4 * 64 * 16);
+}
+
+WsLayout ws_layout(const Shape& sh, int B) {
+  WsLayout w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
+  const int M = B * sh.N;
+  w.Mpad = round_up(std::max(M, 1), kGemmRows);
+  int maxN = 0;
+  size_t part = 0;
+  for (int k = 0; k < 4; ++k) {
+    const GemmGeom g = gemm_geom(sh, k);
+    maxN = std::max(maxN, g.Nout);
+    const int ks = std::max(choose_ksplit(sh, g, 1), choose_ksplit(sh, g, w.Mpad));
+    if (ks > 1) part = std::max(part, (size_t)ks * w.Mpad * g.Nout);
+  }
+  w.ncounters = (w.Mpad / kGemmRows) * (maxN / 16);
+  w.counters = take((size_t)w.ncounters * 4);
+  w.count = take(kMaxViews * 4);
+  w.idx = take((size_t)M * 4);
+  w.sim = take((size_t)M * 4);
+  w.t0 = take((size_t)M * sh.D * 4);
+  w.q = take((size_t)w.Mpad * sh.D * sh.eb);
+  w.o = take((size_t)w.Mpad * sh.D * sh.eb);
+  w.h = take((size_t)w.Mpad * sh.D * 4);
+  w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
+  w.partial = take(part * 4);
+  w.total = off;
+  return w;
+}
+
+}  // namespace
+
+struct incvit_handle {
+  incvit_config cfg;
+  Shape sh;
+  CacheLayout cl;
+  uint32_t hash;
+  const char* packed;
+  PackedLayout pl;
+  std::string err;
+  bool prof = false;
+  struct Rec {
+    int kind;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  double prof_ms[INCVIT_K_COUNT] = {};
+  int64_t prof_n[INCVIT_K_COUNT] = {};
+};
+
+namespace {
+
+incvit_status fail(incvit_handle* h, incvit_status st, const std::string& msg) {
+  if (h) h->err = msg;
+  else g_error = msg;
+  return st;
+}
+
+hipEvent_t take_event(incvit_handle* h) {
+  if (!h->pool.empty()) {
+    hipEvent_t e = h->pool.back();
+    h->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+incvit_status run(incvit_handle* h, int kind, hipStream_t s, F&& launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (h->prof) {
+    e0 = take_event(h);
+    e1 = take_event(h);
+    if (e0) hipEventRecord(e0, s);
+  }
+  const hipError_t err = launch();
+  if (h->prof && e0 && e1) {
+    hipEventRecord(e1, s);
+    h->recs.push_back({kind, e0, e1});
+  }
+  if (err != hipSuccess) {
+    char buf[256];
+    snprintf(buf, sizeof buf, "kernel launch failed (kind %d): %s", kind, hipGetErrorString(err));
+    return fail(h, INCVIT_ERR_HIP, buf);
+  }
+  return INCVIT_OK;
+}
+
+const float* fptr(const incvit_handle* h, size_t off) { return reinterpret_cast<const float*>(h->packed + off); }
+
+// Launch the per-layer kernels for rows described by rm.
+incvit_status run_layers(incvit_handle* h, const RowMap& rm, const Views& views, const WsLayout& wl,
+                         char* ws, int mmax, int max_rows_per_view, bool step, hipStream_t s) {
+  const Shape& sh = h->sh;
+  for (int l = 0; l < sh.L; ++l) {
+    const PackedLayer& P = h->pl.layers[l];
+    GemmArgs ga;
+    memset(&ga, 0, sizeof ga);
+    ga.rm = rm;
+    ga.caches = views;
+    ga.cl = h->cl;
+    ga.sh = sh;
+    ga.layer = l;
+    ga.Mpad = wl.Mpad;
+    ga.partial = reinterpret_cast<float*>(ws + wl.partial);
+    ga.counters = reinterpret_cast<int*>(ws + wl.counters);
+
+    auto gemm = [&](int kind, int epi, int kernel_kind) -> incvit_status {
+      const GemmGeom g = gemm_geom(sh, kind);
+      GemmArgs a = ga;
+      a.K = g.K;
+      a.kchunks = g.kchunks;
+      a.Nout = g.Nout;
+      a.ksplit = choose_ksplit(sh, g, mmax);
+      const size_t lds = gemm_lds(sh, g, a.ksplit);
+      switch (kind) {
+        case G_QKV:
+          a.ln_g = fptr(h, P.ln1_g); a.ln_b = fptr(h, P.ln1_b);
+          a.W = h->packed + P.w_qkv; a.bias = fptr(h, P.b_qkv);
+          a.out = ws + wl.q; a.ldo = sh.D;
+          break;
+        case G_OPROJ:
+          a.A = ws + wl.o; a.lda = sh.D;
+          a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
+          a.out = ws + wl.h; a.ldo = sh.D;
+          break;
+        case G_FC1:
+          a.A = ws + wl.h; a.lda = sh.D;
+          a.ln_g = fptr(h, P.ln2_g); a.ln_b = fptr(h, P.ln2_b);
+          a.W = h->packed + P.w_1; a.bias = fptr(h, P.b_1);
+          a.out = ws + wl.g; a.ldo = sh.Fpad;
+          break;
+        default:
+          a.A = ws + wl.g; a.lda = sh.Fpad;
+          a.W = h->packed + P.w_2; a.bias = fptr(h, P.b_2);
+          a.hres = reinterpret_cast<const float*>(ws + wl.h);
+          break;
+      }
+      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, a, mmax, lds, s); });
+    };
+
+    incvit_status st;
+    if ((st = gemm(G_QKV, EPI_QKV, INCVIT_K_QKV)) != INCVIT_OK) return st;
+    AttnArgs aa;
+    memset(&aa, 0, sizeof aa);
+    aa.rm = rm;
+    aa.caches = views;
+    aa.cl = h->cl;
+    aa.sh = sh;
+    aa.layer = l;
+    aa.q = ws + wl.q;
+    aa.o = ws + wl.o;
+    aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
+    aa.split = step ? 4 : 1;
+    if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, s); })) != INCVIT_OK) return st;
+    if ((st = gemm(G_OPROJ, EPI_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
+    if ((st = gemm(G_FC1, EPI_FC1, INCVIT_K_FC1)) != INCVIT_OK) return st;
+    if ((st = gemm(G_FC2, EPI_FC2, INCVIT_K_FC2)) != INCVIT_OK) return st;
+  }
+  return INCVIT_OK;
+}
+
+incvit_status check_views(incvit_handle* h, int32_t B, void* const* caches, Views& views) {
+  if (!caches) return fail(h, INCVIT_ERR_ARG, "caches is null");
+  memset(&views, 0, sizeof views);
+  for (int v = 0; v < B; ++v) {
+    if (!caches[v]) return fail(h, INCVIT_ERR_ARG, "a cache pointer is null");
+    if (reinterpret_cast<uintptr_t>(caches[v]) % kAlign) return fail(h, INCVIT_ERR_ARG, "cache pointers must be 256-byte aligned");
+    views.p[v] = static_cast<char*>(caches[v]);
+  }
+  return INCVIT_OK;
+}
+
+incvit_status check_common(incvit_handle* h, int32_t B, const float* patches, void* ws) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  if (B < 1 || B > h->cfg.max_streams) return fail(h, INCVIT_ERR_ARG, "B must be in [1, max_streams]");
+  if (!patches) return fail(h, INCVIT_ERR_ARG, "patches is null");
+  if (reinterpret_cast<uintptr_t>(patches) % 16) return fail(h, INCVIT_ERR_ARG, "patches must be 16-byte aligned");
+  if (!ws) return fail(h, INCVIT_ERR_ARG, "workspace is null");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(h, INCVIT_ERR_ARG, "workspace must be 256-byte aligned");
+  return INCVIT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t incvit_canonical_weights_bytes(const incvit_config* cfg) {
+  Shape sh;
+  incvit_status st;
+  std::string err;
+  if (!make_shape(cfg, sh, st, err)) { g_error = err; return 0; }
+  return canon_layout(sh).total * sh.eb;
+}
+
+size_t incvit_packed_weights_bytes(const incvit_config* cfg) {
+  Shape sh;
+  incvit_status st;
+  std::string err;
+  if (!make_shape(cfg, sh, st, err)) { g_error = err; return 0; }
+  return packed_layout(sh).total;
+}
+
+incvit_status incvit_pack_weights(const incvit_config* cfg, const void* canonical, void* packed, void* stream) {
+  Shape sh;
+  incvit_status st;
+  std::string err;
+  if (!make_shape(cfg, sh, st, err)) return fail(nullptr, st, err);
+  if (!canonical || !packed) return fail(nullptr, INCVIT_ERR_ARG, "null weight buffer");
+  if (reinterpret_cast<uintptr_t>(packed) % kAlign || reinterpret_cast<uintptr_t>(canonical) % 16)
+    return fail(nullptr, INCVIT_ERR_ARG, "packed must be 256-byte and canonical 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const PackedLayout pl = packed_layout(sh);
+  const CanonLayout cn = canon_layout(sh);
+  const char* src = static_cast<const char*>(canonical);
+  char* dst = static_cast<char*>(packed);
+  const size_t eb = sh.eb;
+  hipError_t e = hipSuccess;
+  auto conv = [&](size_t coff, size_t poff, long n, long npad) {
+    if (e != hipSuccess) return;
+    ConvArgs a{src + coff * eb, reinterpret_cast<float*>(dst + poff), n, npad, sh.dtype};
+    e = launch_conv(a, s);
+  };
+  auto pack = [&](size_t coff, size_t poff, int K, int Ncols, int Kpad, int Npadc) {
+    if (e != hipSuccess) return;
+    PackArgs a{src + coff * eb, dst + poff, K, Ncols, round_up(Kpad, 32) / 32, round_up(Npadc, 16) / 16, sh.dtype};
+    e = launch_pack(a, s);
+  };
+  const int D = sh.D;
+  e = hipMemcpyAsync(dst + pl.w_pe, src + cn.w_pe * eb, (size_t)sh.P * D * eb, hipMemcpyDeviceToDevice, s);
+  conv(cn.b_pe, pl.b_pe, D, D);
+  conv(cn.pos, pl.pos, (long)sh.N * D, (long)sh.N * D);
+  for (int l = 0; l < sh.L; ++l) {
+    const PackedLayer& C = cn.layers[l];
+    const PackedLayer& P = pl.layers[l];
+    conv(C.ln1_g, P.ln1_g, D, D);
+    conv(C.ln1_b, P.ln1_b, D, D);
+    pack(C.w_qkv, P.w_qkv, D, 3 * D, D, 3 * D);
+    conv(C.b_qkv, P.b_qkv, 3 * D, 3 * D);
+    pack(C.w_o, P.w_o, D, D, D, D);
+    conv(C.b_o, P.b_o, D, D);
+    conv(C.ln2_g, P.ln2_g, D, D);
+    conv(C.ln2_b, P.ln2_b, D, D);
+    pack(C.w_1, P.w_1, D, sh.F, D, sh.Fpad);
+    conv(C.b_1, P.b_1, sh.F, sh.Fpad);
+    pack(C.w_2, P.w_2, sh.F, D, sh.Fpad, D);
+    conv(C.b_2, P.b_2, D, D);
+  }
+  conv(cn.lnf_g, pl.lnf_g, D, D);
+  conv(cn.lnf_b, pl.lnf_b, D, D);
+  if (e != hipSuccess) return fail(nullptr, INCVIT_ERR_HIP, std::string("pack: ") + hipGetErrorString(e));
+  return INCVIT_OK;
+}
+
+incvit_status incvit_create(const incvit_config* cfg, const void* packed_weights, incvit_handle** out) {
+  if (!out) return fail(nullptr, INCVIT_ERR_ARG, "out is null");
+  *out = nullptr;
+  Shape sh;
+  incvit_status st;
+  std::string err;
+  if (!make_shape(cfg, sh, st, err)) return fail(nullptr, st, err);
+  if (!packed_weights || reinterpret_cast<uintptr_t>(packed_weights) % kAlign)
+    return fail(nullptr, INCVIT_ERR_ARG, "packed weights must be non-null and 256-byte aligned");
+  const hipError_t e = gemm_set_lds_limits(kLdsLimit - kLdsStatic);
+  if (e != hipSuccess) return fail(nullptr, INCVIT_ERR_HIP, std::string("hipFuncSetAttribute: ") + hipGetErrorString(e));
+  incvit_handle* h = new incvit_handle();
+  h->cfg = *cfg;
+  h->sh = sh;
+  h->cl = cache_layout(sh);
+  h->hash = config_hash(*cfg);
+  h->packed = static_cast<const char*>(packed_weights);
+  h->pl = packed_layout(sh);
+  *out = h;
+  return INCVIT_OK;
+}
+
+void incvit_destroy(incvit_handle* h) {
+  if (!h) return;
+  for (auto& r : h->recs) {
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+  }
+  for (auto e : h->pool) hipEventDestroy(e);
+  delete h;
+}
+
+size_t incvit_cache_bytes(const incvit_handle* h) { return h ? h->cl.total : 0; }
+
+size_t incvit_cache_canonical_bytes(const incvit_handle* h) {
+  if (!h) return 0;
+  const Shape& sh = h->sh;
+  const size_t nd = (size_t)sh.N * sh.D;
+  return nd * 4 + ((size_t)(sh.L + 1) * nd + 2 * (size_t)sh.L * nd + nd) * sh.eb;
+}
+
+size_t incvit_workspace_bytes(const incvit_handle* h, int32_t B) {
+  if (!h || B < 1 || B > h->cfg.max_streams) return 0;
+  return ws_layout(h->sh, B).total;
+}
+
+incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patches, void* const* caches,
+                                 void* workspace, void* stream) {
+  incvit_status st = check_common(h, B, patches, workspace);
+  if (st != INCVIT_OK) return st;
+  Views views;
+  if ((st = check_views(h, B, caches, views)) != INCVIT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Shape& sh = h->sh;
+  char* ws = static_cast<char*>(workspace);
+  const WsLayout wl = ws_layout(sh, B);
+  int* count = reinterpret_cast<int*>(ws + wl.count);
+  int* idx = reinterpret_cast<int*>(ws + wl.idx);
+  float* t0 = reinterpret_cast<float*>(ws + wl.t0);
+
+  EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
+               B, sh.N, sh.P, sh.D, sh.dtype, reinterpret_cast<int*>(ws + wl.counters), wl.ncounters, idx, count};
+  if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
+  const RowMap rm{count, idx, B, sh.N};
+  const int mmax = B * sh.N;
+  RowsArgs ra;
+  memset(&ra, 0, sizeof ra);
+  ra.rm = rm;
+  ra.caches = views;
+  ra.cl = h->cl;
+  ra.sh = sh;
+  ra.t0 = t0;
+  ra.init_header = 1;
+  ra.hash = h->hash;
+  if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
+  if ((st = run_layers(h, rm, views, wl, ws, mmax, sh.N, false, s)) != INCVIT_OK) return st;
+  ra.init_header = 0;
+  ra.g = fptr(h, h->pl.lnf_g);
+  ra.b = fptr(h, h->pl.lnf_b);
+  ra.refreshed = nullptr;
+  return run(h, INCVIT_K_FINAL, s, [&] { return launch_final(ra, mmax, s); });
+}
+
+incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, void* const* caches, float tau,
+                          const int32_t* cap, int32_t* idx, int32_t* count, void* refreshed, void* workspace,
+                          void* stream) {
+  incvit_status st = check_common(h, B, patches, workspace);
+  if (st != INCVIT_OK) return st;
+  if (std::isnan(tau)) return fail(h, INCVIT_ERR_ARG, "tau is NaN");
+  if (!cap) return fail(h, INCVIT_ERR_ARG, "cap is null");
+  if (!idx || !count) return fail(h, INCVIT_ERR_ARG, "idx and count must be non-null");
+  if (reinterpret_cast<uintptr_t>(refreshed) % 16) return fail(h, INCVIT_ERR_ARG, "refreshed must be 16-byte aligned");
+  Views views;
+  if ((st = check_views(h, B, caches, views)) != INCVIT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Shape& sh = h->sh;
+  char* ws = static_cast<char*>(workspace);
+  const WsLayout wl = ws_layout(sh, B);
+  float* t0 = reinterpret_cast<float*>(ws + wl.t0);
+  float* sim = reinterpret_cast<float*>(ws + wl.sim);
+
+  SelectArgs sa;
+  memset(&sa, 0, sizeof sa);
+  int mmax = 0, max_rows = 0;
+  for (int v = 0; v < B; ++v) {
+    const int c = std::min(std::max(cap[v], 0), sh.N);
+    sa.cap[v] = c;
+    mmax += c;
+    max_rows = std::max(max_rows, c);
+  }
+  EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
+               B, sh.N, sh.P, sh.D, sh.dtype, reinterpret_cast<int*>(ws + wl.counters), wl.ncounters, nullptr, nullptr};
+  if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
+  SimArgs si{t0, views, h->cl.ref, sim, B, sh.N, sh.D};
+  if ((st = run(h, INCVIT_K_SIM, s, [&] { return launch_sim(si, s); })) != INCVIT_OK) return st;
+  sa.sim = sim;
+  sa.caches = views;
+  sa.B = B;
+  sa.N = sh.N;
+  sa.tau = tau;
+  sa.hash = h->hash;
+  sa.idx = idx;
+  sa.count = count;
+  if ((st = run(h, INCVIT_K_SELECT, s, [&] { return launch_select(sa, s); })) != INCVIT_OK) return st;
+  if (mmax == 0) return INCVIT_OK;
+
+  const RowMap rm{count, idx, B, sh.N};
+  RowsArgs ra;
+  memset(&ra, 0, sizeof ra);
+  ra.rm = rm;
+  ra.caches = views;
+  ra.cl = h->cl;
+  ra.sh = sh;
+  ra.t0 = t0;
+  if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
+  if ((st = run_layers(h, rm, views, wl, ws, mmax, max_rows, true, s)) != INCVIT_OK) return st;
+  ra.g = fptr(h, h->pl.lnf_g);
+  ra.b = fptr(h, h->pl.lnf_b);
+  ra.refreshed = refreshed;
+  return run(h, INCVIT_K_FINAL, s, [&] { return launch_final(ra, mmax, s); });
+}
+
+incvit_status incvit_cache_export(const incvit_handle* h, const void* cache, void* canonical_dst, void* stream) {
+  if (!h || !cache || !canonical_dst) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_ARG, "null argument");
+  ExportArgs a{static_cast<const char*>(cache), static_cast<char*>(canonical_dst), h->cl, h->sh, 1, h->hash};
+  const hipError_t e = launch_export(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_HIP, hipGetErrorString(e));
+  return INCVIT_OK;
+}
+
+incvit_status incvit_cache_import(const incvit_handle* h, const void* canonical_src, void* cache, void* stream) {
+  if (!h || !cache || !canonical_src) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_ARG, "null argument");
+  ExportArgs a{static_cast<char*>(cache), static_cast<char*>(const_cast<void*>(canonical_src)), h->cl, h->sh, 0, h->hash};
+  const hipError_t e = launch_export(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_HIP, hipGetErrorString(e));
+  return INCVIT_OK;
+}
+
+incvit_status incvit_cache_status(const incvit_handle* h, const void* cache, void* stream) {
+  if (!h || !cache) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_ARG, "null argument");
+  CacheHeader hdr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(&hdr, cache, sizeof hdr, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_HIP, hipGetErrorString(e));
+  if (hdr.magic != kCacheMagic || hdr.hash != h->hash) return INCVIT_ERR_STATE;
+  if (hdr.status == kStatusNonFinite) return INCVIT_ERR_ARG;
+  return hdr.status == 0 ? INCVIT_OK : INCVIT_ERR_STATE;
+}
+
+const char* incvit_last_error(const incvit_handle* h) { return h ? h->err.c_str() : g_error.c_str(); }
+
+incvit_status incvit_profile_enable(incvit_handle* h, int32_t enable) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  h->prof = enable != 0;
+  return INCVIT_OK;
+}
+
+incvit_status incvit_profile_read(incvit_handle* h, double* total_ms, int64_t* launches, int32_t reset) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  for (auto& r : h->recs) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return fail(h, INCVIT_ERR_HIP, hipGetErrorString(e));
+    h->prof_ms[r.kind] += ms;
+    h->prof_n[r.kind] += 1;
+    h->pool.push_back(r.a);
+    h->pool.push_back(r.b);
+  }
+  h->recs.clear();
+  for (int k = 0; k < INCVIT_K_COUNT; ++k) {
+    if (total_ms) total_ms[k] = h->prof_ms[k];
+    if (launches) launches[k] = h->prof_n[k];
+    if (reset) {
+      h->prof_ms[k] = 0.0;
+      h->prof_n[k] = 0;
+    }
+  }
+  return INCVIT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,264 @@
+// Token selection (paper §III-B: the least similar tokens are updated, chosen
+// once before the first layer) and the per-row kernels around the layers.
+//
+// select: U = {i : sim_i < tau} (strict); if |U| > cap keep the cap lowest
+// similarities, equal similarities going to the lower index; write U ascending.
+// The cap-th smallest key is found by an exact 4-pass radix select over the
+// order-preserving integer image of the fp32 similarity, so the result is a
+// pure function of the similarities.
+#include "common.hpp"
+
+namespace incvit {
+
+constexpr int kSelThreads = 1024;
+
+__device__ __forceinline__ uint32_t order_key(float s) {
+  if (s == 0.0f) s = 0.0f;  // -0 and +0 compare equal
+  const uint32_t u = __float_as_uint(s);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Exclusive scan of one int per thread over the workgroup (in thread order).
+__device__ int block_exclusive_scan(int x, int* s_wave, int& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int incl = x;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) s_wave[w] = incl;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int i = 0; i < nw; ++i) {
+      const int t = s_wave[i];
+      s_wave[i] = acc;
+      acc += t;
+    }
+    s_wave[nw] = acc;
+  }
+  __syncthreads();
+  const int res = s_wave[w] + incl - x;
+  total = s_wave[nw];
+  __syncthreads();
+  return res;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
+  __shared__ uint32_t skey[kMaxTokens];
+  __shared__ int s_hist[256];
+  __shared__ int s_wave[kSelThreads / 64 + 1];
+  __shared__ int s_misc[4];
+  const int v = blockIdx.x, tid = threadIdx.x, N = a.N;
+  CacheHeader* hdr = reinterpret_cast<CacheHeader*>(a.caches.p[v]);
+  if (tid == 0) {
+    s_misc[0] = (hdr->magic == kCacheMagic && hdr->hash == a.hash && hdr->status == 0) ? 1 : 0;
+    s_misc[1] = 0;  // non-finite seen
+    s_misc[2] = 0;  // candidates
+  }
+  __syncthreads();
+  if (!s_misc[0]) {
+    if (tid == 0) a.count[v] = 0;
+    return;
+  }
+  // contiguous token segment per thread (keeps scans in index order)
+  const int per = (N + kSelThreads - 1) / kSelThreads;
+  const int i0 = min(N, tid * per), i1 = min(N, i0 + per);
+  int cand = 0, bad = 0;
+  for (int i = i0; i < i1; ++i) {
+    const float s = a.sim[(size_t)v * N + i];
+    bad |= (s != s);
+    const bool f = s < a.tau;
+    skey[i] = f ? order_key(s) : 0xffffffffu;
+    cand += f;
+  }
+  if (bad) atomicOr(&s_misc[1], 1);
+  atomicAdd(&s_misc[2], cand);
+  __syncthreads();
+  if (s_misc[1]) {
+    if (tid == 0) {
+      hdr->status = kStatusNonFinite;
+      a.count[v] = 0;
+    }
+    return;
+  }
+  const int total = s_misc[2];
+  const int cap = min(max(a.cap[v], 0), N);
+
+  uint32_t thr = 0xffffffffu;  // keys < thr are taken, keys == thr by index
+  int need_eq = 0;
+  if (total > cap) {
+    if (cap == 0) {
+      thr = 0;
+      need_eq = 0;
+    } else {
+      uint32_t prefix = 0;
+      int kth = cap;  // 1-based rank of the wanted key among the remaining
+      for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        for (int b = tid; b < 256; b += kSelThreads) s_hist[b] = 0;
+        __syncthreads();
+        for (int i = i0; i < i1; ++i) {
+          const uint32_t k = skey[i];
+          if (k == 0xffffffffu) continue;
+          if (pass > 0 && (k >> (shift + 8)) != (prefix >> (shift + 8))) continue;
+          atomicAdd(&s_hist[(k >> shift) & 255u], 1);
+        }
+        __syncthreads();
+        if (tid < 64) {  // wave 0 finds the digit holding the kth key
+          const int lane = tid;
+          int loc[4], sum = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            loc[j] = s_hist[4 * lane + j];
+            sum += loc[j];
+          }
+          int incl = sum;
+#pragma unroll
+          for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += y;
+          }
+          int before = incl - sum;
+          for (int j = 0; j < 4; ++j) {
+            if (before < kth && kth <= before + loc[j]) {
+              s_misc[3] = 4 * lane + j;
+              s_wave[0] = before;  // reuse as scratch; consumed below
+            }
+            before += loc[j];
+          }
+        }
+        __syncthreads();
+        const int digit = s_misc[3];
+        kth -= s_wave[0];
+        prefix |= (uint32_t)digit << shift;
+        __syncthreads();
+      }
+      thr = prefix;
+      need_eq = kth;
+    }
+  }
+
+  // Ties at thr are taken in index order: a tie is taken iff the number of
+  // ties before it is < need_eq.  Both scans run over contiguous segments, so
+  // thread order is index order.
+  const bool has_thr = thr != 0xffffffffu;
+  int eq = 0;
+  for (int i = i0; i < i1; ++i) eq += (has_thr && skey[i] == thr);
+  int eq_total;
+  const int eq_before = block_exclusive_scan(eq, s_wave, eq_total);
+  int sel = 0;
+  {
+    int e = eq_before;
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t k = skey[i];
+      if (k == 0xffffffffu) continue;
+      if (k < thr) ++sel;
+      else if (k == thr) sel += (e++ < need_eq);
+    }
+  }
+  int total_sel;
+  int pos = block_exclusive_scan(sel, s_wave, total_sel);
+  {
+    int e = eq_before;
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t k = skey[i];
+      if (k == 0xffffffffu) continue;
+      bool take = k < thr;
+      if (k == thr) take = (e++ < need_eq);
+      if (take) a.idx[(size_t)v * N + pos++] = i;
+    }
+  }
+  if (tid == 0) a.count[v] = total_sel;
+}
+
+// One wave per compact row: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]).
+template <class T>
+__global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
+  __shared__ int s_off[kMaxViews + 1];
+  const int M = row_offsets(a.rm, s_off);
+  if (a.init_header && blockIdx.x == 0 && threadIdx.x < a.rm.B) {
+    CacheHeader* hdr = reinterpret_cast<CacheHeader*>(a.caches.p[threadIdx.x]);
+    hdr->magic = kCacheMagic;
+    hdr->hash = a.hash;
+    hdr->status = 0;
+    hdr->frames = 0;
+  }
+  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= M) return;
+  int v, tok;
+  row_token(a.rm, s_off, r, v, tok);
+  const int D = a.sh.D;
+  const float* src = a.t0 + ((size_t)v * a.rm.N + tok) * D;
+  float* ref = reinterpret_cast<float*>(a.caches.p[v] + a.cl.ref) + (size_t)tok * D;
+  T* x0 = x_row<T>(a.caches, a.cl, a.sh, v, 0, tok);
+  for (int d = lane; d < D; d += 64) {
+    const float t = src[d];
+    ref[d] = t;
+    x0[d] = Elem<T>::cv(t);
+  }
+}
+
+// One wave per compact row: Y[tok] = S(LN_f(X^L[tok])); refreshed[v][j] = Y[tok].
+template <class T>
+__global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
+  __shared__ int s_off[kMaxViews + 1];
+  const int M = row_offsets(a.rm, s_off);
+  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= M) return;
+  int v, tok;
+  row_token(a.rm, s_off, r, v, tok);
+  const int D = a.sh.D;
+  const T* x = x_row<T>(a.caches, a.cl, a.sh, v, a.sh.L, tok);
+  constexpr int kMaxPer = kMaxDim / 64;
+  float vals[kMaxPer];
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kMaxPer; ++j) {
+    const int d = lane + 64 * j;
+    vals[j] = d < D ? Elem<T>::ld(x, d) : 0.0f;
+    s += vals[j];
+  }
+  const float mean = wave_sum(s) / (float)D;
+  float q = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kMaxPer; ++j) {
+    const int d = lane + 64 * j;
+    const float c = vals[j] - mean;
+    q += d < D ? c * c : 0.0f;
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + a.sh.eps);
+  T* y = reinterpret_cast<T*>(a.caches.p[v] + a.cl.y) + (size_t)tok * D;
+  T* out = a.refreshed ? reinterpret_cast<T*>(a.refreshed) + ((size_t)v * a.rm.N + (r - s_off[v])) * D : nullptr;
+#pragma unroll
+  for (int j = 0; j < kMaxPer; ++j) {
+    const int d = lane + 64 * j;
+    if (d < D) {
+      const T o = Elem<T>::cv((vals[j] - mean) * rstd * a.g[d] + a.b[d]);
+      y[d] = o;
+      if (out) out[d] = o;
+    }
+  }
+}
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(select_kernel, dim3(a.B), dim3(kSelThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s) {
+  dim3 grid(max(1, (mmax + 3) / 4));
+  if (a.sh.dtype) hipLaunchKernelGGL(commit_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(commit_kernel<float>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s) {
+  dim3 grid(max(1, (mmax + 3) / 4));
+  if (a.sh.dtype) hipLaunchKernelGGL(final_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(final_kernel<float>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace incvit

@@ -1,0 +1,114 @@
+"""Helpers for the GPU parity tests: run the HIP path and the oracle on the
+same seeded inputs and compare them.
+
+Bars:
+* token indices and counts bit-exact; the fp32 reference rows (`ref`, each
+  token's embedding at its last refresh) and the layer-0 rows bit-exact, since
+  the embedding is computed in the same fixed fp32 order on both sides;
+* per layer, teacher-forced: the oracle's layer applied to the GPU's own cached
+  inputs of that layer gives the GPU's outputs (X^{l+1}, K^l, V^l, and Y)
+  within max|gpu - oracle| / max|oracle| <= 2e-2 (bf16 storage) or 1e-4 (fp32);
+* free-running (GPU from the first frame vs the oracle from the first frame):
+  within FREE_TOL.  With bf16 storage, roundings that sit at a tie flip when
+  accumulation is fp32 instead of fp64 and the flips compound through the
+  residual stream; a CPU implementation that only swaps fp64 for fp32
+  accumulation drifts by the same amount (tests/test_precision_drift.py).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import vit
+from paper_2607_12287_amd import incvit, synth
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+FREE_TOL = {"bf16": 4e-2, "f32": 1e-4}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def rel_err(a: np.ndarray, b: np.ndarray) -> float:
+    den = float(np.abs(b).max())
+    return float(np.abs(a - b).max()) / (den if den > 0 else 1.0)
+
+
+class Pair:
+    """The HIP encoder and the oracle on the same model and weights."""
+
+    def __init__(self, m: synth.ModelShape, w, B: int, oracle_views=None):
+        self.m, self.w, self.B = m, w, B
+        self.enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=B)
+        self.model = vit.Model(m, w)
+        self.buf, self.caches = self.enc.new_caches(B)
+        self.views = list(range(B)) if oracle_views is None else list(oracle_views)
+        self.ora = {}
+
+    def full_encode(self, batch: np.ndarray):
+        self.enc.full_encode(torch.from_numpy(batch).cuda(), self.caches)
+        torch.cuda.synchronize()
+        self.ora = {v: vit.full_encode(self.model, batch[v]) for v in self.views}
+
+    def step(self, batch: np.ndarray, tau: float, caps):
+        idx, count, refreshed = self.enc.step(torch.from_numpy(batch).cuda(), self.caches, tau, caps)
+        torch.cuda.synchronize()
+        res = {v: vit.step(self.model, batch[v], self.ora[v], tau, caps[v]) for v in self.views}
+        return idx.cpu().numpy(), count.cpu().numpy(), refreshed.float().cpu().numpy(), res
+
+    def check_step(self, idx, count, refreshed, res, label=""):
+        tol = FREE_TOL[self.m.dtype]
+        for v in self.views:
+            r = res[v]
+            assert int(count[v]) == r.count, (label, v, int(count[v]), r.count)
+            assert np.array_equal(idx[v, :r.count], r.idx), (label, v)
+            if r.count:
+                g = self.enc.export(self.caches[v])
+                assert np.array_equal(refreshed[v, :r.count], g["Y"][r.idx]), (label, v, "refreshed != Y[idx]")
+                e = rel_err(refreshed[v, :r.count], r.refreshed)
+                assert e <= tol, (label, v, "refreshed", e)
+
+    def check_layers(self, U_of=None, label=""):
+        """Teacher-forced parity of every layer; U_of(v) = refreshed rows
+        (None: all rows, after a full encode).  Returns the worst error."""
+        m, tol, dt = self.m, TOL[self.m.dtype], self.m.dtype
+        worst = 0.0
+        for v in self.views:
+            g = self.enc.export(self.caches[v])
+            U = np.arange(m.n_tokens) if U_of is None else np.asarray(U_of(v))
+            assert np.array_equal(g["ref"], self.ora[v].ref), (label, v, "ref")
+            assert np.array_equal(g["X"][0][U], vit.S(g["ref"][U].astype(np.float64), dt)), (label, v, "X0")
+            if U.size == 0:
+                continue
+            for l in range(m.depth):
+                K, V = g["K"][l].copy(), g["V"][l].copy()
+                Z = vit.layer_rows(self.model, l, g["X"][l][U], U, K, V)
+                for name, a, b in (("X", g["X"][l + 1][U], Z), ("K", g["K"][l][U], K[U]), ("V", g["V"][l][U], V[U])):
+                    e = rel_err(a, b)
+                    worst = max(worst, e)
+                    assert e <= tol, (label, v, "layer", l, name, e)
+            e = rel_err(g["Y"][U], vit.final_rows(self.model, g["X"][m.depth][U]))
+            worst = max(worst, e)
+            assert e <= tol, (label, v, "Y", e)
+        return worst
+
+    def check_caches(self, label=""):
+        tol = FREE_TOL[self.m.dtype]
+        worst = 0.0
+        for v in self.views:
+            g = self.enc.export(self.caches[v])
+            o = self.ora[v]
+            assert np.array_equal(g["ref"], o.ref), (label, v, "ref")
+            for name, depth in (("X", self.m.depth + 1), ("K", self.m.depth), ("V", self.m.depth)):
+                for l in range(depth):
+                    e = rel_err(g[name][l], getattr(o, name)[l])
+                    worst = max(worst, e)
+                    assert e <= tol, (label, v, name, l, e)
+            e = rel_err(g["Y"], o.Y)
+            worst = max(worst, e)
+            assert e <= tol, (label, v, "Y", e)
+        return worst

@@ -1,0 +1,58 @@
+"""The C-ABI library loads and exports every symbol include/incvit.h declares;
+host-only queries (no GPU) validate configs and report sizes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_12287_amd import incvit, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "incvit.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(incvit_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = incvit.lib()
+    declared = header_functions()
+    assert declared == sorted(incvit.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_sizes_match_canonical_layout():
+    for m in (synth.TINY, synth.SO400M, synth.VIT_L, synth.small_model(dtype="bf16")):
+        cfg = incvit.make_config(m, 4)
+        eb = 2 if m.dtype == "bf16" else 4
+        assert incvit.incvit_canonical_weights_bytes(cfg) == synth.canonical_weight_count(m) * eb
+        assert incvit.incvit_packed_weights_bytes(cfg) >= incvit.incvit_canonical_weights_bytes(cfg) // 2
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("patch", 5, incvit.INCVIT_ERR_SHAPE),            # 32 is not a multiple of 5
+    ("heads", 3, incvit.INCVIT_ERR_SHAPE),            # 64 % 3
+    ("dim", 48, incvit.INCVIT_ERR_UNSUPPORTED),       # dim % 32
+    ("dtype", 7, incvit.INCVIT_ERR_UNSUPPORTED),
+    ("max_streams", 0, incvit.INCVIT_ERR_UNSUPPORTED),
+    ("ln_eps", float("nan"), incvit.INCVIT_ERR_SHAPE),
+])
+def test_invalid_configs_are_rejected_before_any_device_work(field, value, status):
+    cfg = incvit.make_config(synth.small_model(dtype="bf16"), 2)
+    setattr(cfg, field, value)
+    assert incvit.incvit_canonical_weights_bytes(cfg) == 0
+    assert incvit.incvit_last_error(None) != ""
+    # packing with an invalid config fails synchronously with the right code
+    assert incvit.incvit_pack_weights(cfg, 256, 256, 0) == status
+
+
+def test_null_arguments_are_rejected():
+    cfg = incvit.make_config(synth.small_model(dtype="bf16"), 2)
+    assert incvit.incvit_pack_weights(cfg, 0, 256, 0) == incvit.INCVIT_ERR_ARG
+    st, h = incvit.incvit_create(cfg, 0)
+    assert st == incvit.INCVIT_ERR_ARG and not h.value
+    assert incvit.lib().incvit_full_encode(None, 1, None, None, None, None) == incvit.INCVIT_ERR_ARG

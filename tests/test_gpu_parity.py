@@ -1,0 +1,86 @@
+"""Parity of the HIP path with the CPU oracle, through the C ABI.
+
+Small models span several GEMM row/column tiles, K splits, head dims 32/64/72
+and token counts with ragged tails; the five workloads run at full size on
+sampled frames (and sampled streams where the oracle would be slow).
+"""
+import numpy as np
+import pytest
+
+from paper_2607_12287_amd import synth
+from tests.gpu_util import Pair, say
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    # name: (dim, depth, heads, mlp, img, patch, dtype, B)
+    "f32_dh32_n16": (64, 2, 2, 96, 32, 8, "f32", 1),
+    "bf16_dh32_n49": (64, 2, 2, 96, 28, 4, "bf16", 2),
+    "bf16_dh64_n100_split": (256, 2, 4, 200, 40, 4, "bf16", 2),
+    "bf16_dh72_n64": (288, 2, 4, 300, 32, 4, "bf16", 1),
+    "f32_dh64_n100_split": (256, 2, 4, 200, 40, 4, "f32", 3),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_small_models_stream(name):
+    dim, depth, heads, mlp, img, patch, dtype, B = SMALL[name]
+    m = synth.small_model(dim=dim, depth=depth, heads=heads, mlp=mlp, img=img, patch=patch, dtype=dtype)
+    w = synth.make_weights(m, 100 + dim)
+    say(f"[{name}] N={m.n_tokens} D={dim} dh={m.head_dim} F={mlp} B={B}")
+    streams = [synth.RefillRectStream(m, 300 + v, v, 2 * patch + 3, 3 * patch) for v in range(B)]
+    its = [s.frames(6) for s in streams]
+    frames = [np.stack([synth.patchify(next(it), patch) for it in its]) for _ in range(6)]
+    p = Pair(m, w, B)
+    p.full_encode(frames[0])
+    p.check_layers(None, f"{name} full")
+    p.check_caches(f"{name} full")
+    rng = np.random.default_rng(7)
+    for t in range(1, 6):
+        tau = [0.98, 0.99, np.inf, 0.98, 0.995][t - 1]
+        caps = [int(rng.integers(0, m.n_tokens + 2)) if t % 2 else m.n_tokens for _ in range(B)]
+        idx, count, refreshed, res = p.step(frames[t], tau, caps)
+        say(f"  step {t}: tau={tau} caps={caps} count={count.tolist()}")
+        p.check_step(idx, count, refreshed, res, f"{name} step {t}")
+        p.check_layers(lambda v: idx[v, :count[v]], f"{name} step {t}")
+        p.check_caches(f"{name} step {t}")
+
+
+def _workload_run(name, steps, oracle_views=None, rho=0.10):
+    wl = synth.workload(name, rho=rho)
+    m = wl.model
+    say(f"[{name}] rho={rho} views={wl.views} steps={steps}")
+    w = wl.weights()
+    p = Pair(m, w, wl.views, oracle_views)
+    frames = list(wl.patch_frames(steps + 1))
+    p.full_encode(frames[0])
+    tf = p.check_layers(None, f"{name} full")
+    worst = p.check_caches(f"{name} full")
+    say(f"  full encode: per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
+    for t in range(1, steps + 1):
+        idx, count, refreshed, res = p.step(frames[t], wl.tau, wl.caps)
+        p.check_step(idx, count, refreshed, res, f"{name} step {t}")
+        tf = p.check_layers(lambda v: idx[v, :count[v]], f"{name} step {t}")
+        worst = p.check_caches(f"{name} step {t}")
+        say(f"  step {t}: count={count.tolist()} per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
+
+
+def test_tiny_workload():
+    _workload_run("tiny", 8)
+
+
+def test_so400m_workload():
+    _workload_run("so400m", 3)
+
+
+def test_so400m_three_views():
+    _workload_run("so400m_x3", 2)
+
+
+@pytest.mark.parametrize("rho", [0.02, 0.10, 1.0])
+def test_so400m_448_top_k(rho):
+    _workload_run("so400m_448", 1, rho=rho)
+
+
+def test_vitl_eight_streams_sampled():
+    _workload_run("vitl_x8", 2, oracle_views=[0, 5])
