@@ -77,7 +77,10 @@ def main() -> int:
     ap.add_argument("--full-repeats", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel events")
+    ap.add_argument("--eager", dest="graph", action="store_false",
+                    help="launch kernel by kernel instead of replaying captured HIP graphs")
+    ap.add_argument("--waves", default=None, help="waves per GEMM workgroup: four comma-separated values (0 = automatic)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -99,48 +102,80 @@ def main() -> int:
     torch.cuda.set_device(dev)
     frames = torch.from_numpy(np.stack(frames_np)).to(dev)  # [T][B][N][P], resident in HBM
     enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
+    if args.waves:
+        incvit._check(incvit.incvit_set_tuning(enc.h, [int(x) for x in args.waves.split(",")]), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),
            torch.empty((B, m.n_tokens, m.dim), dtype=enc.dtype, device=dev))
     counts = torch.zeros((total, B), dtype=torch.int32, device=dev)
 
+    inp = torch.empty_like(frames[0])  # the fixed input buffer the graphs read
+
     # full re-encode: the baseline the speedup divides by (scratch caches)
     sbuf, scratch = enc.new_caches(B)
+    inp.copy_(frames[0])
+    gfull = enc.full_graph(inp, scratch) if args.graph else None
+    run_full = (lambda: enc.launch(gfull)) if args.graph else (lambda: enc.full_encode(inp, scratch))
     for _ in range(3):
-        enc.full_encode(frames[0], scratch)
+        run_full()
     torch.cuda.synchronize()
     full_ms = []
     for _ in range(args.full_repeats):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        enc.full_encode(frames[0], scratch)
+        run_full()
         e1.record()
         e1.synchronize()
         full_ms.append(e0.elapsed_time(e1))
+    if gfull is not None:
+        enc.drop_graph(gfull)
     del sbuf, scratch
 
     # the stream: full encode of frame 0, warmup steps, timed steps
     enc.full_encode(frames[0], caches)
+    gstep = enc.step_graph(inp, caches, wl.tau, wl.caps, out) if args.graph else None
+
+    def one_step(t):
+        inp.copy_(frames[t])
+        if gstep is not None:
+            enc.launch(gstep)
+        else:
+            enc.step(inp, caches, wl.tau, wl.caps, out=out)
+
     for t in range(1, args.warmup + 1):
-        enc.step(frames[t], caches, wl.tau, wl.caps, out=out)
-        counts[t].copy_(out[1])
+        one_step(t)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_start = time.perf_counter()
     e0.record()
     for t in range(args.warmup + 1, total):
-        enc.step(frames[t], caches, wl.tau, wl.caps, out=out)
-        counts[t].copy_(out[1])
+        one_step(t)
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     dev_ms = e0.elapsed_time(e1)
     step_ms = wall * 1e3 / args.steps
     fps = args.steps * B / wall
+    full_med = statistics.median(full_ms)
+    if gstep is not None:
+        enc.drop_graph(gstep)
+
+    # same frames again, eagerly, with per-kernel events on the launch stream
+    buf2, caches2 = enc.new_caches(B)
+    enc.full_encode(frames[0], caches2)
+    for t in range(1, args.warmup + 1):
+        enc.step(frames[t], caches2, wl.tau, wl.caps, out=out)
+    torch.cuda.synchronize()
+    if not args.no_profile:
+        incvit.incvit_profile_read(enc.h, reset=True)
+        incvit.incvit_profile_enable(enc.h, True)
+    for t in range(args.warmup + 1, total):
+        enc.step(frames[t], caches2, wl.tau, wl.caps, out=out)
+        counts[t].copy_(out[1])
+    torch.cuda.synchronize()
     k = counts[args.warmup + 1:].float().cpu().numpy()
     mean_rows = float(k.sum(axis=1).mean())
-    full_med = statistics.median(full_ms)
 
     result = {
         "metric": METRIC, "value": round(fps, 2), "unit": "frames/s", "n_gpus": 1,
@@ -153,26 +188,15 @@ def main() -> int:
                    "views": B, "tokens": m.n_tokens, "refresh_mean": round(mean_rows / (B * m.n_tokens), 4),
                    "rows_mean": round(mean_rows, 2)},
         "device_ms_per_step": round(dev_ms / args.steps, 5),
+        "launch": "hip-graph" if args.graph else "eager",
         "full_encode_ms": round(full_med, 5),
         "full_encode_frames_per_s": round(B * 1e3 / full_med, 2),
         "speedup_vs_full_encode": round(full_med / step_ms, 3),
     }
 
     if not args.no_profile:
-        # same frames again with per-kernel events on the launch stream
-        buf2, caches2 = enc.new_caches(B)
-        enc.full_encode(frames[0], caches2)
-        for t in range(1, args.warmup + 1):
-            enc.step(frames[t], caches2, wl.tau, wl.caps, out=out)
-        torch.cuda.synchronize()
-        incvit.incvit_profile_read(enc.h, reset=True)
-        incvit.incvit_profile_enable(enc.h, True)
-        for t in range(args.warmup + 1, total):
-            enc.step(frames[t], caches2, wl.tau, wl.caps, out=out)
-        torch.cuda.synchronize()
         prof = incvit.incvit_profile_read(enc.h, reset=True)
         incvit.incvit_profile_enable(enc.h, False)
-        del buf2, caches2
         kinds = {k: v for k, v in prof.items() if v[1] > 0}
         dom = max(kinds, key=lambda k: kinds[k][0])
         avg_us = kinds[dom][0] * 1e3 / kinds[dom][1]
@@ -189,7 +213,9 @@ def main() -> int:
             "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
             "traffic": None, "avg_launch_us": round(avg_us, 3), "bytes_per_launch": nbytes,
         }
+        result["kernel_us_per_launch"] = {k: round(v[0] * 1e3 / v[1], 3) for k, v in kinds.items()}
         result["kernel_ms_per_step"] = {k: round(v[0] / args.steps, 5) for k, v in kinds.items()}
+    del buf2, caches2
 
     if not args.no_cpu_baseline:
         n_cpu = min(len(frames_np), 64)

@@ -166,6 +166,44 @@ incvit_status incvit_cache_status(const incvit_handle* h, const void* cache, voi
  * h is NULL).  Valid until the next call on h. */
 const char* incvit_last_error(const incvit_handle* h);
 
+/* ------------------------------------------------------------ HIP graphs -- */
+
+typedef struct incvit_graph incvit_graph;
+
+/* Capture one incvit_step (same arguments, no stream) into a HIP graph, for
+ * callers that encode frame after frame with fixed buffers: write the next
+ * frame into `patches` (on the stream you launch on), then incvit_graph_launch.
+ * The buffers, caches, tau and caps are baked in and must stay valid.  The
+ * graph holds no memory operations other than kernels, so it is safe to
+ * replay any number of times; one graph must not run concurrently with
+ * itself or with other work on the same caches or workspace. */
+incvit_status incvit_step_graph_create(incvit_handle* h, int32_t B, const float* patches,
+                                       void* const* caches, float tau, const int32_t* cap,
+                                       int32_t* idx, int32_t* count, void* refreshed,
+                                       void* workspace, incvit_graph** out);
+
+/* Same for incvit_full_encode. */
+incvit_status incvit_full_graph_create(incvit_handle* h, int32_t B, const float* patches,
+                                       void* const* caches, void* workspace, incvit_graph** out);
+
+/* Enqueue a captured graph on `stream`. */
+incvit_status incvit_graph_launch(incvit_graph* g, void* stream);
+
+void incvit_graph_destroy(incvit_graph* g);
+
+/* ---------------------------------------------------------------- tuning -- */
+
+/* Performance knobs; every setting gives a deterministic result, and the
+ * settings differ only in the order of fp32 partial sums.
+ * waves[k]: waves per workgroup of GEMM k (0 = QKV, 1 = output projection,
+ * 2 = MLP up, 3 = MLP down): 4, 8 or 16; 0 = automatic.  A NULL pointer
+ * restores the defaults. */
+typedef struct {
+  int32_t waves[4];
+} incvit_tuning;
+
+incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);
+
 /* ------------------------------------------------------------- profiling -- */
 
 /* Kernel kinds for the per-kernel timers. */

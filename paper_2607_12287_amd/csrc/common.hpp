@@ -15,13 +15,14 @@ constexpr int kMaxHeadDim = 128;
 constexpr uint32_t kCacheMagic = 0x31435649u;  // "IVC1"
 constexpr int kStatusNonFinite = -1;           // a step saw a NaN similarity
 
-// GEMM tiling: a workgroup of 4 waves owns 64 rows x 16 columns; each wave
-// takes every 4th 32-deep K chunk; the 4 partial tiles are summed in a fixed
-// order.  Weights are packed so that one chunk is one 16-byte (bf16) or
-// 32-byte (fp32) load per lane, already in MFMA operand order.
+// GEMM tiling: a workgroup streams one 16-column block of the weights for
+// blocks of 64 rows; its waves take every NW-th 32-deep K chunk and their
+// partial tiles are summed in wave order.  Weights are packed so that one
+// chunk is one 16-byte (bf16) or 32-byte (fp32) load per lane, already in
+// MFMA operand order.
 constexpr int kGemmRows = 64;
-constexpr int kGemmWaves = 4;
 constexpr int kChunkElems = 512;  // 64 lanes x 8 elements
+constexpr int kMaxStat = kMaxDim / 16;  // LayerNorm partials per row
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -52,9 +53,23 @@ struct Views {
   char* p[kMaxViews];
 };
 
-// Rows of a call: row r of the compact M rows belongs to the view v with
-// off[v] <= r < off[v+1] (off = prefix sum of count) and is token
-// idx[v*N + r - off[v]].
+// Rows of a call: row r of the compact M rows is token `tok` of the stream
+// whose cache starts at `cache`.  Written once per call (by the commit
+// kernel) so that later kernels find a row with a single load.
+struct RowInfo {
+  char* cache;
+  int tok;
+  int view;
+};
+
+// Per-call bookkeeping in the workspace.
+struct Meta {
+  int m;                     // M: rows of the call
+  int off[kMaxViews + 1];    // first compact row of each stream
+};
+
+// Rows of a call as the selection left them: count[v] rows of stream v are
+// tokens idx[v*N + 0 .. count[v]).  Read only by the commit kernel.
 struct RowMap {
   const int* count;
   const int* idx;
@@ -110,8 +125,10 @@ struct SelectArgs {
   int* count;  // [B]
 };
 
-struct RowsArgs {  // commit (ref/X0 of refreshed rows) and final LayerNorm
+struct RowsArgs {  // commit (ref/X0 of refreshed rows, row map) and final LayerNorm
   RowMap rm;
+  RowInfo* rows;     // commit writes, final reads
+  Meta* meta;        // commit writes, final reads
   Views caches;
   CacheLayout cl;
   Shape sh;
@@ -121,13 +138,15 @@ struct RowsArgs {  // commit (ref/X0 of refreshed rows) and final LayerNorm
   void* refreshed;   // final: optional [B][N][D]
   int init_header;   // commit of a full encode: write header
   uint32_t hash;
+  float2* stats;     // commit: (sum, sum of squares) of each X0 row, stride stat_stride
+  int stat_stride;
 };
 
 enum Epi { EPI_QKV = 0, EPI_OPROJ = 1, EPI_FC1 = 2, EPI_FC2 = 3 };
 
 struct GemmArgs {
-  RowMap rm;
-  Views caches;
+  const RowInfo* rows;
+  const Meta* meta;
   CacheLayout cl;
   Shape sh;
   int layer;
@@ -137,24 +156,27 @@ struct GemmArgs {
   const float* ln_b;
   const void* W;      // packed [Nout/16][kchunks][512]
   const float* bias;  // [Nout]
-  int K, kchunks, Nout;
-  int ksplit;
-  int Mpad;
-  float* partial;     // [ksplit][Mpad][Nout] when ksplit > 1
-  int* counters;      // [gridDim.y][gridDim.x]
+  int kchunks, Nout;
   void* out;          // QKV: Q [Mpad][D]; OPROJ: H f32 [Mpad][D]; FC1: G [Mpad][Fpad]
   int ldo;
   const float* hres;  // FC2: H f32 [Mpad][D]
+  // LayerNorm statistics: per compact row, nstat partial (sum, sum of squares)
+  // pairs at stride stat_stride; read by QKV/FC1, written by OPROJ/FC2
+  const float2* stats_in;
+  float2* stats_out;
+  int nstat, stat_stride;
 };
 
 struct AttnArgs {
-  RowMap rm;
+  const Meta* meta;
+  int B;
   Views caches;
   CacheLayout cl;
   Shape sh;
   int layer;
   const void* q;  // [Mpad][D]
   void* o;        // [Mpad][D]
+  int qmax;       // Mpad - 1: last row a clamped load may touch
   float scale_log2;
   int split;      // 4: one 16-query tile per workgroup, keys split over 4 waves;
                   // 1: four 16-query tiles per workgroup, one per wave
@@ -188,12 +210,11 @@ hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s);
-hipError_t launch_gemm(int epi, const GemmArgs& a, int mmax, size_t lds_bytes, hipStream_t s);
+hipError_t launch_gemm(int epi, int waves, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);
 hipError_t launch_export(const ExportArgs& a, hipStream_t s);
-hipError_t gemm_set_lds_limits(size_t bytes);
 
 }  // namespace incvit
 
@@ -203,6 +224,20 @@ namespace incvit {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+// Pointers read from memory (the row map) are generic to the compiler, which
+// then emits flat accesses; flat accesses count against both the vector-memory
+// and the LDS counters and defeat load pipelining.  Every such pointer here
+// points to device global memory, so it is cast to the global address space.
+#define INCVIT_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ INCVIT_GLOBAL T* gbl(T* p) {
+  return (INCVIT_GLOBAL T*)p;
+}
+template <class T>
+__device__ __forceinline__ const INCVIT_GLOBAL T* gbl(const T* p) {
+  return (const INCVIT_GLOBAL T*)p;
+}
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
@@ -216,11 +251,13 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 
 template <class T> struct Elem;
 template <> struct Elem<uint16_t> {
+  __device__ static float f(uint16_t x) { return bf2f(x); }
   __device__ static float ld(const uint16_t* p, long i) { return bf2f(p[i]); }
   __device__ static uint16_t cv(float f) { return f2bf(f); }
   __device__ static float rnd(float f) { return bf2f(f2bf(f)); }
 };
 template <> struct Elem<float> {
+  __device__ static float f(float x) { return x; }
   __device__ static float ld(const float* p, long i) { return p[i]; }
   __device__ static float cv(float f) { return f; }
   __device__ static float rnd(float f) { return f; }
@@ -228,16 +265,18 @@ template <> struct Elem<float> {
 
 // 8 consecutive elements of one lane: one MFMA operand for a 32-deep chunk.
 template <class T> struct V8;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
 template <> struct V8<uint16_t> {
   uint4 v;
-  __device__ void load(const uint16_t* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ void load(const uint16_t* p) { v = __builtin_bit_cast(uint4, *(const INCVIT_GLOBAL u32x4_t*)p); }
   __device__ void zero() { v = make_uint4(0, 0, 0, 0); }
 };
 template <> struct V8<float> {
   float4 a, b;
   __device__ void load(const float* p) {
-    a = reinterpret_cast<const float4*>(p)[0];
-    b = reinterpret_cast<const float4*>(p)[1];
+    a = __builtin_bit_cast(float4, ((const INCVIT_GLOBAL f32x4_t*)p)[0]);
+    b = __builtin_bit_cast(float4, ((const INCVIT_GLOBAL f32x4_t*)p)[1]);
   }
   __device__ void zero() { a = make_float4(0, 0, 0, 0); b = a; }
 };
@@ -272,31 +311,9 @@ __device__ __forceinline__ float wave_max(float x) {
   return x;
 }
 
-// Per-view row offsets (prefix sums of count) into shared memory; returns M.
-__device__ __forceinline__ int row_offsets(const RowMap& rm, int* s_off) {
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int v = 0; v < rm.B; ++v) {
-      s_off[v] = acc;
-      acc += rm.count[v];
-    }
-    s_off[rm.B] = acc;
-  }
-  __syncthreads();
-  return s_off[rm.B];
-}
-
-// Compact row r -> (view, token).
-__device__ __forceinline__ void row_token(const RowMap& rm, const int* s_off, int r, int& v, int& tok) {
-  int vv = 0;
-  while (vv + 1 < rm.B && s_off[vv + 1] <= r) ++vv;
-  v = vv;
-  tok = rm.idx[vv * rm.N + (r - s_off[vv])];
-}
-
 template <class T>
-__device__ __forceinline__ T* x_row(const Views& c, const CacheLayout& cl, const Shape& sh, int v, int layer, int tok) {
-  return reinterpret_cast<T*>(c.p[v] + cl.x + (size_t)layer * cl.x_layer) + (size_t)tok * sh.D;
+__device__ __forceinline__ T* x_row(char* cache, const CacheLayout& cl, const Shape& sh, int layer, int tok) {
+  return reinterpret_cast<T*>(cache + cl.x + (size_t)layer * cl.x_layer) + (size_t)tok * sh.D;
 }
 
 }  // namespace incvit

@@ -15,8 +15,6 @@ using namespace incvit;
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr size_t kLdsLimit = 160 * 1024;
-constexpr size_t kLdsStatic = 2048;  // static __shared__ of the GEMM kernel (upper bound)
 constexpr int kMaxSplit = 8;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -38,8 +36,8 @@ struct CanonLayout {  // element offsets into the canonical buffer
 };
 
 struct WsLayout {
-  size_t counters, count, idx, sim, t0, q, o, h, g, partial, total;
-  int Mpad, ncounters;
+  size_t meta, rows, count, idx, sim, t0, q, o, h, g, stats_x, stats_h, total;
+  int Mpad, stat_stride;
 };
 
 enum GemmKind { G_QKV = 0, G_OPROJ = 1, G_FC1 = 2, G_FC2 = 3 };
@@ -191,23 +189,13 @@ GemmGeom gemm_geom(const Shape& sh, int kind) {
   return g;
 }
 
-// Split of K over workgroups: enough to fit the A block in LDS, and enough
-// workgroups to keep the chip busy when there are few rows.
-int choose_ksplit(const Shape& sh, const GemmGeom& g, int mmax) {
-  const size_t per_row = (kLdsLimit - kLdsStatic) / kGemmRows;
-  const int max_chunks = (int)((per_row - 16) / sh.eb / 32);
-  const int ks_lds = (g.kchunks + max_chunks - 1) / max_chunks;
-  const int gy = std::max(1, (mmax + kGemmRows - 1) / kGemmRows);
-  const int ks_occ = (200 + g.nblocks * gy - 1) / (g.nblocks * gy);
-  int ks = std::min(ks_occ, std::max(1, g.kchunks / 4));
-  ks = std::max(ks, ks_lds);
-  return std::min(std::max(ks, 1), std::max(kMaxSplit, ks_lds));
-}
+// Waves per GEMM workgroup: 8 keeps enough loads in flight per CU without
+// register spills (16 waves cap a wave at 128 registers).
+int auto_waves(const GemmGeom&) { return 8; }
 
-size_t gemm_lds(const Shape& sh, const GemmGeom& g, int ks) {
-  const int chunks = (g.kchunks + ks - 1) / ks;
-  const size_t a = (size_t)kGemmRows * ((size_t)chunks * 32 * sh.eb + 16);
-  return std::max(a, (size_t)kGemmWaves * 4 * 64 * 16);
+int waves_of(const int* tuned, const GemmGeom& g, int kind) {
+  const int t = tuned ? tuned[kind] : 0;
+  return t > 0 ? t : auto_waves(g);
 }
 
 WsLayout ws_layout(const Shape& sh, int B) {
@@ -216,16 +204,9 @@ WsLayout ws_layout(const Shape& sh, int B) {
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
   const int M = B * sh.N;
   w.Mpad = round_up(std::max(M, 1), kGemmRows);
-  int maxN = 0;
-  size_t part = 0;
-  for (int k = 0; k < 4; ++k) {
-    const GemmGeom g = gemm_geom(sh, k);
-    maxN = std::max(maxN, g.Nout);
-    const int ks = std::max(choose_ksplit(sh, g, 1), choose_ksplit(sh, g, w.Mpad));
-    if (ks > 1) part = std::max(part, (size_t)ks * w.Mpad * g.Nout);
-  }
-  w.ncounters = (w.Mpad / kGemmRows) * (maxN / 16);
-  w.counters = take((size_t)w.ncounters * 4);
+  w.stat_stride = sh.D / 16;
+  w.meta = take(sizeof(Meta));
+  w.rows = take((size_t)w.Mpad * sizeof(RowInfo));
   w.count = take(kMaxViews * 4);
   w.idx = take((size_t)M * 4);
   w.sim = take((size_t)M * 4);
@@ -234,7 +215,8 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
   w.h = take((size_t)w.Mpad * sh.D * 4);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
-  w.partial = take(part * 4);
+  w.stats_x = take((size_t)w.Mpad * w.stat_stride * 8);
+  w.stats_h = take((size_t)w.Mpad * w.stat_stride * 8);
   w.total = off;
   return w;
 }
@@ -258,6 +240,12 @@ struct incvit_handle {
   std::vector<hipEvent_t> pool;
   double prof_ms[INCVIT_K_COUNT] = {};
   int64_t prof_n[INCVIT_K_COUNT] = {};
+  int waves[4] = {0, 0, 0, 0};  // 0 = automatic
+};
+
+struct incvit_graph {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
 };
 
 namespace {
@@ -285,11 +273,11 @@ incvit_status run(incvit_handle* h, int kind, hipStream_t s, F&& launch) {
   if (h->prof) {
     e0 = take_event(h);
     e1 = take_event(h);
-    if (e0) hipEventRecord(e0, s);
+    if (e0) (void)hipEventRecord(e0, s);
   }
   const hipError_t err = launch();
   if (h->prof && e0 && e1) {
-    hipEventRecord(e1, s);
+    (void)hipEventRecord(e1, s);
     h->recs.push_back({kind, e0, e1});
   }
   if (err != hipSuccess) {
@@ -302,68 +290,72 @@ incvit_status run(incvit_handle* h, int kind, hipStream_t s, F&& launch) {
 
 const float* fptr(const incvit_handle* h, size_t off) { return reinterpret_cast<const float*>(h->packed + off); }
 
-// Launch the per-layer kernels for rows described by rm.
-incvit_status run_layers(incvit_handle* h, const RowMap& rm, const Views& views, const WsLayout& wl,
-                         char* ws, int mmax, int max_rows_per_view, bool step, hipStream_t s) {
+// Launch the per-layer kernels for the rows of the call (row map in ws).
+incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLayout& wl, char* ws,
+                         int max_rows_per_view, bool step, hipStream_t s) {
   const Shape& sh = h->sh;
+  const RowInfo* rows = reinterpret_cast<const RowInfo*>(ws + wl.rows);
+  const Meta* meta = reinterpret_cast<const Meta*>(ws + wl.meta);
+  float2* stats_x = reinterpret_cast<float2*>(ws + wl.stats_x);
+  float2* stats_h = reinterpret_cast<float2*>(ws + wl.stats_h);
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
-    GemmArgs ga;
-    memset(&ga, 0, sizeof ga);
-    ga.rm = rm;
-    ga.caches = views;
-    ga.cl = h->cl;
-    ga.sh = sh;
-    ga.layer = l;
-    ga.Mpad = wl.Mpad;
-    ga.partial = reinterpret_cast<float*>(ws + wl.partial);
-    ga.counters = reinterpret_cast<int*>(ws + wl.counters);
-
     auto gemm = [&](int kind, int epi, int kernel_kind) -> incvit_status {
       const GemmGeom g = gemm_geom(sh, kind);
-      GemmArgs a = ga;
-      a.K = g.K;
+      GemmArgs a;
+      memset(&a, 0, sizeof a);
+      a.rows = rows;
+      a.meta = meta;
+      a.cl = h->cl;
+      a.sh = sh;
+      a.layer = l;
       a.kchunks = g.kchunks;
       a.Nout = g.Nout;
-      a.ksplit = choose_ksplit(sh, g, mmax);
-      const size_t lds = gemm_lds(sh, g, a.ksplit);
+      a.stat_stride = wl.stat_stride;
       switch (kind) {
         case G_QKV:
           a.ln_g = fptr(h, P.ln1_g); a.ln_b = fptr(h, P.ln1_b);
           a.W = h->packed + P.w_qkv; a.bias = fptr(h, P.b_qkv);
           a.out = ws + wl.q; a.ldo = sh.D;
+          a.stats_in = stats_x; a.nstat = l == 0 ? 1 : sh.D / 16;
           break;
         case G_OPROJ:
           a.A = ws + wl.o; a.lda = sh.D;
           a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
           a.out = ws + wl.h; a.ldo = sh.D;
+          a.stats_out = stats_h;
           break;
         case G_FC1:
           a.A = ws + wl.h; a.lda = sh.D;
           a.ln_g = fptr(h, P.ln2_g); a.ln_b = fptr(h, P.ln2_b);
           a.W = h->packed + P.w_1; a.bias = fptr(h, P.b_1);
           a.out = ws + wl.g; a.ldo = sh.Fpad;
+          a.stats_in = stats_h; a.nstat = sh.D / 16;
           break;
         default:
           a.A = ws + wl.g; a.lda = sh.Fpad;
           a.W = h->packed + P.w_2; a.bias = fptr(h, P.b_2);
           a.hres = reinterpret_cast<const float*>(ws + wl.h);
+          a.stats_out = stats_x;
           break;
       }
-      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, a, mmax, lds, s); });
+      const int waves = waves_of(h->waves, g, kind);
+      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, waves, a, s); });
     };
 
     incvit_status st;
     if ((st = gemm(G_QKV, EPI_QKV, INCVIT_K_QKV)) != INCVIT_OK) return st;
     AttnArgs aa;
     memset(&aa, 0, sizeof aa);
-    aa.rm = rm;
+    aa.meta = meta;
+    aa.B = B;
     aa.caches = views;
     aa.cl = h->cl;
     aa.sh = sh;
     aa.layer = l;
     aa.q = ws + wl.q;
     aa.o = ws + wl.o;
+    aa.qmax = wl.Mpad - 1;
     aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
     aa.split = step ? 4 : 1;
     if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, s); })) != INCVIT_OK) return st;
@@ -475,8 +467,6 @@ incvit_status incvit_create(const incvit_config* cfg, const void* packed_weights
   if (!make_shape(cfg, sh, st, err)) return fail(nullptr, st, err);
   if (!packed_weights || reinterpret_cast<uintptr_t>(packed_weights) % kAlign)
     return fail(nullptr, INCVIT_ERR_ARG, "packed weights must be non-null and 256-byte aligned");
-  const hipError_t e = gemm_set_lds_limits(kLdsLimit - kLdsStatic);
-  if (e != hipSuccess) return fail(nullptr, INCVIT_ERR_HIP, std::string("hipFuncSetAttribute: ") + hipGetErrorString(e));
   incvit_handle* h = new incvit_handle();
   h->cfg = *cfg;
   h->sh = sh;
@@ -527,21 +517,24 @@ incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patch
   float* t0 = reinterpret_cast<float*>(ws + wl.t0);
 
   EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
-               B, sh.N, sh.P, sh.D, sh.dtype, reinterpret_cast<int*>(ws + wl.counters), wl.ncounters, idx, count};
+               B, sh.N, sh.P, sh.D, sh.dtype, nullptr, 0, idx, count};
   if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
-  const RowMap rm{count, idx, B, sh.N};
   const int mmax = B * sh.N;
   RowsArgs ra;
   memset(&ra, 0, sizeof ra);
-  ra.rm = rm;
+  ra.rm = RowMap{count, idx, B, sh.N};
+  ra.rows = reinterpret_cast<RowInfo*>(ws + wl.rows);
+  ra.meta = reinterpret_cast<Meta*>(ws + wl.meta);
   ra.caches = views;
   ra.cl = h->cl;
   ra.sh = sh;
   ra.t0 = t0;
   ra.init_header = 1;
   ra.hash = h->hash;
+  ra.stats = reinterpret_cast<float2*>(ws + wl.stats_x);
+  ra.stat_stride = wl.stat_stride;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  if ((st = run_layers(h, rm, views, wl, ws, mmax, sh.N, false, s)) != INCVIT_OK) return st;
+  if ((st = run_layers(h, views, B, wl, ws, sh.N, false, s)) != INCVIT_OK) return st;
   ra.init_header = 0;
   ra.g = fptr(h, h->pl.lnf_g);
   ra.b = fptr(h, h->pl.lnf_b);
@@ -577,7 +570,7 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
     max_rows = std::max(max_rows, c);
   }
   EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
-               B, sh.N, sh.P, sh.D, sh.dtype, reinterpret_cast<int*>(ws + wl.counters), wl.ncounters, nullptr, nullptr};
+               B, sh.N, sh.P, sh.D, sh.dtype, nullptr, 0, nullptr, nullptr};
   if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
   SimArgs si{t0, views, h->cl.ref, sim, B, sh.N, sh.D};
   if ((st = run(h, INCVIT_K_SIM, s, [&] { return launch_sim(si, s); })) != INCVIT_OK) return st;
@@ -592,16 +585,19 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   if ((st = run(h, INCVIT_K_SELECT, s, [&] { return launch_select(sa, s); })) != INCVIT_OK) return st;
   if (mmax == 0) return INCVIT_OK;
 
-  const RowMap rm{count, idx, B, sh.N};
   RowsArgs ra;
   memset(&ra, 0, sizeof ra);
-  ra.rm = rm;
+  ra.rm = RowMap{count, idx, B, sh.N};
+  ra.rows = reinterpret_cast<RowInfo*>(ws + wl.rows);
+  ra.meta = reinterpret_cast<Meta*>(ws + wl.meta);
   ra.caches = views;
   ra.cl = h->cl;
   ra.sh = sh;
   ra.t0 = t0;
+  ra.stats = reinterpret_cast<float2*>(ws + wl.stats_x);
+  ra.stat_stride = wl.stat_stride;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  if ((st = run_layers(h, rm, views, wl, ws, mmax, max_rows, true, s)) != INCVIT_OK) return st;
+  if ((st = run_layers(h, views, B, wl, ws, max_rows, true, s)) != INCVIT_OK) return st;
   ra.g = fptr(h, h->pl.lnf_g);
   ra.b = fptr(h, h->pl.lnf_b);
   ra.refreshed = refreshed;
@@ -666,6 +662,82 @@ incvit_status incvit_profile_read(incvit_handle* h, double* total_ms, int64_t* l
     }
   }
   return INCVIT_OK;
+}
+
+incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  for (int k = 0; k < 4; ++k) {
+    const int v = t ? t->waves[k] : 0;
+    if (v != 0 && v != 4 && v != 8 && v != 16) return fail(h, INCVIT_ERR_ARG, "waves must be 0, 4, 8 or 16");
+    h->waves[k] = v;
+  }
+  return INCVIT_OK;
+}
+
+}  // extern "C"
+
+namespace {
+template <class F>
+incvit_status capture(incvit_handle* h, incvit_graph** out, F&& body) {
+  if (!out) return fail(h, INCVIT_ERR_ARG, "out is null");
+  *out = nullptr;
+  hipStream_t cs = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+  if (e != hipSuccess) return fail(h, INCVIT_ERR_HIP, std::string("hipStreamCreate: ") + hipGetErrorString(e));
+  const bool prof = h->prof;
+  h->prof = false;
+  incvit_graph* g = new incvit_graph();
+  incvit_status st = INCVIT_OK;
+  e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+  if (e == hipSuccess) {
+    st = body(cs);
+    const hipError_t e2 = hipStreamEndCapture(cs, &g->graph);
+    if (st == INCVIT_OK && e2 != hipSuccess) e = e2;
+  }
+  if (st == INCVIT_OK && e == hipSuccess) e = hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0);
+  h->prof = prof;
+  hipStreamDestroy(cs);
+  if (st != INCVIT_OK || e != hipSuccess) {
+    if (g->exec) hipGraphExecDestroy(g->exec);
+    if (g->graph) hipGraphDestroy(g->graph);
+    delete g;
+    if (st != INCVIT_OK) return st;
+    return fail(h, INCVIT_ERR_HIP, std::string("graph capture: ") + hipGetErrorString(e));
+  }
+  *out = g;
+  return INCVIT_OK;
+}
+}  // namespace
+
+extern "C" {
+
+incvit_status incvit_step_graph_create(incvit_handle* h, int32_t B, const float* patches, void* const* caches,
+                                       float tau, const int32_t* cap, int32_t* idx, int32_t* count,
+                                       void* refreshed, void* workspace, incvit_graph** out) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  return capture(h, out, [&](hipStream_t cs) {
+    return incvit_step(h, B, patches, caches, tau, cap, idx, count, refreshed, workspace, cs);
+  });
+}
+
+incvit_status incvit_full_graph_create(incvit_handle* h, int32_t B, const float* patches, void* const* caches,
+                                       void* workspace, incvit_graph** out) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  return capture(h, out, [&](hipStream_t cs) { return incvit_full_encode(h, B, patches, caches, workspace, cs); });
+}
+
+incvit_status incvit_graph_launch(incvit_graph* g, void* stream) {
+  if (!g || !g->exec) return fail(nullptr, INCVIT_ERR_ARG, "null graph");
+  const hipError_t e = hipGraphLaunch(g->exec, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(nullptr, INCVIT_ERR_HIP, std::string("hipGraphLaunch: ") + hipGetErrorString(e));
+  return INCVIT_OK;
+}
+
+void incvit_graph_destroy(incvit_graph* g) {
+  if (!g) return;
+  if (g->exec) hipGraphExecDestroy(g->exec);
+  if (g->graph) hipGraphDestroy(g->graph);
+  delete g;
 }
 
 }  // extern "C"

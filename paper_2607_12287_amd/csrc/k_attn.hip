@@ -73,40 +73,60 @@ __device__ __forceinline__ void store4<float>(float* dst, const float* v) {
 }
 
 constexpr int kMaxDT = kMaxHeadDim / 16;  // 16-wide d tiles
-constexpr int kMaxDC = kMaxHeadDim / 32;  // 32-deep d chunks
 
-template <class T>
+// Loads below are unconditional with clamped addresses (out-of-range values
+// are zeroed by selects afterwards), so the wait before each MFMA covers only
+// the loads it needs.
+
+// K operands of one 32-key block: tile t holds keys kb*32 + 16t + (lane%16).
+template <class T, int NDC>
+__device__ __forceinline__ void load_kblock(V8<T> (&kop)[2][NDC], const T* kbase, int kb, int N, int dh,
+                                            int g, int n) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int key = kb * 32 + 16 * t + n;
+    const int kc = min(key, N - 1);
+#pragma unroll
+    for (int c = 0; c < NDC; ++c) {
+      const int dd = 32 * c + 8 * g;
+      kop[t][c].load(kbase + (size_t)kc * dh + (dd < dh ? dd : 0));
+      if (key >= N || dd >= dh) kop[t][c].zero();
+    }
+  }
+}
+
+// V^T operands of one 32-key block: d tile t, row d = 16t + (lane%16).
+template <class T, int NDT>
+__device__ __forceinline__ void load_vblock(V8<T> (&vop)[NDT], const T* vbase, int kb, int N, int dh, int Npad,
+                                            int g, int n) {
+#pragma unroll
+  for (int t = 0; t < NDT; ++t) {
+    const int d = 16 * t + n;
+    load_v<T>(vop[t], vbase + (size_t)min(d, dh - 1) * Npad, kb * 32 + 4 * g, N);
+    if (d >= dh) vop[t].zero();
+  }
+}
+
+template <class T, int NDC, int NDT>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
-  __shared__ int s_off[kMaxViews + 1];
   __shared__ float s_m[4][16], s_l[4][16];
-  __shared__ f32x4_t s_o[4][kMaxDT][64];
+  __shared__ f32x4_t s_o[4][NDT][64];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, n = lane & 15;
   const int h = blockIdx.y, v = blockIdx.z;
-  row_offsets(a.rm, s_off);
-  const int kv = s_off[v + 1] - s_off[v];
-  const int rowbase = s_off[v];
+  const int rowbase = a.meta->off[v];
+  const int kv = a.meta->off[v + 1] - rowbase;
   const int qt = a.split == 4 ? (int)blockIdx.x : (int)blockIdx.x * 4 + w;
   const int q0 = qt * 16;
   if (a.split == 4 && q0 >= kv) return;
   const bool active = q0 < kv;
   const int N = a.sh.N, Npad = a.sh.Npad, dh = a.sh.dh, D = a.sh.D;
-  const int ndc = (dh + 31) / 32, ndt = (dh + 15) / 16;
   const T* kbase = reinterpret_cast<const T*>(a.caches.p[v] + a.cl.k + (size_t)a.layer * a.cl.kv_layer) +
                    (size_t)h * Npad * dh;
   const T* vbase = reinterpret_cast<const T*>(a.caches.p[v] + a.cl.v + (size_t)a.layer * a.cl.kv_layer) +
                    (size_t)h * dh * Npad;
   const T* Q = static_cast<const T*>(a.q);
-
-  const int qrow = q0 + n;
-  V8<T> qop[kMaxDC];
-#pragma unroll
-  for (int c = 0; c < kMaxDC; ++c) {
-    qop[c].zero();
-    if (c < ndc && active && qrow < kv && 32 * c + 8 * g < dh)
-      qop[c].load(Q + (size_t)(rowbase + qrow) * D + h * dh + 32 * c + 8 * g);
-  }
 
   const int nkb = (N + 31) / 32;
   int kb0 = 0, kb1 = nkb;
@@ -116,27 +136,38 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
   if (!active) kb1 = kb0;
 
-  float m_run = -INFINITY, l_run = 0.0f;
-  f32x4_t o[kMaxDT];
+  // one batch: Q, and K/V of the first key block
+  const int qrow = q0 + n;
+  const bool qok = active && qrow < kv;
+  const int qr = min(max(rowbase + min(qrow, kv - 1), 0), a.qmax);
+  V8<T> qop[NDC];
 #pragma unroll
-  for (int t = 0; t < kMaxDT; ++t) o[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int c = 0; c < NDC; ++c) {
+    const int dd = 32 * c + 8 * g;
+    qop[c].load(Q + (size_t)qr * D + h * dh + (dd < dh ? dd : 0));
+    if (!qok || dd >= dh) qop[c].zero();
+  }
+  V8<T> kop[2][NDC], vop[NDT];
+  load_kblock<T, NDC>(kop, kbase, min(kb0, nkb - 1), N, dh, g, n);
+  load_vblock<T, NDT>(vop, vbase, min(kb0, nkb - 1), N, dh, Npad, g, n);
+
+  float m_run = -INFINITY, l_run = 0.0f;
+  f32x4_t o[NDT];
+#pragma unroll
+  for (int t = 0; t < NDT; ++t) o[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
   for (int kb = kb0; kb < kb1; ++kb) {
+    V8<T> kn[2][NDC], vn[NDT];
+    // next block in flight while this one computes (past the end: a repeat)
+    load_kblock<T, NDC>(kn, kbase, min(kb + 1, nkb - 1), N, dh, g, n);
+    load_vblock<T, NDT>(vn, vbase, min(kb + 1, nkb - 1), N, dh, Npad, g, n);
     const int kbase0 = kb * 32;
     f32x4_t st[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       st[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-      const int key = kbase0 + 16 * t + n;
 #pragma unroll
-      for (int c = 0; c < kMaxDC; ++c) {
-        if (c < ndc) {
-          V8<T> kop;
-          kop.zero();
-          if (key < N && 32 * c + 8 * g < dh) kop.load(kbase + (size_t)key * dh + 32 * c + 8 * g);
-          mma(st[t], kop, qop[c]);
-        }
-      }
+      for (int c = 0; c < NDC; ++c) mma(st[t], kop[t][c], qop[c]);
     }
     // st[t][i] = score of key kbase0 + 16t + 4g + i for query n
     float s[8];
@@ -162,21 +193,20 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       psum += p[j];
     }
     l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int t = 0; t < kMaxDT; ++t) o[t] *= alpha;
     V8<T> pop;
     pack_p(pop, p);
 #pragma unroll
-    for (int t = 0; t < kMaxDT; ++t) {
-      if (t < ndt) {
-        const int d = 16 * t + n;
-        V8<T> vop;
-        vop.zero();
-        if (d < dh) load_v<T>(vop, vbase + (size_t)d * Npad, kbase0 + 4 * g, N);
-        mma(o[t], vop, pop);
-      }
+    for (int t = 0; t < NDT; ++t) {
+      o[t] *= alpha;
+      mma(o[t], vop[t], pop);
     }
     m_run = m_new;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int c = 0; c < NDC; ++c) kop[t][c] = kn[t][c];
+#pragma unroll
+    for (int t = 0; t < NDT; ++t) vop[t] = vn[t];
   }
 
   float l_tot = l_run + __shfl_xor(l_run, 16, 64);
@@ -188,8 +218,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       s_l[w][n] = l_tot;
     }
 #pragma unroll
-    for (int t = 0; t < kMaxDT; ++t)
-      if (t < ndt) s_o[w][t][lane] = o[t];
+    for (int t = 0; t < NDT; ++t) s_o[w][t][lane] = o[t];
     __syncthreads();
     if (w != 0) return;
     float mm = -INFINITY;
@@ -203,13 +232,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       l_tot += f[ww] * s_l[ww][n];
     }
 #pragma unroll
-    for (int t = 0; t < kMaxDT; ++t) {
-      if (t < ndt) {
-        f32x4_t acc = s_o[0][t][lane] * f[0];
+    for (int t = 0; t < NDT; ++t) {
+      f32x4_t acc = s_o[0][t][lane] * f[0];
 #pragma unroll
-        for (int ww = 1; ww < 4; ++ww) acc += s_o[ww][t][lane] * f[ww];
-        o[t] = acc;
-      }
+      for (int ww = 1; ww < 4; ++ww) acc += s_o[ww][t][lane] * f[ww];
+      o[t] = acc;
     }
   }
 
@@ -217,9 +244,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const float inv = 1.0f / l_tot;
   T* out = static_cast<T*>(a.o) + (size_t)(rowbase + qrow) * D + h * dh;
 #pragma unroll
-  for (int t = 0; t < kMaxDT; ++t) {
+  for (int t = 0; t < NDT; ++t) {
     const int d0 = 16 * t + 4 * g;
-    if (t < ndt && d0 < dh) {
+    if (d0 < dh) {
       float r[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) r[i] = o[t][i] * inv;
@@ -228,12 +255,26 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
+template <class T, int NDC, int NDT>
+static void launch_t(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  hipLaunchKernelGGL((attn_kernel<T, NDC, NDT>), grid, dim3(256), 0, s, a);
+}
+
+template <class T>
+static void launch_dh(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  const int dh = a.sh.dh;
+  if (dh <= 32) launch_t<T, 1, 2>(a, grid, s);
+  else if (dh <= 64) launch_t<T, 2, 4>(a, grid, s);
+  else if (dh <= 96) launch_t<T, 3, 6>(a, grid, s);
+  else launch_t<T, 4, 8>(a, grid, s);
+}
+
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s) {
   const int qtiles = (max_rows_per_view + 15) / 16;
-  dim3 grid(a.split == 4 ? qtiles : (qtiles + 3) / 4, a.sh.H, a.rm.B);
+  dim3 grid(a.split == 4 ? qtiles : (qtiles + 3) / 4, a.sh.H, a.B);
   if (grid.x == 0) return hipSuccess;
-  if (a.sh.dtype) hipLaunchKernelGGL(attn_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(attn_kernel<float>, grid, dim3(256), 0, s, a);
+  if (a.sh.dtype) launch_dh<uint16_t>(a, grid, s);
+  else launch_dh<float>(a, grid, s);
   return hipGetLastError();
 }
 

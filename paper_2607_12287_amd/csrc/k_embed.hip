@@ -14,7 +14,8 @@
 namespace incvit {
 
 // Workgroup: 16 tokens x 64 columns; wave w computes tokens 4w..4w+3 of the
-// tile, lane = column.  k is staged through LDS in tiles of 64.
+// tile, lane = column.  k is staged through LDS in tiles of 64; the next
+// tile's global loads are issued before the current tile is computed.
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   __shared__ __align__(16) float sx[64][16];  // [k][token]
   __shared__ __align__(16) float sw[64][64];  // [k][column]
@@ -31,30 +32,51 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   }
 
   const int d = c0 + lane;
-  float acc[4];
-  const float bias = d < D ? a.b_pe[d] : 0.0f;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) acc[r] = bias;
-
   const float* xp = a.patches + (size_t)v * N * P;
-  for (int kt = 0; kt < P; kt += 64) {
-    for (int e = tid; e < 16 * 64; e += 256) {
-      const int t = e >> 6, kk = e & 63;
-      const int tok = tok0 + t, k = kt + kk;
-      sx[kk][t] = (tok < N && k < P) ? xp[(size_t)tok * P + k] : 0.0f;
+  // this thread's share of a tile: 4 patch values and 16 weights
+  float rx[4], rw[16];
+  auto fetch = [&](int kt) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j, t = e >> 6, k = kt + (e & 63), tok = tok0 + t;
+      rx[j] = (tok < N && k < P) ? xp[(size_t)tok * P + k] : 0.0f;
     }
-    for (int e = tid; e < 64 * 64; e += 256) {
-      const int kk = e >> 6, cc = e & 63;
-      const int k = kt + kk, col = c0 + cc;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int e = tid + 256 * j, k = kt + (e >> 6), col = c0 + (e & 63);
       float wv = 0.0f;
       if (k < P && col < D) {
         const size_t i = (size_t)k * D + col;
         wv = a.dtype ? bf2f(static_cast<const uint16_t*>(a.w_pe)[i]) : static_cast<const float*>(a.w_pe)[i];
       }
-      sw[kk][cc] = wv;
+      rw[j] = wv;
+    }
+  };
+  float acc[4];
+  const float bias = d < D ? a.b_pe[d] : 0.0f;
+  float posv[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    acc[r] = bias;
+    const int tok = tok0 + 4 * w + r;
+    posv[r] = (tok < N && d < D) ? a.pos[(size_t)tok * D + d] : 0.0f;
+  }
+  fetch(0);
+  for (int kt = 0; kt < P; kt += 64) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j;
+      sx[e & 63][e >> 6] = rx[j];
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int e = tid + 256 * j;
+      sw[e >> 6][e & 63] = rw[j];
     }
     __syncthreads();
+    if (kt + 64 < P) fetch(kt + 64);  // in flight while this tile computes
     const int kmax = min(64, P - kt);
+#pragma unroll 8
     for (int kk = 0; kk < kmax; ++kk) {
       const float wv = sw[kk][lane];
       const float4 xv = *reinterpret_cast<const float4*>(&sx[kk][4 * w]);
@@ -69,12 +91,12 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int tok = tok0 + 4 * w + r;
-      if (tok < N) a.t0[((size_t)v * N + tok) * D + d] = __fadd_rn(acc[r], a.pos[(size_t)tok * D + d]);
+      if (tok < N) a.t0[((size_t)v * N + tok) * D + d] = __fadd_rn(acc[r], posv[r]);
     }
   }
 }
 
-// One wave per token: cos(T0[v][i], ref[v][i]).
+// One wave per token: cos(T0[v][i], ref[v][i]); the wave's loads go out in one batch.
 __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gt = blockIdx.x * 4 + w;
@@ -82,12 +104,22 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
   const int v = gt / a.N, tok = gt - v * a.N;
   const float* x = a.t0 + (size_t)gt * a.D;
   const float* y = reinterpret_cast<const float*>(a.caches.p[v] + a.ref_off) + (size_t)tok * a.D;
+  constexpr int kPer = kMaxDim / 64;
+  float xv[kPer], yv[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int d = lane + 64 * j;
+    xv[j] = d < a.D ? x[d] : 0.0f;
+    yv[j] = d < a.D ? y[d] : 0.0f;
+  }
   float pd = 0.0f, pa = 0.0f, pb = 0.0f;
-  for (int d = lane; d < a.D; d += 64) {
-    const float xv = x[d], yv = y[d];
-    pd = __fmaf_rn(xv, yv, pd);
-    pa = __fmaf_rn(xv, xv, pa);
-    pb = __fmaf_rn(yv, yv, pb);
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {  // d = lane + 64 j in increasing d; zero pads add nothing
+    if (lane + 64 * j < a.D) {
+      pd = __fmaf_rn(xv[j], yv[j], pd);
+      pa = __fmaf_rn(xv[j], xv[j], pa);
+      pb = __fmaf_rn(yv[j], yv[j], pb);
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {

@@ -5,13 +5,23 @@
 //   OPROJ: H = X^l[U] + (O W_o + b_o)            (fp32)
 //   FC1 : G = S(GELU(S(LN2(H)) W_1 + b_1))
 //   FC2 : X^{l+1}[U] = S(H + (G W_2 + b_2))      scattered into the cache.
-// Only the rows of U (M rows over all streams) are computed: with M small the
-// work is streaming the weights from HBM, so each workgroup reads its weight
-// columns exactly once, straight into MFMA operand registers (the packed
-// layout makes every 32-deep chunk one vector load per lane), while the M
-// activation rows sit in LDS.  K is split over the 4 waves and, when asked,
-// over workgroups; partial sums are combined in a fixed order (no float
-// atomics), so results are deterministic.
+//
+// Only the rows of U (M rows over all streams) are computed.  With M small
+// the time is set by memory latency, not bandwidth, so the kernel is laid out
+// as a fixed number of dependent load batches:
+//   1. the first weight chunks (straight into MFMA operand registers: the
+//      packed layout makes a 32-deep chunk one vector load per lane), M, and
+//      the LayerNorm parameters;
+//   2. the row map, the per-row LayerNorm partials (sum, sum of squares) that
+//      the producing kernel wrote in its epilogue, the compact A rows, and the
+//      compact residual of FC2;
+//   3. the rows gathered from the caches (QKV's A, OPROJ's residual);
+// then the MFMA loop with a prefetch ring, a fixed-order reduction of the
+// waves' partial tiles through LDS, and the stores.  Nothing is summed with
+// atomics, so results are deterministic.
+//
+// Grid: one workgroup per 16-column block of the output; it loops over the M
+// rows in blocks of 64; its NW waves take every NW-th 32-deep K chunk.
 #include "common.hpp"
 
 namespace incvit {
@@ -21,261 +31,335 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   return 0.5f * x * (1.0f + tanhf(u));
 }
 
-template <class T, int EPI>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a) {
+// A-operand element type: H is fp32, everything else is the storage dtype.
+template <class T, int EPI> struct AType { using type = T; };
+template <class T> struct AType<T, EPI_FC1> { using type = float; };
+
+// Normalise 8 A values (one lane's share of a 32-deep chunk) to the storage type.
+__device__ __forceinline__ void ln8(V8<uint16_t>& out, const float* x, float mean, float rstd,
+                                    const float* g, const float* b) {
+  uint32_t q[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float y0 = (x[2 * e] - mean) * rstd * g[2 * e] + b[2 * e];
+    const float y1 = (x[2 * e + 1] - mean) * rstd * g[2 * e + 1] + b[2 * e + 1];
+    q[e] = (uint32_t)f2bf(y0) | ((uint32_t)f2bf(y1) << 16);
+  }
+  out.v = make_uint4(q[0], q[1], q[2], q[3]);
+}
+__device__ __forceinline__ void ln8(V8<float>& out, const float* x, float mean, float rstd,
+                                    const float* g, const float* b) {
+  float y[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) y[e] = (x[e] - mean) * rstd * g[e] + b[e];
+  out.a = make_float4(y[0], y[1], y[2], y[3]);
+  out.b = make_float4(y[4], y[5], y[6], y[7]);
+}
+
+__device__ __forceinline__ void unpack8(float* x, const V8<uint16_t>& v) {
+  const uint32_t q[4] = {v.v.x, v.v.y, v.v.z, v.v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(q[e] << 16);
+    x[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void unpack8(float* x, const V8<float>& v) {
+  x[0] = v.a.x; x[1] = v.a.y; x[2] = v.a.z; x[3] = v.a.w;
+  x[4] = v.b.x; x[5] = v.b.y; x[6] = v.b.z; x[7] = v.b.w;
+}
+
+template <class T, int EPI, int NW>
+__global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
   constexpr bool kLN = (EPI == EPI_QKV || EPI == EPI_FC1);
-  constexpr int PF = sizeof(T) == 2 ? 8 : 4;  // weight chunks in flight per wave
-  constexpr int EB = sizeof(T);
+  using TA = typename AType<T, EPI>::type;
+  constexpr int PF = (sizeof(TA) == 4 || NW >= 16) ? 2 : 4;  // chunks in flight per wave
+  constexpr int RT = 4;                                       // 16-row tiles per row block
+  constexpr int NT = NW * 64;
+  constexpr int kGB = (kMaxDim + NT - 1) / NT;                // LN parameters per thread
+  constexpr int kJ = (kMaxStat + NW - 1) / NW;                // LN partials per thread
   extern __shared__ __align__(16) char smem[];
-  __shared__ int s_off[kMaxViews + 1];
-  __shared__ int s_view[kGemmRows], s_tok[kGemmRows];
-  __shared__ int s_last;
+  __shared__ RowInfo s_rows[kGemmRows];
+  __shared__ float s_mean[kGemmRows], s_rstd[kGemmRows];
+  __shared__ int s_m;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, n = lane & 15;
-  const int cb = blockIdx.x, m0 = blockIdx.y * kGemmRows, z = blockIdx.z;
-  const int M = row_offsets(a.rm, s_off);
-  if (m0 >= M) return;
-  const int mrows = min(kGemmRows, M - m0);
-  const int nrt = (mrows + 15) >> 4;
-  if (tid < kGemmRows) {
-    int v = 0, tok = 0;
-    if (tid < mrows) row_token(a.rm, s_off, m0 + tid, v, tok);
-    s_view[tid] = v;
-    s_tok[tid] = tok;
-  }
-
-  // K chunks of this workgroup, and every 4th of them for this wave.
-  const int kc0 = (int)((long)z * a.kchunks / a.ksplit);
-  const int kc1 = (int)((long)(z + 1) * a.kchunks / a.ksplit);
-  const int nw = max(0, (kc1 - kc0 - w + kGemmWaves - 1) / kGemmWaves);
+  const int cb = blockIdx.x;
+  const int D = a.sh.D;
+  const int col = cb * 16 + n;
+  const int nw = max(0, (a.kchunks - w + NW - 1) / NW);
   const T* wbase = static_cast<const T*>(a.W) + (size_t)cb * a.kchunks * kChunkElems + lane * 8;
+  float* s_g = reinterpret_cast<float*>(smem + NW * RT * 64 * 16);
+  float* s_b = s_g + D;
 
+  // ---- batch 1: weights, M, LayerNorm parameters
+  // Every load below is issued unconditionally (addresses clamped into range),
+  // so each loop iteration issues a fixed number of loads and the wait before
+  // an MFMA covers only the loads it needs, not the prefetches behind them.
+  const int kclamp = a.kchunks - 1;
+  auto chunk = [&](int i) { return min(w + NW * i, kclamp); };
   V8<T> wb[PF];
 #pragma unroll
-  for (int s = 0; s < PF; ++s)
-    if (s < nw) wb[s].load(wbase + (size_t)(kc0 + w + kGemmWaves * s) * kChunkElems);
-  __syncthreads();
-
-  // Stage this workgroup's A block (mrows x [klo, klo+kwid)) in LDS.
-  const int D = a.sh.D;
-  const int klo = kc0 * 32, kwid = (kc1 - kc0) * 32;
-  const int ldsb = kwid * EB + 16;  // row stride in bytes (+16: no bank conflicts)
+  for (int s = 0; s < PF; ++s) wb[s].load(wbase + (size_t)chunk(s) * kChunkElems);
+  if (tid == 0) s_m = a.meta->m;
   if constexpr (kLN) {
-    constexpr int kG = kMaxDim / 512;  // 8-element groups per lane
-    for (int rl = w; rl < mrows; rl += kGemmWaves) {
-      float x[kG][8];
+    float gv[kGB], bv[kGB];
 #pragma unroll
-      for (int j = 0; j < kG; ++j) {
-        const int d = 8 * lane + 512 * j;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[j][e] = 0.0f;
-        if (d < D) {
-          if constexpr (EPI == EPI_QKV) {
-            const T* src = x_row<T>(a.caches, a.cl, a.sh, s_view[rl], a.layer, s_tok[rl]) + d;
-            V8<T> t;
-            t.load(src);
-            if constexpr (sizeof(T) == 2) {
-              const uint32_t q[4] = {t.v.x, t.v.y, t.v.z, t.v.w};
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                x[j][2 * e] = __uint_as_float(q[e] << 16);
-                x[j][2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
-              }
-            } else {
-              x[j][0] = t.a.x; x[j][1] = t.a.y; x[j][2] = t.a.z; x[j][3] = t.a.w;
-              x[j][4] = t.b.x; x[j][5] = t.b.y; x[j][6] = t.b.z; x[j][7] = t.b.w;
-            }
-          } else {
-            const float4* src = reinterpret_cast<const float4*>(
-                static_cast<const float*>(a.A) + (size_t)(m0 + rl) * a.lda + d);
-            const float4 p0 = src[0], p1 = src[1];
-            x[j][0] = p0.x; x[j][1] = p0.y; x[j][2] = p0.z; x[j][3] = p0.w;
-            x[j][4] = p1.x; x[j][5] = p1.y; x[j][6] = p1.z; x[j][7] = p1.w;
-          }
-        }
-      }
-      float s = 0.0f;
-#pragma unroll
-      for (int j = 0; j < kG; ++j)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s += x[j][e];
-      const float mean = wave_sum(s) / (float)D;
-      float q = 0.0f;
-#pragma unroll
-      for (int j = 0; j < kG; ++j) {
-        if (8 * lane + 512 * j < D) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float c = x[j][e] - mean;
-            q += c * c;
-          }
-        }
-      }
-      const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + a.sh.eps);
-      char* row = smem + rl * ldsb;
-#pragma unroll
-      for (int j = 0; j < kG; ++j) {
-        const int d = 8 * lane + 512 * j;
-        if (d < D && d >= klo && d < klo + kwid) {
-          T* dst = reinterpret_cast<T*>(row + (d - klo) * EB);
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            dst[e] = Elem<T>::cv((x[j][e] - mean) * rstd * a.ln_g[d + e] + a.ln_b[d + e]);
-        }
-      }
+    for (int j = 0; j < kGB; ++j) {
+      const int k = tid + NT * j;
+      gv[j] = k < D ? a.ln_g[k] : 0.0f;
+      bv[j] = k < D ? a.ln_b[k] : 0.0f;
     }
-  } else {
-    // plain copy of the compact rows, 8 elements (one MFMA operand) at a time
-    const int groups = kwid / 8;
-    for (int rl = w; rl < mrows; rl += kGemmWaves) {
-      const T* src = static_cast<const T*>(a.A) + (size_t)(m0 + rl) * a.lda + klo;
-      char* row = smem + rl * ldsb;
-      for (int e = lane; e < groups; e += 64) {
-        V8<T> t;
-        t.load(src + 8 * e);
-        *reinterpret_cast<V8<T>*>(row + 8 * e * EB) = t;
+#pragma unroll
+    for (int j = 0; j < kGB; ++j) {
+      const int k = tid + NT * j;
+      if (k < D) {
+        s_g[k] = gv[j];
+        s_b[k] = bv[j];
       }
     }
   }
+  const float bias = a.bias[col];
   __syncthreads();
+  const int M = s_m;
 
-  f32x4_t acc[4];
+  V8<TA> ab[PF][RT];
+  const TA* ap[RT];
+  for (int m0 = 0; m0 < M; m0 += kGemmRows) {
+    const int mrows = min(kGemmRows, M - m0);
+    const int nrt = (mrows + 15) >> 4;
+    const int rt = w;  // the row tile this wave finishes
+    // ---- batch 2: row map, LayerNorm partials, compact rows
+    if (tid < kGemmRows) s_rows[tid] = a.rows[m0 + min(tid, mrows - 1)];
+    if (m0 > 0) {
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt) acc[rt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  for (int i0 = 0; i0 < nw; i0 += PF) {
+      for (int s = 0; s < PF; ++s) wb[s].load(wbase + (size_t)chunk(s) * kChunkElems);
+    }
+    float2 part = make_float2(0.0f, 0.0f);
+    const int srow = tid / NW, sq = tid % NW;  // NW threads (adjacent lanes) per row
+    if constexpr (kLN) {
+      float2 pv[kJ];
+      const float2* sp = a.stats_in + (size_t)(m0 + min(srow, mrows - 1)) * a.stat_stride;
 #pragma unroll
-    for (int s = 0; s < PF; ++s) {
-      const int i = i0 + s;
-      if (i < nw) {
-        const int kc = kc0 + w + kGemmWaves * i;
-        const char* abase = smem + n * ldsb + ((kc - kc0) * 32 + 8 * g) * EB;
+      for (int jj = 0; jj < kJ; ++jj) pv[jj] = sp[min(sq + NW * jj, a.nstat - 1)];
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-          if (rt < nrt) {
-            V8<T> av = *reinterpret_cast<const V8<T>*>(abase + 16 * rt * ldsb);
-            mma(acc[rt], av, wb[s]);
-          }
+      for (int jj = 0; jj < kJ; ++jj) {
+        if (sq + NW * jj < a.nstat) {
+          part.x += pv[jj].x;
+          part.y += pv[jj].y;
         }
-        if (i + PF < nw) wb[s].load(wbase + (size_t)(kc + kGemmWaves * PF) * kChunkElems);
       }
     }
-  }
-
-  // Sum the 4 waves' partial tiles in wave order; wave w finishes row tile w.
-  __syncthreads();
-  f32x4_t* red = reinterpret_cast<f32x4_t*>(smem);
+    if constexpr (EPI != EPI_QKV) {
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
-    if (rt < nrt) red[(w * 4 + rt) * 64 + lane] = acc[rt];
-  __syncthreads();
-  const int rt = w;
-  f32x4_t val = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  if (rt < nrt) {
-    val = red[(0 * 4 + rt) * 64 + lane];
+      for (int r = 0; r < RT; ++r)
+        ap[r] = static_cast<const TA*>(a.A) + (size_t)(m0 + min(16 * r + n, mrows - 1)) * a.lda + 8 * g;
 #pragma unroll
-    for (int ww = 1; ww < kGemmWaves; ++ww) val += red[(ww * 4 + rt) * 64 + lane];
-  }
-  const int col = cb * 16 + n;
-
-  if (a.ksplit > 1) {
-    // Partial tile to global; the last workgroup of this tile adds all splits
-    // in split order and runs the epilogue; it then re-arms the counter.
-    if (rt < nrt) {
+      for (int s = 0; s < PF; ++s)
+#pragma unroll
+        for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + chunk(s) * 32);
+    }
+    float res[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // epilogue residual of this lane's 4 rows
+    if constexpr (EPI == EPI_FC2) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        res[i] = a.hres[(size_t)(m0 + min(16 * min(rt, RT - 1) + 4 * g + i, mrows - 1)) * D + col];
+    }
+    __syncthreads();  // s_rows
+    // ---- batch 3: rows gathered from the caches
+    if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        const RowInfo ri = s_rows[min(16 * r + n, mrows - 1)];
+        ap[r] = x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok) + 8 * g;
+      }
+#pragma unroll
+      for (int s = 0; s < PF; ++s)
+#pragma unroll
+        for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + chunk(s) * 32);
+    }
+    if constexpr (EPI == EPI_OPROJ) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = m0 + 16 * rt + 4 * g + i;
-        a.partial[((size_t)z * a.Mpad + row) * a.Nout + col] = val[i];
+        const RowInfo ri = s_rows[min(16 * min(rt, RT - 1) + 4 * g + i, mrows - 1)];
+        res[i] = Elem<T>::f(gbl(x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok))[col]);
       }
     }
-    __threadfence();
-    __syncthreads();
-    int* ctr = a.counters + blockIdx.y * gridDim.x + cb;
-    if (tid == 0) {
-      const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (prev == a.ksplit - 1);
+    // ---- LayerNorm statistics of the block's rows (fixed-order reduction)
+    if constexpr (kLN) {
+#pragma unroll
+      for (int off = NW / 2; off >= 1; off >>= 1) {
+        part.x += __shfl_xor(part.x, off, NW);
+        part.y += __shfl_xor(part.y, off, NW);
+      }
+      if (sq == 0 && srow < mrows) {
+        const float mean = part.x / (float)D;
+        const float var = fmaxf(part.y / (float)D - mean * mean, 0.0f);
+        s_mean[srow] = mean;
+        s_rstd[srow] = 1.0f / sqrtf(var + a.sh.eps);
+      }
+      __syncthreads();
     }
+    float rmean[RT], rrstd[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const int rl = min(16 * r + n, mrows - 1);
+      rmean[r] = kLN ? s_mean[rl] : 0.0f;
+      rrstd[r] = kLN ? s_rstd[rl] : 0.0f;
+    }
+
+    // ---- MFMA over this wave's chunks
+    f32x4_t acc[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) acc[r] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i0 = 0; i0 < nw; i0 += PF) {
+#pragma unroll
+      for (int s = 0; s < PF; ++s) {
+        const int i = i0 + s;
+        if (i < nw) {  // uniform; no memory operation inside
+          const int kc = w + NW * i;
+          float gg[8], bb[8];
+          if constexpr (kLN) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              gg[e] = s_g[kc * 32 + 8 * g + e];
+              bb[e] = s_b[kc * 32 + 8 * g + e];
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < RT; ++r) {
+            if (r < nrt) {
+              if constexpr (kLN) {
+                float x[8];
+                unpack8(x, ab[s][r]);
+                V8<T> av;
+                ln8(av, x, rmean[r], rrstd[r], gg, bb);
+                mma(acc[r], av, wb[s]);
+              } else {
+                mma(acc[r], ab[s][r], wb[s]);
+              }
+            }
+          }
+        }
+        const int kn = chunk(i + PF);
+        wb[s].load(wbase + (size_t)kn * kChunkElems);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + kn * 32);
+      }
+    }
+
+    // ---- sum the waves' partial tiles in wave order; wave w finishes row tile w
+    f32x4_t* red = reinterpret_cast<f32x4_t*>(smem);
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+      if (r < nrt) red[(w * RT + r) * 64 + lane] = acc[r];
     __syncthreads();
-    if (!s_last) return;
-    __threadfence();
     if (rt < nrt) {
-      val = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-      for (int zz = 0; zz < a.ksplit; ++zz) {
+      f32x4_t val = red[rt * 64 + lane];
+#pragma unroll
+      for (int ww = 1; ww < NW; ++ww) val += red[(ww * RT + rt) * 64 + lane];
+
+      // ---- epilogue: stores only
+      float y[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rl = 16 * rt + 4 * g + i;
+        const float x = val[i] + bias;
+        const RowInfo ri = s_rows[min(rl, mrows - 1)];
+        const bool ok = rl < mrows;
+        y[i] = 0.0f;
+        if constexpr (EPI == EPI_QKV) {
+          const int which = col / D, c = col - which * D;
+          const T o = Elem<T>::cv(x);
+          if (ok) {
+            if (which == 0) {
+              static_cast<T*>(a.out)[(size_t)(m0 + rl) * a.ldo + c] = o;
+            } else {
+              const int hh = c / a.sh.dh, d = c - hh * a.sh.dh;
+              char* base = ri.cache + (which == 1 ? a.cl.k : a.cl.v) + (size_t)a.layer * a.cl.kv_layer;
+              const size_t e = which == 1 ? ((size_t)hh * a.sh.Npad + ri.tok) * a.sh.dh + d
+                                          : ((size_t)hh * a.sh.dh + d) * a.sh.Npad + ri.tok;
+              gbl(reinterpret_cast<T*>(base))[e] = o;
+            }
+          }
+        } else if constexpr (EPI == EPI_OPROJ) {
+          y[i] = res[i] + x;
+          if (ok) static_cast<float*>(a.out)[(size_t)(m0 + rl) * a.ldo + col] = y[i];
+        } else if constexpr (EPI == EPI_FC1) {
+          if (ok) static_cast<T*>(a.out)[(size_t)(m0 + rl) * a.ldo + col] = Elem<T>::cv(gelu_tanh(x));
+        } else {
+          const T o = Elem<T>::cv(res[i] + x);
+          y[i] = Elem<T>::ld(&o, 0);
+          if (ok) gbl(x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok))[col] = o;
+        }
+      }
+      if constexpr (EPI == EPI_OPROJ || EPI == EPI_FC2) {
+        // per-row (sum, sum of squares) over this block's 16 columns: the
+        // LayerNorm statistics of the next GEMM, combined there in block order
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = m0 + 16 * rt + 4 * g + i;
-          val[i] += __hip_atomic_load(a.partial + ((size_t)zz * a.Mpad + row) * a.Nout + col,
-                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          float s1 = y[i], s2 = y[i] * y[i];
+#pragma unroll
+          for (int off = 8; off >= 1; off >>= 1) {
+            s1 += __shfl_xor(s1, off, 16);
+            s2 += __shfl_xor(s2, off, 16);
+          }
+          const int rl = 16 * rt + 4 * g + i;
+          if (n == 0 && rl < mrows) a.stats_out[(size_t)(m0 + rl) * a.stat_stride + cb] = make_float2(s1, s2);
         }
       }
     }
-    if (tid == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  if (rt >= nrt) return;
-
-  const float bias = a.bias[col];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rl = 16 * rt + 4 * g + i;
-    if (rl >= mrows) continue;
-    const float x = val[i] + bias;
-    const int v = s_view[rl], tok = s_tok[rl];
-    if constexpr (EPI == EPI_QKV) {
-      const int which = col / D, c = col - which * D;
-      const T o = Elem<T>::cv(x);
-      if (which == 0) {
-        static_cast<T*>(a.out)[(size_t)(m0 + rl) * a.ldo + c] = o;
-      } else {
-        const int hh = c / a.sh.dh, d = c - hh * a.sh.dh;
-        char* base = a.caches.p[v] + (which == 1 ? a.cl.k : a.cl.v) + (size_t)a.layer * a.cl.kv_layer;
-        const size_t e = which == 1 ? ((size_t)hh * a.sh.Npad + tok) * a.sh.dh + d
-                                    : ((size_t)hh * a.sh.dh + d) * a.sh.Npad + tok;
-        reinterpret_cast<T*>(base)[e] = o;
-      }
-    } else if constexpr (EPI == EPI_OPROJ) {
-      const float xin = Elem<T>::ld(x_row<T>(a.caches, a.cl, a.sh, v, a.layer, tok), col);
-      static_cast<float*>(a.out)[(size_t)(m0 + rl) * a.ldo + col] = xin + x;
-    } else if constexpr (EPI == EPI_FC1) {
-      static_cast<T*>(a.out)[(size_t)(m0 + rl) * a.ldo + col] = Elem<T>::cv(gelu_tanh(x));
-    } else {
-      const float hv = a.hres[(size_t)(m0 + rl) * D + col];
-      x_row<T>(a.caches, a.cl, a.sh, v, a.layer + 1, tok)[col] = Elem<T>::cv(hv + x);
-    }
+    __syncthreads();  // shared state reused by the next row block
   }
 }
 
-template <int EPI>
-static hipError_t launch_one(const GemmArgs& a, dim3 grid, size_t lds, hipStream_t s) {
-  if (a.sh.dtype) hipLaunchKernelGGL((gemm_kernel<uint16_t, EPI>), grid, dim3(256), lds, s, a);
-  else hipLaunchKernelGGL((gemm_kernel<float, EPI>), grid, dim3(256), lds, s, a);
+template <int NW>
+static size_t gemm_lds(const GemmArgs& a) {
+  return (size_t)NW * 4 * 64 * 16 + (size_t)2 * a.sh.D * sizeof(float);
+}
+
+// Allow each instantiation the largest dynamic LDS any shape needs, once.
+template <class T, int EPI, int NW>
+static hipError_t allow_lds() {
+  static hipError_t done = hipErrorNotReady;
+  if (done != hipSuccess) {
+    const int most = NW * 4 * 64 * 16 + 2 * kMaxDim * (int)sizeof(float);
+    done = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<T, EPI, NW>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, most);
+  }
+  return done;
+}
+
+template <int EPI, int NW>
+static hipError_t launch_nw(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid(a.Nout / 16);
+  const size_t lds = gemm_lds<NW>(a);
+  hipError_t e;
+  if (a.sh.dtype) {
+    if ((e = allow_lds<uint16_t, EPI, NW>()) != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_kernel<uint16_t, EPI, NW>), grid, dim3(NW * 64), lds, s, a);
+  } else {
+    if ((e = allow_lds<float, EPI, NW>()) != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_kernel<float, EPI, NW>), grid, dim3(NW * 64), lds, s, a);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(int epi, const GemmArgs& a, int mmax, size_t lds, hipStream_t s) {
-  dim3 grid(a.Nout / 16, (mmax + kGemmRows - 1) / kGemmRows, a.ksplit);
-  switch (epi) {
-    case EPI_QKV: return launch_one<EPI_QKV>(a, grid, lds, s);
-    case EPI_OPROJ: return launch_one<EPI_OPROJ>(a, grid, lds, s);
-    case EPI_FC1: return launch_one<EPI_FC1>(a, grid, lds, s);
-    default: return launch_one<EPI_FC2>(a, grid, lds, s);
-  }
-}
-
 template <int EPI>
-static hipError_t set_lds(size_t bytes) {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<uint16_t, EPI>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<float, EPI>),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+static hipError_t launch_epi(int waves, const GemmArgs& a, hipStream_t s) {
+  if (waves >= 16) return launch_nw<EPI, 16>(a, s);
+  if (waves >= 8) return launch_nw<EPI, 8>(a, s);
+  return launch_nw<EPI, 4>(a, s);
 }
 
-hipError_t gemm_set_lds_limits(size_t bytes) {
-  hipError_t e;
-  if ((e = set_lds<EPI_QKV>(bytes)) != hipSuccess) return e;
-  if ((e = set_lds<EPI_OPROJ>(bytes)) != hipSuccess) return e;
-  if ((e = set_lds<EPI_FC1>(bytes)) != hipSuccess) return e;
-  return set_lds<EPI_FC2>(bytes);
+hipError_t launch_gemm(int epi, int waves, const GemmArgs& a, hipStream_t s) {
+  switch (epi) {
+    case EPI_QKV: return launch_epi<EPI_QKV>(waves, a, s);
+    case EPI_OPROJ: return launch_epi<EPI_OPROJ>(waves, a, s);
+    case EPI_FC1: return launch_epi<EPI_FC1>(waves, a, s);
+    default: return launch_epi<EPI_FC2>(waves, a, s);
+  }
 }
 
 }  // namespace incvit

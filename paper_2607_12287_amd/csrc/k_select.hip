@@ -53,25 +53,34 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   const int v = blockIdx.x, tid = threadIdx.x, N = a.N;
   CacheHeader* hdr = reinterpret_cast<CacheHeader*>(a.caches.p[v]);
   if (tid == 0) {
-    s_misc[0] = (hdr->magic == kCacheMagic && hdr->hash == a.hash && hdr->status == 0) ? 1 : 0;
+    const CacheHeader h = *hdr;
+    s_misc[0] = (h.magic == kCacheMagic && h.hash == a.hash && h.status == 0) ? 1 : 0;
     s_misc[1] = 0;  // non-finite seen
     s_misc[2] = 0;  // candidates
   }
-  __syncthreads();
-  if (!s_misc[0]) {
-    if (tid == 0) a.count[v] = 0;
-    return;
-  }
-  // contiguous token segment per thread (keeps scans in index order)
+  // contiguous token segment per thread (keeps scans in index order); the
+  // segment's similarities are loaded in one batch
+  constexpr int kPer = kMaxTokens / kSelThreads;
   const int per = (N + kSelThreads - 1) / kSelThreads;
   const int i0 = min(N, tid * per), i1 = min(N, i0 + per);
+  float sv[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) sv[j] = (i0 + j < i1) ? a.sim[(size_t)v * N + i0 + j] : 0.0f;
   int cand = 0, bad = 0;
-  for (int i = i0; i < i1; ++i) {
-    const float s = a.sim[(size_t)v * N + i];
-    bad |= (s != s);
-    const bool f = s < a.tau;
-    skey[i] = f ? order_key(s) : 0xffffffffu;
-    cand += f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    if (i0 + j < i1) {
+      const float sj = sv[j];
+      bad |= (sj != sj);
+      const bool f = sj < a.tau;
+      skey[i0 + j] = f ? order_key(sj) : 0xffffffffu;
+      cand += f;
+    }
+  }
+  __syncthreads();
+  if (!s_misc[0]) {  // never encoded, or another model: this stream is a no-op
+    if (tid == 0) a.count[v] = 0;
+    return;
   }
   if (bad) atomicOr(&s_misc[1], 1);
   atomicAdd(&s_misc[2], cand);
@@ -173,53 +182,94 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   if (tid == 0) a.count[v] = total_sel;
 }
 
-// One wave per compact row: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]).
+// One wave per compact row: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]),
+// and the row's entry in the row map with its LayerNorm statistics.  Block 0
+// also publishes M and the per-stream row offsets.
 template <class T>
 __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
+  __shared__ int s_cnt[kMaxViews];
   __shared__ int s_off[kMaxViews + 1];
-  const int M = row_offsets(a.rm, s_off);
-  if (a.init_header && blockIdx.x == 0 && threadIdx.x < a.rm.B) {
-    CacheHeader* hdr = reinterpret_cast<CacheHeader*>(a.caches.p[threadIdx.x]);
-    hdr->magic = kCacheMagic;
-    hdr->hash = a.hash;
-    hdr->status = 0;
-    hdr->frames = 0;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int B = a.rm.B, N = a.rm.N, D = a.sh.D;
+  if (tid < B) s_cnt[tid] = a.rm.count[tid];
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int v = 0; v < B; ++v) {
+      s_off[v] = acc;
+      acc += s_cnt[v];
+    }
+    s_off[B] = acc;
   }
-  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  __syncthreads();
+  const int M = s_off[B];
+  if (blockIdx.x == 0) {
+    if (tid <= B) a.meta->off[tid] = s_off[tid];
+    if (tid == 0) a.meta->m = M;
+    if (a.init_header && tid < B) {
+      CacheHeader* hdr = reinterpret_cast<CacheHeader*>(a.caches.p[tid]);
+      hdr->magic = kCacheMagic;
+      hdr->hash = a.hash;
+      hdr->status = 0;
+      hdr->frames = 0;
+    }
+  }
+  const int r = blockIdx.x * 4 + (tid >> 6);
   if (r >= M) return;
-  int v, tok;
-  row_token(a.rm, s_off, r, v, tok);
-  const int D = a.sh.D;
-  const float* src = a.t0 + ((size_t)v * a.rm.N + tok) * D;
-  float* ref = reinterpret_cast<float*>(a.caches.p[v] + a.cl.ref) + (size_t)tok * D;
-  T* x0 = x_row<T>(a.caches, a.cl, a.sh, v, 0, tok);
-  for (int d = lane; d < D; d += 64) {
-    const float t = src[d];
-    ref[d] = t;
-    x0[d] = Elem<T>::cv(t);
+  int v = 0;
+  while (v + 1 < B && s_off[v + 1] <= r) ++v;
+  const int tok = a.rm.idx[v * N + (r - s_off[v])];
+  char* cache = a.caches.p[v];
+  const float* src = a.t0 + ((size_t)v * N + tok) * D;
+  constexpr int kPer = kMaxDim / 64;
+  float t[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) t[j] = (lane + 64 * j < D) ? src[lane + 64 * j] : 0.0f;
+  float* ref = reinterpret_cast<float*>(cache + a.cl.ref) + (size_t)tok * D;
+  T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
+  float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int d = lane + 64 * j;
+    if (d < D) {
+      const T o = Elem<T>::cv(t[j]);
+      ref[d] = t[j];
+      x0[d] = o;
+      const float q = Elem<T>::ld(&o, 0);
+      s1 += q;
+      s2 += q * q;
+    }
+  }
+  s1 = wave_sum(s1);
+  s2 = wave_sum(s2);
+  if (lane == 0) {
+    a.rows[r] = RowInfo{cache, tok, v};
+    a.stats[(size_t)r * a.stat_stride] = make_float2(s1, s2);
   }
 }
 
 // One wave per compact row: Y[tok] = S(LN_f(X^L[tok])); refreshed[v][j] = Y[tok].
 template <class T>
 __global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
-  __shared__ int s_off[kMaxViews + 1];
-  const int M = row_offsets(a.rm, s_off);
   const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int M = a.meta->m;
+  const RowInfo ri = a.rows[r];  // in bounds for every launched row; used only if r < M
   if (r >= M) return;
-  int v, tok;
-  row_token(a.rm, s_off, r, v, tok);
   const int D = a.sh.D;
-  const T* x = x_row<T>(a.caches, a.cl, a.sh, v, a.sh.L, tok);
+  const int j0 = r - a.meta->off[ri.view];
+  const INCVIT_GLOBAL T* x = gbl(x_row<T>(ri.cache, a.cl, a.sh, a.sh.L, ri.tok));
   constexpr int kMaxPer = kMaxDim / 64;
-  float vals[kMaxPer];
-  float s = 0.0f;
+  float vals[kMaxPer], gv[kMaxPer], bv[kMaxPer];
 #pragma unroll
   for (int j = 0; j < kMaxPer; ++j) {
     const int d = lane + 64 * j;
-    vals[j] = d < D ? Elem<T>::ld(x, d) : 0.0f;
-    s += vals[j];
+    vals[j] = d < D ? Elem<T>::f(x[d]) : 0.0f;
+    gv[j] = d < D ? a.g[d] : 0.0f;
+    bv[j] = d < D ? a.b[d] : 0.0f;
   }
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kMaxPer; ++j) s += vals[j];
   const float mean = wave_sum(s) / (float)D;
   float q = 0.0f;
 #pragma unroll
@@ -229,13 +279,13 @@ __global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
     q += d < D ? c * c : 0.0f;
   }
   const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + a.sh.eps);
-  T* y = reinterpret_cast<T*>(a.caches.p[v] + a.cl.y) + (size_t)tok * D;
-  T* out = a.refreshed ? reinterpret_cast<T*>(a.refreshed) + ((size_t)v * a.rm.N + (r - s_off[v])) * D : nullptr;
+  INCVIT_GLOBAL T* y = gbl(reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D);
+  T* out = a.refreshed ? reinterpret_cast<T*>(a.refreshed) + ((size_t)ri.view * a.rm.N + j0) * D : nullptr;
 #pragma unroll
   for (int j = 0; j < kMaxPer; ++j) {
     const int d = lane + 64 * j;
     if (d < D) {
-      const T o = Elem<T>::cv((vals[j] - mean) * rstd * a.g[d] + a.b[d]);
+      const T o = Elem<T>::cv((vals[j] - mean) * rstd * gv[j] + bv[j]);
       y[d] = o;
       if (out) out[d] = o;
     }

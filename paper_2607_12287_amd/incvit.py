@@ -27,7 +27,8 @@ EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "inc
            "incvit_create", "incvit_destroy", "incvit_cache_bytes", "incvit_cache_canonical_bytes",
            "incvit_workspace_bytes", "incvit_full_encode", "incvit_step", "incvit_cache_export",
            "incvit_cache_import", "incvit_cache_status", "incvit_last_error", "incvit_profile_enable",
-           "incvit_profile_read")
+           "incvit_profile_read", "incvit_step_graph_create", "incvit_full_graph_create",
+           "incvit_graph_launch", "incvit_graph_destroy", "incvit_set_tuning")
 
 
 class incvit_config(ctypes.Structure):
@@ -35,6 +36,10 @@ class incvit_config(ctypes.Structure):
                 ("patch", ctypes.c_int32), ("dim", ctypes.c_int32), ("depth", ctypes.c_int32),
                 ("heads", ctypes.c_int32), ("mlp_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("ln_eps", ctypes.c_float), ("max_streams", ctypes.c_int32)]
+
+
+class incvit_tuning(ctypes.Structure):
+    _fields_ = [("waves", ctypes.c_int32 * 4)]
 
 
 class IncvitError(RuntimeError):
@@ -71,6 +76,11 @@ def lib() -> ctypes.CDLL:
             "incvit_last_error": (ctypes.c_char_p, [P]),
             "incvit_profile_enable": (I32, [P, I32]),
             "incvit_profile_read": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), I32]),
+            "incvit_step_graph_create": (I32, [P, I32, P, P, F32, P, P, P, P, P, ctypes.POINTER(P)]),
+            "incvit_full_graph_create": (I32, [P, I32, P, P, P, ctypes.POINTER(P)]),
+            "incvit_graph_launch": (I32, [P, P]),
+            "incvit_graph_destroy": (None, [P]),
+            "incvit_set_tuning": (I32, [P, ctypes.POINTER(incvit_tuning)]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -163,6 +173,36 @@ def incvit_profile_read(h, reset: bool = True):
     n = (ctypes.c_int64 * len(KERNEL_KINDS))()
     _check(lib().incvit_profile_read(h, ms, n, 1 if reset else 0), h)
     return {k: (ms[i], n[i]) for i, k in enumerate(KERNEL_KINDS)}
+
+
+def incvit_step_graph_create(h, B: int, patches: int, caches: Sequence[int], tau: float, cap: Sequence[int],
+                             idx: int, count: int, refreshed: int, workspace: int):
+    caps = (ctypes.c_int32 * B)(*[int(c) for c in cap])
+    g = ctypes.c_void_p()
+    st = lib().incvit_step_graph_create(h, B, patches, _ptr_array(caches), float(tau), caps, idx, count,
+                                        refreshed, workspace, ctypes.byref(g))
+    return st, g
+
+
+def incvit_full_graph_create(h, B: int, patches: int, caches: Sequence[int], workspace: int):
+    g = ctypes.c_void_p()
+    st = lib().incvit_full_graph_create(h, B, patches, _ptr_array(caches), workspace, ctypes.byref(g))
+    return st, g
+
+
+def incvit_graph_launch(g, stream: int = 0) -> int:
+    return lib().incvit_graph_launch(g, stream)
+
+
+def incvit_graph_destroy(g) -> None:
+    lib().incvit_graph_destroy(g)
+
+
+def incvit_set_tuning(h, waves: Optional[Sequence[int]] = None) -> int:
+    if waves is None:
+        return lib().incvit_set_tuning(h, None)
+    t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in waves]))
+    return lib().incvit_set_tuning(h, ctypes.byref(t))
 
 
 # --- convenience wrapper -------------------------------------------------------
@@ -258,6 +298,29 @@ class Encoder:
                            refreshed.data_ptr() if refreshed is not None else 0, self.workspace(B).data_ptr(),
                            self.stream_ptr()), self.h)
         return idx, count, refreshed
+
+    def step_graph(self, patches, caches: Sequence[int], tau: float, cap: Sequence[int], out):
+        """Capture one step with fixed buffers; replay with launch(graph) after
+        writing the next frame into `patches`.  Destroy with drop_graph."""
+        idx, count, refreshed = out
+        st, g = incvit_step_graph_create(self.h, len(caches), patches.data_ptr(), caches, tau, cap, idx.data_ptr(),
+                                         count.data_ptr(), refreshed.data_ptr() if refreshed is not None else 0,
+                                         self.workspace(len(caches)).data_ptr())
+        _check(st, self.h)
+        return g
+
+    def full_graph(self, patches, caches: Sequence[int]):
+        st, g = incvit_full_graph_create(self.h, len(caches), patches.data_ptr(), caches,
+                                         self.workspace(len(caches)).data_ptr())
+        _check(st, self.h)
+        return g
+
+    def launch(self, graph):
+        _check(incvit_graph_launch(graph, self.stream_ptr()))
+
+    @staticmethod
+    def drop_graph(graph):
+        incvit_graph_destroy(graph)
 
     def export(self, cache: int) -> Dict[str, np.ndarray]:
         """Canonical copy of one cache as float64 numpy arrays: ref, X, K, V, Y."""
