@@ -195,11 +195,13 @@ void incvit_graph_destroy(incvit_graph* g);
 
 /* Performance knobs; every setting gives a deterministic result, and the
  * settings differ only in the order of fp32 partial sums.
- * waves[k]: waves per workgroup of GEMM k (0 = QKV, 1 = output projection,
- * 2 = MLP up, 3 = MLP down): 4, 8 or 16; 0 = automatic.  A NULL pointer
- * restores the defaults. */
+ * For GEMM k (0 = QKV, 1 = output projection, 2 = MLP up, 3 = MLP down):
+ * waves[k]: waves per workgroup, 4 or 8; cols[k]: 16-column blocks per
+ * workgroup, 1 or 2 (2 only when the block count is even); 0 = automatic.
+ * A NULL pointer restores the defaults. */
 typedef struct {
   int32_t waves[4];
+  int32_t cols[4];
 } incvit_tuning;
 
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);

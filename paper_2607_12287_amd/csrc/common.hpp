@@ -210,7 +210,7 @@ hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s);
-hipError_t launch_gemm(int epi, int waves, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm(int epi, int waves, int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);

@@ -189,13 +189,18 @@ GemmGeom gemm_geom(const Shape& sh, int kind) {
   return g;
 }
 
-// Waves per GEMM workgroup: 8 keeps enough loads in flight per CU without
-// register spills (16 waves cap a wave at 128 registers).
-int auto_waves(const GemmGeom&) { return 8; }
-
-int waves_of(const int* tuned, const GemmGeom& g, int kind) {
+// Waves per GEMM workgroup: 8 keeps enough loads in flight per CU.
+int waves_of(const int* tuned, const GemmGeom&, int kind) {
   const int t = tuned ? tuned[kind] : 0;
-  return t > 0 ? t : auto_waves(g);
+  return t > 0 ? t : 8;
+}
+
+// Column blocks per workgroup: outputs with more blocks than CUs take two per
+// workgroup (each A row is then read once for 32 columns).
+int cols_of(const int* tuned, const GemmGeom& g, int kind) {
+  const int t = tuned ? tuned[kind] : 0;
+  if (t > 0) return t;
+  return g.nblocks > 256 ? 2 : 1;
 }
 
 WsLayout ws_layout(const Shape& sh, int B) {
@@ -241,6 +246,7 @@ struct incvit_handle {
   double prof_ms[INCVIT_K_COUNT] = {};
   int64_t prof_n[INCVIT_K_COUNT] = {};
   int waves[4] = {0, 0, 0, 0};  // 0 = automatic
+  int cols[4] = {0, 0, 0, 0};   // 0 = automatic
 };
 
 struct incvit_graph {
@@ -340,7 +346,8 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           break;
       }
       const int waves = waves_of(h->waves, g, kind);
-      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, waves, a, s); });
+      const int cols = cols_of(h->cols, g, kind);
+      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, waves, cols, a, s); });
     };
 
     incvit_status st;
@@ -667,9 +674,13 @@ incvit_status incvit_profile_read(incvit_handle* h, double* total_ms, int64_t* l
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
   for (int k = 0; k < 4; ++k) {
-    const int v = t ? t->waves[k] : 0;
-    if (v != 0 && v != 4 && v != 8 && v != 16) return fail(h, INCVIT_ERR_ARG, "waves must be 0, 4, 8 or 16");
-    h->waves[k] = v;
+    const int v = t ? t->waves[k] : 0, c = t ? t->cols[k] : 0;
+    if (v != 0 && v != 4 && v != 8) return fail(h, INCVIT_ERR_ARG, "waves must be 0, 4 or 8");
+    if (c < 0 || c > 2) return fail(h, INCVIT_ERR_ARG, "cols must be 0, 1 or 2");
+  }
+  for (int k = 0; k < 4; ++k) {
+    h->waves[k] = t ? t->waves[k] : 0;
+    h->cols[k] = t ? t->cols[k] : 0;
   }
   return INCVIT_OK;
 }

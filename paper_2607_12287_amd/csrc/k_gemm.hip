@@ -7,21 +7,24 @@
 //   FC2 : X^{l+1}[U] = S(H + (G W_2 + b_2))      scattered into the cache.
 //
 // Only the rows of U (M rows over all streams) are computed.  With M small
-// the time is set by memory latency, not bandwidth, so the kernel is laid out
-// as a fixed number of dependent load batches:
-//   1. the first weight chunks (straight into MFMA operand registers: the
-//      packed layout makes a 32-deep chunk one vector load per lane), M, and
-//      the LayerNorm parameters;
-//   2. the row map, the per-row LayerNorm partials (sum, sum of squares) that
-//      the producing kernel wrote in its epilogue, the compact A rows, and the
-//      compact residual of FC2;
-//   3. the rows gathered from the caches (QKV's A, OPROJ's residual);
-// then the MFMA loop with a prefetch ring, a fixed-order reduction of the
-// waves' partial tiles through LDS, and the stores.  Nothing is summed with
-// atomics, so results are deterministic.
-//
-// Grid: one workgroup per 16-column block of the output; it loops over the M
-// rows in blocks of 64; its NW waves take every NW-th 32-deep K chunk.
+// the time is set by memory latency and by the traffic through each CU's load
+// path, not by HBM bandwidth, so:
+//   * the loads whose addresses are known first (M, the row map and the
+//     per-row LayerNorm partials of the first 64 rows) go out before anything
+//     else; the A rows and residuals follow; the bulk weight stream last;
+//   * weights come straight into MFMA operand registers: the packed layout
+//     makes one 32-deep chunk of a 16-column block one vector load per lane;
+//   * the number of 16-row tiles of a block is a template parameter chosen at
+//     run time, so a lane issues exactly the loads it needs, unconditionally
+//     (addresses clamped), and the wait before an MFMA covers only its own
+//     operands;
+//   * wide outputs give a workgroup two column blocks, so each A row is read
+//     once for 32 columns;
+//   * the LayerNorm of the A operand is applied in registers from per-row
+//     (sum, sum of squares) partials that the producing kernel wrote in its
+//     epilogue.
+// The waves' partial tiles are summed in a fixed order through LDS; nothing is
+// summed with atomics, so results are deterministic.
 #include "common.hpp"
 
 namespace incvit {
@@ -69,204 +72,179 @@ __device__ __forceinline__ void unpack8(float* x, const V8<float>& v) {
   x[4] = v.b.x; x[5] = v.b.y; x[6] = v.b.z; x[7] = v.b.w;
 }
 
-template <class T, int EPI, int NW>
-__global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
+// Residual element type: the cached X row (storage type) for the output
+// projection, H (fp32) for the MLP down projection.
+template <class T, int EPI> struct ResType { using type = float; };
+template <class T> struct ResType<T, EPI_OPROJ> { using type = T; };
+
+struct GemmShared {
+  RowInfo rows[kGemmRows];
+  float mean[kGemmRows], rstd[kGemmRows];
+  int m;
+};
+
+// One block of up to 64 rows (RT 16-row tiles) against this workgroup's NB
+// column blocks.  part: this thread's share of the LayerNorm partial sums of
+// row (tid / NW), already loaded.
+template <class T, int EPI, int NW, int NB, int RT>
+__device__ __forceinline__ void gemm_rows(const GemmArgs& a, GemmShared& sh, char* smem, int m0, int mrows,
+                                          float2 part) {
   constexpr bool kLN = (EPI == EPI_QKV || EPI == EPI_FC1);
   using TA = typename AType<T, EPI>::type;
-  constexpr int PF = (sizeof(TA) == 4 || NW >= 16) ? 2 : 4;  // chunks in flight per wave
-  constexpr int RT = 4;                                       // 16-row tiles per row block
-  constexpr int NT = NW * 64;
-  constexpr int kGB = (kMaxDim + NT - 1) / NT;                // LN parameters per thread
-  constexpr int kJ = (kMaxStat + NW - 1) / NW;                // LN partials per thread
-  extern __shared__ __align__(16) char smem[];
-  __shared__ RowInfo s_rows[kGemmRows];
-  __shared__ float s_mean[kGemmRows], s_rstd[kGemmRows];
-  __shared__ int s_m;
-
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  constexpr int PF = (sizeof(TA) == 4 || RT >= 3) ? 2 : 4;  // chunks in flight per wave
+  // w is read into a scalar register so every guard that depends on it is a
+  // scalar branch: an MFMA must never sit under a lane mask (it would still
+  // accumulate with the mask empty).
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, n = lane & 15;
-  const int cb = blockIdx.x;
   const int D = a.sh.D;
-  const int col = cb * 16 + n;
+  const int cb0 = blockIdx.x * NB;
   const int nw = max(0, (a.kchunks - w + NW - 1) / NW);
-  const T* wbase = static_cast<const T*>(a.W) + (size_t)cb * a.kchunks * kChunkElems + lane * 8;
-  float* s_g = reinterpret_cast<float*>(smem + NW * RT * 64 * 16);
-  float* s_b = s_g + D;
-
-  // ---- batch 1: weights, M, LayerNorm parameters
-  // Every load below is issued unconditionally (addresses clamped into range),
-  // so each loop iteration issues a fixed number of loads and the wait before
-  // an MFMA covers only the loads it needs, not the prefetches behind them.
   const int kclamp = a.kchunks - 1;
   auto chunk = [&](int i) { return min(w + NW * i, kclamp); };
-  V8<T> wb[PF];
+  const float* s_g = reinterpret_cast<const float*>(smem + NW * 4 * NB * 64 * 16);
+  const float* s_b = s_g + D;
+
+  // ---- A rows (and residuals): latency-critical, issued first
+  const TA* ap[RT];
 #pragma unroll
-  for (int s = 0; s < PF; ++s) wb[s].load(wbase + (size_t)chunk(s) * kChunkElems);
-  if (tid == 0) s_m = a.meta->m;
-  if constexpr (kLN) {
-    float gv[kGB], bv[kGB];
-#pragma unroll
-    for (int j = 0; j < kGB; ++j) {
-      const int k = tid + NT * j;
-      gv[j] = k < D ? a.ln_g[k] : 0.0f;
-      bv[j] = k < D ? a.ln_b[k] : 0.0f;
+  for (int r = 0; r < RT; ++r) {
+    const int rl = min(16 * r + n, mrows - 1);
+    if constexpr (EPI == EPI_QKV) {
+      const RowInfo ri = sh.rows[rl];
+      ap[r] = x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok) + 8 * g;
+    } else {
+      ap[r] = static_cast<const TA*>(a.A) + (size_t)(m0 + rl) * a.lda + 8 * g;
     }
+  }
+  V8<TA> ab[PF][RT];
 #pragma unroll
-    for (int j = 0; j < kGB; ++j) {
-      const int k = tid + NT * j;
-      if (k < D) {
-        s_g[k] = gv[j];
-        s_b[k] = bv[j];
+  for (int s = 0; s < PF; ++s)
+#pragma unroll
+    for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + chunk(s) * 32);
+  const int rt = w;  // the row tile this wave finishes (if rt < RT)
+  // epilogue residuals of this lane's 4 rows, kept raw until the epilogue;
+  // loaded by every wave (clamped) so no branch waits on them
+  typename ResType<T, EPI>::type rres[NB][4];
+  if constexpr (EPI == EPI_FC2 || EPI == EPI_OPROJ) {
+    const int rtl = min(rt, RT - 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rl = min(16 * rtl + 4 * g + i, mrows - 1);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int col = (cb0 + b) * 16 + n;
+        if constexpr (EPI == EPI_FC2) {
+          rres[b][i] = a.hres[(size_t)(m0 + rl) * D + col];
+        } else {
+          const RowInfo ri = sh.rows[rl];
+          rres[b][i] = gbl(x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok))[col];
+        }
       }
     }
   }
-  const float bias = a.bias[col];
-  __syncthreads();
-  const int M = s_m;
+  // ---- the weight stream
+  const T* wbase[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    wbase[b] = static_cast<const T*>(a.W) + (size_t)(cb0 + b) * a.kchunks * kChunkElems + lane * 8;
+  V8<T> wb[PF][NB];
+#pragma unroll
+  for (int s = 0; s < PF; ++s)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) wb[s][b].load(wbase[b] + (size_t)chunk(s) * kChunkElems);
 
-  V8<TA> ab[PF][RT];
-  const TA* ap[RT];
-  for (int m0 = 0; m0 < M; m0 += kGemmRows) {
-    const int mrows = min(kGemmRows, M - m0);
-    const int nrt = (mrows + 15) >> 4;
-    const int rt = w;  // the row tile this wave finishes
-    // ---- batch 2: row map, LayerNorm partials, compact rows
-    if (tid < kGemmRows) s_rows[tid] = a.rows[m0 + min(tid, mrows - 1)];
-    if (m0 > 0) {
+  // ---- LayerNorm statistics of the block's rows (fixed-order reduction)
+  if constexpr (kLN) {
 #pragma unroll
-      for (int s = 0; s < PF; ++s) wb[s].load(wbase + (size_t)chunk(s) * kChunkElems);
+    for (int off = NW / 2; off >= 1; off >>= 1) {
+      part.x += __shfl_xor(part.x, off, NW);
+      part.y += __shfl_xor(part.y, off, NW);
     }
-    float2 part = make_float2(0.0f, 0.0f);
-    const int srow = tid / NW, sq = tid % NW;  // NW threads (adjacent lanes) per row
-    if constexpr (kLN) {
-      float2 pv[kJ];
-      const float2* sp = a.stats_in + (size_t)(m0 + min(srow, mrows - 1)) * a.stat_stride;
-#pragma unroll
-      for (int jj = 0; jj < kJ; ++jj) pv[jj] = sp[min(sq + NW * jj, a.nstat - 1)];
-#pragma unroll
-      for (int jj = 0; jj < kJ; ++jj) {
-        if (sq + NW * jj < a.nstat) {
-          part.x += pv[jj].x;
-          part.y += pv[jj].y;
-        }
-      }
+    const int srow = tid / NW;
+    if (tid % NW == 0 && srow < mrows) {
+      const float mean = part.x / (float)D;
+      const float var = fmaxf(part.y / (float)D - mean * mean, 0.0f);
+      sh.mean[srow] = mean;
+      sh.rstd[srow] = 1.0f / sqrtf(var + a.sh.eps);
     }
-    if constexpr (EPI != EPI_QKV) {
-#pragma unroll
-      for (int r = 0; r < RT; ++r)
-        ap[r] = static_cast<const TA*>(a.A) + (size_t)(m0 + min(16 * r + n, mrows - 1)) * a.lda + 8 * g;
-#pragma unroll
-      for (int s = 0; s < PF; ++s)
-#pragma unroll
-        for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + chunk(s) * 32);
-    }
-    float res[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // epilogue residual of this lane's 4 rows
-    if constexpr (EPI == EPI_FC2) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        res[i] = a.hres[(size_t)(m0 + min(16 * min(rt, RT - 1) + 4 * g + i, mrows - 1)) * D + col];
-    }
-    __syncthreads();  // s_rows
-    // ---- batch 3: rows gathered from the caches
-    if constexpr (EPI == EPI_QKV) {
-#pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        const RowInfo ri = s_rows[min(16 * r + n, mrows - 1)];
-        ap[r] = x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok) + 8 * g;
-      }
-#pragma unroll
-      for (int s = 0; s < PF; ++s)
-#pragma unroll
-        for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + chunk(s) * 32);
-    }
-    if constexpr (EPI == EPI_OPROJ) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const RowInfo ri = s_rows[min(16 * min(rt, RT - 1) + 4 * g + i, mrows - 1)];
-        res[i] = Elem<T>::f(gbl(x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok))[col]);
-      }
-    }
-    // ---- LayerNorm statistics of the block's rows (fixed-order reduction)
-    if constexpr (kLN) {
-#pragma unroll
-      for (int off = NW / 2; off >= 1; off >>= 1) {
-        part.x += __shfl_xor(part.x, off, NW);
-        part.y += __shfl_xor(part.y, off, NW);
-      }
-      if (sq == 0 && srow < mrows) {
-        const float mean = part.x / (float)D;
-        const float var = fmaxf(part.y / (float)D - mean * mean, 0.0f);
-        s_mean[srow] = mean;
-        s_rstd[srow] = 1.0f / sqrtf(var + a.sh.eps);
-      }
-      __syncthreads();
-    }
-    float rmean[RT], rrstd[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-      const int rl = min(16 * r + n, mrows - 1);
-      rmean[r] = kLN ? s_mean[rl] : 0.0f;
-      rrstd[r] = kLN ? s_rstd[rl] : 0.0f;
-    }
-
-    // ---- MFMA over this wave's chunks
-    f32x4_t acc[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) acc[r] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    for (int i0 = 0; i0 < nw; i0 += PF) {
-#pragma unroll
-      for (int s = 0; s < PF; ++s) {
-        const int i = i0 + s;
-        if (i < nw) {  // uniform; no memory operation inside
-          const int kc = w + NW * i;
-          float gg[8], bb[8];
-          if constexpr (kLN) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              gg[e] = s_g[kc * 32 + 8 * g + e];
-              bb[e] = s_b[kc * 32 + 8 * g + e];
-            }
-          }
-#pragma unroll
-          for (int r = 0; r < RT; ++r) {
-            if (r < nrt) {
-              if constexpr (kLN) {
-                float x[8];
-                unpack8(x, ab[s][r]);
-                V8<T> av;
-                ln8(av, x, rmean[r], rrstd[r], gg, bb);
-                mma(acc[r], av, wb[s]);
-              } else {
-                mma(acc[r], ab[s][r], wb[s]);
-              }
-            }
-          }
-        }
-        const int kn = chunk(i + PF);
-        wb[s].load(wbase + (size_t)kn * kChunkElems);
-#pragma unroll
-        for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + kn * 32);
-      }
-    }
-
-    // ---- sum the waves' partial tiles in wave order; wave w finishes row tile w
-    f32x4_t* red = reinterpret_cast<f32x4_t*>(smem);
-#pragma unroll
-    for (int r = 0; r < RT; ++r)
-      if (r < nrt) red[(w * RT + r) * 64 + lane] = acc[r];
     __syncthreads();
-    if (rt < nrt) {
-      f32x4_t val = red[rt * 64 + lane];
+  }
+  float rmean[RT], rrstd[RT];
 #pragma unroll
-      for (int ww = 1; ww < NW; ++ww) val += red[(ww * RT + rt) * 64 + lane];
+  for (int r = 0; r < RT; ++r) {
+    const int rl = min(16 * r + n, mrows - 1);
+    rmean[r] = kLN ? sh.mean[rl] : 0.0f;
+    rrstd[r] = kLN ? sh.rstd[rl] : 0.0f;
+  }
 
-      // ---- epilogue: stores only
+  // ---- MFMA over this wave's chunks
+  f32x4_t acc[RT][NB];
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[r][b] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int i0 = 0; i0 < nw; i0 += PF) {
+#pragma unroll
+    for (int s = 0; s < PF; ++s) {
+      const int i = i0 + s;
+      if (i < nw) {  // uniform; no memory operation inside
+        const int kc = w + NW * i;
+        float gg[8], bb[8];
+        if constexpr (kLN) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            gg[e] = s_g[kc * 32 + 8 * g + e];
+            bb[e] = s_b[kc * 32 + 8 * g + e];
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+          if constexpr (kLN) {
+            float x[8];
+            unpack8(x, ab[s][r]);
+            V8<T> av;
+            ln8(av, x, rmean[r], rrstd[r], gg, bb);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) mma(acc[r][b], av, wb[s][b]);
+          } else {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) mma(acc[r][b], ab[s][r], wb[s][b]);
+          }
+        }
+      }
+      const int kn = chunk(i + PF);
+#pragma unroll
+      for (int r = 0; r < RT; ++r) ab[s][r].load(ap[r] + kn * 32);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) wb[s][b].load(wbase[b] + (size_t)kn * kChunkElems);
+    }
+  }
+
+  // ---- sum the waves' partial tiles in wave order; wave w finishes row tile w
+  f32x4_t* red = reinterpret_cast<f32x4_t*>(smem);
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) red[((w * RT + r) * NB + b) * 64 + lane] = acc[r][b];
+  __syncthreads();
+  if (rt < RT) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int cb = cb0 + b;
+      const int col = cb * 16 + n;
+      f32x4_t val = red[((0 * RT + rt) * NB + b) * 64 + lane];
+#pragma unroll
+      for (int ww = 1; ww < NW; ++ww) val += red[((ww * RT + rt) * NB + b) * 64 + lane];
+      const float bias = a.bias[col];
+
+      // ---- epilogue: stores
       float y[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int rl = 16 * rt + 4 * g + i;
         const float x = val[i] + bias;
-        const RowInfo ri = s_rows[min(rl, mrows - 1)];
+        const RowInfo ri = sh.rows[min(rl, mrows - 1)];
         const bool ok = rl < mrows;
         y[i] = 0.0f;
         if constexpr (EPI == EPI_QKV) {
@@ -284,13 +262,13 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
             }
           }
         } else if constexpr (EPI == EPI_OPROJ) {
-          y[i] = res[i] + x;
+          y[i] = Elem<T>::f(rres[b][i]) + x;
           if (ok) static_cast<float*>(a.out)[(size_t)(m0 + rl) * a.ldo + col] = y[i];
         } else if constexpr (EPI == EPI_FC1) {
           if (ok) static_cast<T*>(a.out)[(size_t)(m0 + rl) * a.ldo + col] = Elem<T>::cv(gelu_tanh(x));
         } else {
-          const T o = Elem<T>::cv(res[i] + x);
-          y[i] = Elem<T>::ld(&o, 0);
+          const T o = Elem<T>::cv(rres[b][i] + x);
+          y[i] = Elem<T>::f(o);
           if (ok) gbl(x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok))[col] = o;
         }
       }
@@ -310,55 +288,130 @@ __global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
         }
       }
     }
-    __syncthreads();  // shared state reused by the next row block
   }
 }
 
+// LayerNorm partials of row (m0 + tid / NW): this thread sums the partials
+// j = tid % NW, + NW, ... in order.
 template <int NW>
+__device__ __forceinline__ float2 load_partials(const GemmArgs& a, int m0, int rows_bound) {
+  constexpr int kJ = (kMaxStat + NW - 1) / NW;
+  const int srow = min((int)threadIdx.x / NW, rows_bound - 1), sq = threadIdx.x % NW;
+  const float2* sp = a.stats_in + (size_t)(m0 + srow) * a.stat_stride;
+  float2 pv[kJ];
+#pragma unroll
+  for (int jj = 0; jj < kJ; ++jj) pv[jj] = sp[min(sq + NW * jj, a.nstat - 1)];
+  float2 part = make_float2(0.0f, 0.0f);
+#pragma unroll
+  for (int jj = 0; jj < kJ; ++jj) {
+    if (sq + NW * jj < a.nstat) {
+      part.x += pv[jj].x;
+      part.y += pv[jj].y;
+    }
+  }
+  return part;
+}
+
+template <class T, int EPI, int NW, int NB>
+__global__ __launch_bounds__(NW * 64) void gemm_kernel(GemmArgs a) {
+  constexpr bool kLN = (EPI == EPI_QKV || EPI == EPI_FC1);
+  constexpr int NT = NW * 64;
+  constexpr int kGB = (kMaxDim + NT - 1) / NT;
+  extern __shared__ __align__(16) char smem[];
+  __shared__ GemmShared sh;
+  const int tid = threadIdx.x;
+  const int D = a.sh.D;
+
+  // ---- first: M, the row map and LayerNorm partials of the first 64 rows
+  // (rows past M are read but never used), and the LayerNorm parameters
+  if (tid == 0) sh.m = a.meta->m;
+  if (tid < kGemmRows) sh.rows[tid] = a.rows[tid];
+  float2 part = make_float2(0.0f, 0.0f);
+  if constexpr (kLN) part = load_partials<NW>(a, 0, kGemmRows);
+  float* s_g = reinterpret_cast<float*>(smem + NW * 4 * NB * 64 * 16);
+  float* s_b = s_g + D;
+  if constexpr (kLN) {
+    float gv[kGB], bv[kGB];
+#pragma unroll
+    for (int j = 0; j < kGB; ++j) {
+      const int k = min(tid + NT * j, D - 1);
+      gv[j] = a.ln_g[k];
+      bv[j] = a.ln_b[k];
+    }
+#pragma unroll
+    for (int j = 0; j < kGB; ++j) {
+      const int k = tid + NT * j;
+      if (k < D) {
+        s_g[k] = gv[j];
+        s_b[k] = bv[j];
+      }
+    }
+  }
+  __syncthreads();
+  const int M = sh.m;
+  for (int m0 = 0; m0 < M; m0 += kGemmRows) {
+    const int mrows = min(kGemmRows, M - m0);
+    if (m0 > 0) {  // later blocks: row map and partials of this block
+      __syncthreads();
+      if (tid < kGemmRows) sh.rows[tid] = a.rows[m0 + min(tid, mrows - 1)];
+      if constexpr (kLN) part = load_partials<NW>(a, m0, mrows);
+      __syncthreads();
+    }
+    switch ((mrows + 15) >> 4) {
+      case 1: gemm_rows<T, EPI, NW, NB, 1>(a, sh, smem, m0, mrows, part); break;
+      case 2: gemm_rows<T, EPI, NW, NB, 2>(a, sh, smem, m0, mrows, part); break;
+      case 3: gemm_rows<T, EPI, NW, NB, 3>(a, sh, smem, m0, mrows, part); break;
+      default: gemm_rows<T, EPI, NW, NB, 4>(a, sh, smem, m0, mrows, part); break;
+    }
+  }
+}
+
+template <int NW, int NB>
 static size_t gemm_lds(const GemmArgs& a) {
-  return (size_t)NW * 4 * 64 * 16 + (size_t)2 * a.sh.D * sizeof(float);
+  return (size_t)NW * 4 * NB * 64 * 16 + (size_t)2 * a.sh.D * sizeof(float);
 }
 
 // Allow each instantiation the largest dynamic LDS any shape needs, once.
-template <class T, int EPI, int NW>
+template <class T, int EPI, int NW, int NB>
 static hipError_t allow_lds() {
   static hipError_t done = hipErrorNotReady;
   if (done != hipSuccess) {
-    const int most = NW * 4 * 64 * 16 + 2 * kMaxDim * (int)sizeof(float);
-    done = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<T, EPI, NW>),
+    const int most = NW * 4 * NB * 64 * 16 + 2 * kMaxDim * (int)sizeof(float);
+    done = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<T, EPI, NW, NB>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, most);
   }
   return done;
 }
 
-template <int EPI, int NW>
-static hipError_t launch_nw(const GemmArgs& a, hipStream_t s) {
-  const dim3 grid(a.Nout / 16);
-  const size_t lds = gemm_lds<NW>(a);
+template <int EPI, int NW, int NB>
+static hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
+  const dim3 grid(a.Nout / 16 / NB);
+  const size_t lds = gemm_lds<NW, NB>(a);
   hipError_t e;
   if (a.sh.dtype) {
-    if ((e = allow_lds<uint16_t, EPI, NW>()) != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_kernel<uint16_t, EPI, NW>), grid, dim3(NW * 64), lds, s, a);
+    if ((e = allow_lds<uint16_t, EPI, NW, NB>()) != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_kernel<uint16_t, EPI, NW, NB>), grid, dim3(NW * 64), lds, s, a);
   } else {
-    if ((e = allow_lds<float, EPI, NW>()) != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_kernel<float, EPI, NW>), grid, dim3(NW * 64), lds, s, a);
+    if ((e = allow_lds<float, EPI, NW, NB>()) != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_kernel<float, EPI, NW, NB>), grid, dim3(NW * 64), lds, s, a);
   }
   return hipGetLastError();
 }
 
+// cols: column blocks per workgroup (1 or 2; 2 needs an even block count).
 template <int EPI>
-static hipError_t launch_epi(int waves, const GemmArgs& a, hipStream_t s) {
-  if (waves >= 16) return launch_nw<EPI, 16>(a, s);
-  if (waves >= 8) return launch_nw<EPI, 8>(a, s);
-  return launch_nw<EPI, 4>(a, s);
+static hipError_t launch_epi(int waves, int cols, const GemmArgs& a, hipStream_t s) {
+  const bool two = cols == 2 && (a.Nout / 16) % 2 == 0;
+  if (waves >= 8) return two ? launch_cfg<EPI, 8, 2>(a, s) : launch_cfg<EPI, 8, 1>(a, s);
+  return two ? launch_cfg<EPI, 4, 2>(a, s) : launch_cfg<EPI, 4, 1>(a, s);
 }
 
-hipError_t launch_gemm(int epi, int waves, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(int epi, int waves, int cols, const GemmArgs& a, hipStream_t s) {
   switch (epi) {
-    case EPI_QKV: return launch_epi<EPI_QKV>(waves, a, s);
-    case EPI_OPROJ: return launch_epi<EPI_OPROJ>(waves, a, s);
-    case EPI_FC1: return launch_epi<EPI_FC1>(waves, a, s);
-    default: return launch_epi<EPI_FC2>(waves, a, s);
+    case EPI_QKV: return launch_epi<EPI_QKV>(waves, cols, a, s);
+    case EPI_OPROJ: return launch_epi<EPI_OPROJ>(waves, cols, a, s);
+    case EPI_FC1: return launch_epi<EPI_FC1>(waves, cols, a, s);
+    default: return launch_epi<EPI_FC2>(waves, cols, a, s);
   }
 }
 

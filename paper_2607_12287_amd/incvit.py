@@ -39,7 +39,7 @@ class incvit_config(ctypes.Structure):
 
 
 class incvit_tuning(ctypes.Structure):
-    _fields_ = [("waves", ctypes.c_int32 * 4)]
+    _fields_ = [("waves", ctypes.c_int32 * 4), ("cols", ctypes.c_int32 * 4)]
 
 
 class IncvitError(RuntimeError):
@@ -198,10 +198,11 @@ def incvit_graph_destroy(g) -> None:
     lib().incvit_graph_destroy(g)
 
 
-def incvit_set_tuning(h, waves: Optional[Sequence[int]] = None) -> int:
-    if waves is None:
+def incvit_set_tuning(h, waves: Optional[Sequence[int]] = None, cols: Optional[Sequence[int]] = None) -> int:
+    if waves is None and cols is None:
         return lib().incvit_set_tuning(h, None)
-    t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in waves]))
+    t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in (waves or [0] * 4)]),
+                      (ctypes.c_int32 * 4)(*[int(k) for k in (cols or [0] * 4)]))
     return lib().incvit_set_tuning(h, ctypes.byref(t))
 
 
