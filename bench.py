@@ -15,14 +15,61 @@ bounded sample of the same stream.
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
 
 METRIC = "incremental ViT frames/sec at 10% refresh (So400m shape); speedup vs full encode"
 HBM_PEAK_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+PROFILES = os.path.join(ROOT, "profiles")
+GEMM_KIND = {"0": "qkv", "1": "oproj", "2": "fc1", "3": "fc2"}
+
+
+def source_hash() -> str:
+    """Hash of every kernel and ABI source: stored counters are used only while it matches."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2607_12287_amd", "csrc", "*")) +
+                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_kind(name: str):
+    """Kernel kind of a dispatch name in a rocprofv3 trace (None for other kernels)."""
+    m = re.search(r"incvit::(\w+)_kernel(?:<([^>]*)>)?", name)
+    if not m:
+        return None
+    if m.group(1) == "gemm":
+        return GEMM_KIND.get(m.group(2).split(",")[1].strip())
+    return m.group(1)
+
+
+def stored_traffic(workload: str, kind: str):
+    """HBM bytes per launch of `kind` from the committed counter summary, if the
+    kernels have not changed since it was taken."""
+    path = os.path.join(PROFILES, f"step_hbm_traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    vals, src = {}, None
+    for line in open(path):
+        f = line.split()
+        if len(f) == 2 and f[0] == "source_hash":
+            src = f[1]
+        if len(f) == 3 and f[0] == "traffic_bytes_per_launch":
+            vals[f[1]] = float(f[2])
+    if src != source_hash():
+        return None
+    return vals.get(kind)
 
 
 def gemm_bytes(m, M: float, kind: str) -> float:
@@ -66,9 +113,141 @@ def cpu_baseline(wl, frames, seconds: float):
                       f"(frames 1..{steps}) of the same stream; value = frames / summed step time"}
 
 
+def _csv_rows(directory: str, suffix: str):
+    import gzip
+    files = glob.glob(os.path.join(directory, "**", f"*{suffix}"), recursive=True)
+    files += glob.glob(os.path.join(directory, "**", f"*{suffix}.gz"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no *{suffix} under {directory}")
+    opener = gzip.open if files[0].endswith(".gz") else open
+    with opener(files[0], "rt", newline="") as fh:
+        return list(csv.DictReader(fh))
+
+
+def _bench_json(path: str) -> dict:
+    lines = [ln for ln in open(path) if ln.startswith("{")]
+    return json.loads(lines[-1])
+
+
+def summarize_trace(trace_dir: str, bench_log: str, plain_log: str, out: str, command: str) -> None:
+    """Per-kind average dispatch duration from a rocprofv3 kernel trace of a
+    bench.py run: the last n dispatches of each kind are the ones bench.py
+    timed with its own per-launch events (n = its kernel_launches).  Shown next
+    to bench.py's event averages in the traced run and in a run of the same
+    command without the profiler (the run whose figures bench.py reports)."""
+    b = _bench_json(bench_log)
+    plain = _bench_json(plain_log)
+    rows = sorted(_csv_rows(trace_dir, "kernel_trace.csv"), key=lambda r: int(r["Dispatch_Id"]))
+    by_kind = {}
+    for r in rows:
+        k = kernel_kind(r["Kernel_Name"])
+        if k:
+            by_kind.setdefault(k, []).append((r["Kernel_Name"], (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3))
+    stats = _csv_rows(trace_dir, "kernel_stats.csv")
+    lines = [f"# rocprofv3 kernel trace of one bench.py run: {b['config']['workload']}",
+             f"# command: {command}",
+             f"# bench: {b['value']} {b['unit']}, {b['ms_per_step']} ms/step ({b['launch']}), "
+             f"full encode {b['full_encode_ms']} ms, mean rows/step {b['config']['rows_mean']}",
+             f"# same command without the profiler: {plain['value']} {plain['unit']}, {plain['ms_per_step']} ms/step, "
+             f"full encode {plain['full_encode_ms']} ms",
+             "# per kind: the last n dispatches (bench.py's own event-timed launches); events_traced = bench.py's",
+             "# dispatch events in the traced run (the tracer delays event completion), events_plain = the same",
+             "# events without the profiler; ratio = events_plain / rocprof",
+             f"{'kind':8s} {'n':>7s} {'rocprof_us':>11s} {'events_traced_us':>17s} {'events_plain_us':>16s} "
+             f"{'ratio':>6s}  kernel"]
+    for k, n in b["kernel_launches"].items():
+        d = by_kind.get(k, [])[-n:]
+        if not d:
+            continue
+        avg = statistics.mean(x[1] for x in d)
+        ev = b["kernel_us_per_launch"][k]
+        evp = plain["kernel_us_per_launch"].get(k, float("nan"))
+        lines.append(f"{k:8s} {n:7d} {avg:11.3f} {ev:17.3f} {evp:16.3f} {evp / avg:6.3f}  {d[-1][0]}")
+    lines.append("")
+    lines.append("# rocprofv3 --stats (whole run: includes the full-encode timing and warm-up dispatches)")
+    lines.append(f"{'calls':>7s} {'avg_us':>10s} {'min_us':>10s} {'max_us':>10s} {'pct':>6s}  name")
+    for r in stats[:24]:
+        lines.append(f"{int(r['Calls']):7d} {float(r['AverageNs']) * 1e-3:10.3f} {float(r['MinNs']) * 1e-3:10.3f} "
+                     f"{float(r['MaxNs']) * 1e-3:10.3f} {float(r['Percentage']):6.2f}  {r['Name'][:110]}")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _pmc_per_dispatch(directory: str, counter: str):
+    vals = {}
+    for r in _csv_rows(directory, "counter_collection.csv"):
+        if r["Counter_Name"] == counter:
+            key = (int(r["Dispatch_Id"]), r["Kernel_Name"])
+            vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+    return [(d, n, v) for (d, n), v in sorted(vals.items())]
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str, copy_fetch_dir: str, copy_write_dir: str,
+                  bench_log: str, copy_log: str, out: str, commands: str) -> None:
+    """HBM bytes per launch of each kernel kind from FETCH_SIZE and WRITE_SIZE
+    passes (KiB per dispatch), each scaled by what the same counter reads for a
+    plain device copy of known size."""
+    b = _bench_json(bench_log)
+    nbytes = _bench_json(copy_log)["copy_bytes"]
+    scale = {}
+    for name, d in (("FETCH_SIZE", copy_fetch_dir), ("WRITE_SIZE", copy_write_dir)):
+        big = [v for _, n, v in _pmc_per_dispatch(d, name) if "copy" in n.lower() and v * 1024 > 0.5 * nbytes]
+        if not big:
+            raise RuntimeError(f"no copy dispatch with {name} near {nbytes} bytes in {d}")
+        scale[name] = nbytes / (statistics.median(big) * 1024.0)
+    per = {}
+    for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        by_kind = {}
+        for _, n, v in _pmc_per_dispatch(d, name):
+            k = kernel_kind(n)
+            if k:
+                by_kind.setdefault(k, []).append(v)
+        for k, n in b["kernel_launches"].items():
+            vals = by_kind.get(k, [])[-n:]
+            if vals:
+                per.setdefault(k, {})[name] = statistics.mean(vals) * 1024.0 * scale[name]
+    lines = [f"# HBM traffic per launch from rocprofv3 --pmc passes over one bench.py run: {b['config']['workload']}",
+             f"# commands: {commands}",
+             f"# mean rows/step {b['config']['rows_mean']}; per kind: mean over the last n dispatches "
+             "(the bench's event-timed steps)",
+             f"# copy calibration ({nbytes} bytes copied): FETCH_SIZE scale {scale['FETCH_SIZE']:.4f}, "
+             f"WRITE_SIZE scale {scale['WRITE_SIZE']:.4f}",
+             f"source_hash {source_hash()}",
+             f"# {'kind':8s} {'fetch_bytes':>14s} {'write_bytes':>14s}"]
+    for k, v in per.items():
+        lines.append(f"# {k:8s} {v.get('FETCH_SIZE', float('nan')):14.0f} {v.get('WRITE_SIZE', float('nan')):14.0f}")
+    for k, v in per.items():
+        if "FETCH_SIZE" in v and "WRITE_SIZE" in v:
+            lines.append(f"traffic_bytes_per_launch {k} {v['FETCH_SIZE'] + v['WRITE_SIZE']:.0f}")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def copy_pass(mib: int) -> int:
+    """A plain device-to-device copy of known size: the calibration for the HBM counters."""
+    import torch
+    n = mib << 20
+    a = torch.full((n,), 7, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "reps": 3}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--copy-pass", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device (calibration of the HBM counters)")
+    ap.add_argument("--summarize-trace", nargs=5, metavar=("TRACE_DIR", "TRACED_BENCH_LOG", "PLAIN_BENCH_LOG", "OUT",
+                                                           "COMMAND"))
+    ap.add_argument("--summarize-pmc", nargs=8, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+                                                         "COPY_WRITE_DIR", "BENCH_LOG", "COPY_LOG", "OUT", "COMMANDS"))
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="so400m",
@@ -83,12 +262,20 @@ def main() -> int:
     ap.add_argument("--waves", default=None, help="waves per GEMM workgroup: four comma-separated values (0 = automatic)")
     ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four values (0 = automatic)")
     args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return 0
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the encoder's state is per stream and this build runs "
               "single-GPU only (streams would shard across GPUs with no exchange); use --gpus 1.",
               file=sys.stderr)
         return 2
+    if args.copy_pass:
+        return copy_pass(args.copy_pass)
 
     import numpy as np
     import torch
@@ -214,8 +401,10 @@ def main() -> int:
             "kernel": dom, "bound": "hbm", "achieved": round(achieved, 1) if achieved else None,
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
-            "traffic": None, "avg_launch_us": round(avg_us, 3), "bytes_per_launch": nbytes,
+            "traffic": stored_traffic(wl.name, dom), "avg_launch_us": round(avg_us, 3),
+            "bytes_per_launch": nbytes,
         }
+        result["kernel_launches"] = {k: int(v[1]) for k, v in kinds.items()}
         result["kernel_us_per_launch"] = {k: round(v[0] * 1e3 / v[1], 3) for k, v in kinds.items()}
         result["kernel_ms_per_step"] = {k: round(v[0] / args.steps, 5) for k, v in kinds.items()}
     del buf2, caches2

@@ -2,6 +2,7 @@
 // structs, launchers and small device helpers.  gfx950 (CDNA4) only.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -203,6 +204,24 @@ struct ExportArgs {
   int to_canonical;  // 1 export, 0 import
   uint32_t hash;
 };
+
+// Start/stop events that the next kernel launch on this host thread records
+// with its own dispatch (per-kernel timing that adds no stream operations);
+// both null outside profiled calls.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+// Every kernel here takes one argument struct by value.
+template <class A>
+hipError_t launch_k(void (*kernel)(A), dim3 grid, dim3 block, size_t lds, hipStream_t s, A arg) {
+  void* argv[] = {&arg};
+  const LaunchEvents& ev = launch_events();
+  if (ev.start)
+    return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, lds, s, ev.start, ev.stop, 0);
+  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, lds, s);
+}
 
 // launchers (return the launch error)
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);

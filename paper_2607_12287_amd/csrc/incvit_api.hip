@@ -254,6 +254,11 @@ struct incvit_graph {
   hipGraphExec_t exec = nullptr;
 };
 
+LaunchEvents& incvit::launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
+
 namespace {
 
 incvit_status fail(incvit_handle* h, incvit_status st, const std::string& msg) {
@@ -273,18 +278,23 @@ hipEvent_t take_event(incvit_handle* h) {
   return e;
 }
 
+// One kernel launch; with profiling on, the launch itself records a start and
+// a stop event (timestamps of its own dispatch, as a kernel trace sees it).
 template <class F>
 incvit_status run(incvit_handle* h, int kind, hipStream_t s, F&& launch) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (h->prof) {
     e0 = take_event(h);
     e1 = take_event(h);
-    if (e0) (void)hipEventRecord(e0, s);
   }
+  if (e0 && e1) launch_events() = {e0, e1};
   const hipError_t err = launch();
-  if (h->prof && e0 && e1) {
-    (void)hipEventRecord(e1, s);
+  launch_events() = {};
+  if (e0 && e1) {
     h->recs.push_back({kind, e0, e1});
+  } else {
+    if (e0) h->pool.push_back(e0);
+    if (e1) h->pool.push_back(e1);
   }
   if (err != hipSuccess) {
     char buf[256];

@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 
 template <class T, int NDC, int NDT>
 static void launch_t(const AttnArgs& a, dim3 grid, hipStream_t s) {
-  hipLaunchKernelGGL((attn_kernel<T, NDC, NDT>), grid, dim3(256), 0, s, a);
+  (void)launch_k((attn_kernel<T, NDC, NDT>), grid, dim3(256), 0, s, a);
 }
 
 template <class T>

@@ -135,13 +135,13 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
-  hipLaunchKernelGGL(embed_kernel, grid, dim3(256), 0, s, a);
+  (void)launch_k(embed_kernel, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_sim(const SimArgs& a, hipStream_t s) {
   dim3 grid((a.B * a.N + 3) / 4);
-  hipLaunchKernelGGL(sim_kernel, grid, dim3(256), 0, s, a);
+  (void)launch_k(sim_kernel, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -390,10 +390,10 @@ static hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   hipError_t e;
   if (a.sh.dtype) {
     if ((e = allow_lds<uint16_t, EPI, NW, NB>()) != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_kernel<uint16_t, EPI, NW, NB>), grid, dim3(NW * 64), lds, s, a);
+    (void)launch_k((gemm_kernel<uint16_t, EPI, NW, NB>), grid, dim3(NW * 64), lds, s, a);
   } else {
     if ((e = allow_lds<float, EPI, NW, NB>()) != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_kernel<float, EPI, NW, NB>), grid, dim3(NW * 64), lds, s, a);
+    (void)launch_k((gemm_kernel<float, EPI, NW, NB>), grid, dim3(NW * 64), lds, s, a);
   }
   return hipGetLastError();
 }

@@ -78,19 +78,19 @@ __global__ void export_kernel(ExportArgs a) {
 }
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
-  if (a.dtype) hipLaunchKernelGGL(pack_kernel<uint16_t>, dim3(1024), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(pack_kernel<float>, dim3(1024), dim3(256), 0, s, a);
+  if (a.dtype) (void)launch_k(pack_kernel<uint16_t>, dim3(1024), dim3(256), 0, s, a);
+  else (void)launch_k(pack_kernel<float>, dim3(1024), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(conv_kernel, dim3(256), dim3(256), 0, s, a);
+  (void)launch_k(conv_kernel, dim3(256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_export(const ExportArgs& a, hipStream_t s) {
-  if (a.sh.dtype) hipLaunchKernelGGL(export_kernel<uint16_t>, dim3(1024), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(export_kernel<float>, dim3(1024), dim3(256), 0, s, a);
+  if (a.sh.dtype) (void)launch_k(export_kernel<uint16_t>, dim3(1024), dim3(256), 0, s, a);
+  else (void)launch_k(export_kernel<float>, dim3(1024), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -293,21 +293,21 @@ __global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(select_kernel, dim3(a.B), dim3(kSelThreads), 0, s, a);
+  (void)launch_k(select_kernel, dim3(a.B), dim3(kSelThreads), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s) {
   dim3 grid(max(1, (mmax + 3) / 4));
-  if (a.sh.dtype) hipLaunchKernelGGL(commit_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(commit_kernel<float>, grid, dim3(256), 0, s, a);
+  if (a.sh.dtype) (void)launch_k(commit_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else (void)launch_k(commit_kernel<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s) {
   dim3 grid(max(1, (mmax + 3) / 4));
-  if (a.sh.dtype) hipLaunchKernelGGL(final_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(final_kernel<float>, grid, dim3(256), 0, s, a);
+  if (a.sh.dtype) (void)launch_k(final_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else (void)launch_k(final_kernel<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
