@@ -259,8 +259,8 @@ def main() -> int:
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel events")
     ap.add_argument("--eager", dest="graph", action="store_false",
                     help="launch kernel by kernel instead of replaying captured HIP graphs")
-    ap.add_argument("--waves", default=None, help="waves per GEMM workgroup: four comma-separated values (0 = automatic)")
-    ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four values (0 = automatic)")
+    ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four comma-separated values "
+                                                 "(QKV, O-proj, fc1, fc2; 0 = automatic)")
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
@@ -290,10 +290,8 @@ def main() -> int:
     torch.cuda.set_device(dev)
     frames = torch.from_numpy(np.stack(frames_np)).to(dev)  # [T][B][N][P], resident in HBM
     enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
-    if args.waves or args.cols:
-        incvit._check(incvit.incvit_set_tuning(
-            enc.h, [int(x) for x in args.waves.split(",")] if args.waves else None,
-            [int(x) for x in args.cols.split(",")] if args.cols else None), enc.h)
+    if args.cols:
+        incvit._check(incvit.incvit_set_tuning(enc.h, [int(x) for x in args.cols.split(",")]), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),

@@ -195,12 +195,10 @@ void incvit_graph_destroy(incvit_graph* g);
 
 /* Performance knobs; every setting gives a deterministic result, and the
  * settings differ only in the order of fp32 partial sums.
- * For GEMM k (0 = QKV, 1 = output projection, 2 = MLP up, 3 = MLP down):
- * waves[k]: waves per workgroup, 4 or 8; cols[k]: 16-column blocks per
- * workgroup, 1 or 2 (2 only when the block count is even); 0 = automatic.
- * A NULL pointer restores the defaults. */
+ * cols[k]: 16-column blocks per workgroup of GEMM k (0 = QKV, 1 = output
+ * projection, 2 = MLP up, 3 = MLP down): 1 or 2 (2 only takes effect when the
+ * block count is even); 0 = automatic.  A NULL pointer restores the defaults. */
 typedef struct {
-  int32_t waves[4];
   int32_t cols[4];
 } incvit_tuning;
 
@@ -212,14 +210,15 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);
 typedef enum {
   INCVIT_K_EMBED = 0, INCVIT_K_SIM, INCVIT_K_SELECT, INCVIT_K_COMMIT,
   INCVIT_K_QKV, INCVIT_K_ATTN, INCVIT_K_OPROJ, INCVIT_K_FC1, INCVIT_K_FC2,
-  INCVIT_K_FINAL, INCVIT_K_COUNT
+  INCVIT_K_FINAL, INCVIT_K_FC2_FIX, INCVIT_K_COUNT
 } incvit_kernel_kind;
 
-/* When enabled, every kernel launch of the encode calls is bracketed by a pair
- * of hipEvents on the call's stream; incvit_profile_read synchronises those
- * events and returns, per kind, the summed duration (ms) and the number of
- * launches since the last reset.  Timing adds event records between kernels,
- * so measure throughput with profiling off. */
+/* When enabled, every kernel launch of the encode calls records a start and a
+ * stop event with its own dispatch on the call's stream (no extra stream
+ * operations); incvit_profile_read synchronises those events and returns, per
+ * kind, the summed duration (ms) and the number of launches since the last
+ * reset.  INCVIT_K_FC2 counts the MLP down projection's GEMM and
+ * INCVIT_K_FC2_FIX the row kernel that finishes it when its K is split. */
 incvit_status incvit_profile_enable(incvit_handle* h, int32_t enable);
 incvit_status incvit_profile_read(incvit_handle* h, double* total_ms /* [INCVIT_K_COUNT] */,
                                   int64_t* launches /* [INCVIT_K_COUNT] */, int32_t reset);

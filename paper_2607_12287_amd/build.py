@@ -14,7 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libincvit.so")
-SOURCES = ["incvit_api.hip", "k_embed.hip", "k_select.hip", "k_gemm.hip", "k_attn.hip", "k_misc.hip"]
+SOURCES = ["incvit_api.hip", "k_embed.hip", "k_select.hip", "k_gemm.hip", "k_gemm_qkv.hip", "k_gemm_oproj.hip",
+           "k_gemm_fc1.hip", "k_gemm_fc2.hip", "k_gemm_part.hip", "k_attn.hip", "k_misc.hip"]
 # the fixed-order fp32 embedding and cosine must not be contracted beyond the
 # explicit fma intrinsics
 NO_CONTRACT = {"k_embed.hip"}
@@ -42,7 +43,7 @@ def _compile(src: str) -> str:
 def build(verbose: bool = False) -> str:
     """Compile every source for gfx950 and link libincvit.so; returns its path."""
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(10, os.cpu_count() or 1)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp]

@@ -16,14 +16,13 @@ constexpr int kMaxHeadDim = 128;
 constexpr uint32_t kCacheMagic = 0x31435649u;  // "IVC1"
 constexpr int kStatusNonFinite = -1;           // a step saw a NaN similarity
 
-// GEMM tiling: a workgroup streams one 16-column block of the weights for
-// blocks of 64 rows; its waves take every NW-th 32-deep K chunk and their
-// partial tiles are summed in wave order.  Weights are packed so that one
-// chunk is one 16-byte (bf16) or 32-byte (fp32) load per lane, already in
-// MFMA operand order.
+// Compact row buffers (row map, Z, Q, O, H, G) are padded to a multiple of
+// kGemmRows rows, so a GEMM may read rows past M of its current 32-row block
+// before it knows M.  Weights are packed so that one 32-deep chunk of a
+// 16-column block is one 16-byte (bf16) or 32-byte (fp32) load per lane,
+// already in MFMA operand order.
 constexpr int kGemmRows = 64;
 constexpr int kChunkElems = 512;  // 64 lanes x 8 elements
-constexpr int kMaxStat = kMaxDim / 16;  // LayerNorm partials per row
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
@@ -139,33 +138,44 @@ struct RowsArgs {  // commit (ref/X0 of refreshed rows, row map) and final Layer
   void* refreshed;   // final: optional [B][N][D]
   int init_header;   // commit of a full encode: write header
   uint32_t hash;
-  float2* stats;     // commit: (sum, sum of squares) of each X0 row, stride stat_stride
-  int stat_stride;
+  void* z;           // compact rows [Mpad][D]: commit writes Z_0, final reads Z_L
 };
 
-enum Epi { EPI_QKV = 0, EPI_OPROJ = 1, EPI_FC1 = 2, EPI_FC2 = 3 };
+enum Epi { EPI_QKV = 0, EPI_OPROJ = 1, EPI_FC1 = 2, EPI_FC2 = 3, EPI_PART = 4 };
 
 struct GemmArgs {
-  const RowInfo* rows;
+  const RowInfo* rows;  // row map (cache, token, stream) of each compact row
   const Meta* meta;
   CacheLayout cl;
   Shape sh;
   int layer;
-  const void* A;      // OPROJ: O [Mpad][D]; FC1: H f32 [Mpad][D]; FC2: G [Mpad][Fpad]
+  const void* A;      // compact A rows: QKV Z_l, OPROJ O, FC1 H (f32), FC2 G
   int lda;
-  const float* ln_g;
+  const float* ln_g;  // QKV: LN1, FC1: LN2
   const float* ln_b;
   const void* W;      // packed [Nout/16][kchunks][512]
   const float* bias;  // [Nout]
   int kchunks, Nout;
-  void* out;          // QKV: Q [Mpad][D]; OPROJ: H f32 [Mpad][D]; FC1: G [Mpad][Fpad]
+  void* out;          // compact output: QKV Q, OPROJ H (f32), FC1 G, FC2 Z_{l+1}
   int ldo;
-  const float* hres;  // FC2: H f32 [Mpad][D]
-  // LayerNorm statistics: per compact row, nstat partial (sum, sum of squares)
-  // pairs at stride stat_stride; read by QKV/FC1, written by OPROJ/FC2
-  const float2* stats_in;
-  float2* stats_out;
-  int nstat, stat_stride;
+  const void* res;    // compact residual: OPROJ Z_l, FC2 H (f32); [row][D]
+  int ksplit;         // K is split over gridDim.y = ksplit workgroups (EPI_PART only)
+  int mpad;           // rows of one partial slice of `out` (EPI_PART)
+};
+
+// The rows of the MLP down projection when its K is split: Z_{l+1} =
+// S(H + (sum of the split partials, in split order) + b_2).
+struct FixArgs {
+  const Meta* meta;
+  const RowInfo* rows;
+  CacheLayout cl;
+  Shape sh;
+  int layer;
+  const float* part;  // [ksplit][mpad][D]
+  int ksplit, mpad;
+  const float* h;     // [Mpad][D]
+  const float* bias;  // b_2 [D]
+  void* z;            // compact Z_{l+1} [Mpad][D]
 };
 
 struct AttnArgs {
@@ -229,7 +239,8 @@ hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s);
-hipError_t launch_gemm(int epi, int waves, int cols, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
+hipError_t launch_fix(const FixArgs& a, int mmax, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);

@@ -36,8 +36,8 @@ struct CanonLayout {  // element offsets into the canonical buffer
 };
 
 struct WsLayout {
-  size_t meta, rows, count, idx, sim, t0, q, o, h, g, stats_x, stats_h, total;
-  int Mpad, stat_stride;
+  size_t meta, rows, count, idx, sim, t0, z, q, o, h, g, part, total;
+  int Mpad;
 };
 
 enum GemmKind { G_QKV = 0, G_OPROJ = 1, G_FC1 = 2, G_FC2 = 3 };
@@ -173,7 +173,7 @@ uint32_t config_hash(const incvit_config& c) {
 }
 
 struct GemmGeom {
-  int K, kchunks, Nout, nblocks;
+  int K, kchunks, Nout, nblocks, ksplit;
 };
 
 GemmGeom gemm_geom(const Shape& sh, int kind) {
@@ -186,13 +186,13 @@ GemmGeom gemm_geom(const Shape& sh, int kind) {
   }
   g.kchunks = round_up(g.K, 32) / 32;
   g.nblocks = g.Nout / 16;
+  // Split K over workgroups when one workgroup's 8 waves would each need more
+  // than 8 chunks in registers (the MLP down projection, K = F): the partial
+  // sums then finish in a row kernel.  The LayerNorm GEMMs have K = D <= 2048,
+  // which never splits (their statistics need whole rows).
+  const int need = (g.kchunks + 7) / 8;
+  g.ksplit = need > 8 ? std::min(4, (need + 5) / 6) : 1;
   return g;
-}
-
-// Waves per GEMM workgroup: 8 keeps enough loads in flight per CU.
-int waves_of(const int* tuned, const GemmGeom&, int kind) {
-  const int t = tuned ? tuned[kind] : 0;
-  return t > 0 ? t : 8;
 }
 
 // Column blocks per workgroup: outputs with more blocks than CUs take two per
@@ -209,19 +209,19 @@ WsLayout ws_layout(const Shape& sh, int B) {
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
   const int M = B * sh.N;
   w.Mpad = round_up(std::max(M, 1), kGemmRows);
-  w.stat_stride = sh.D / 16;
   w.meta = take(sizeof(Meta));
   w.rows = take((size_t)w.Mpad * sizeof(RowInfo));
   w.count = take(kMaxViews * 4);
   w.idx = take((size_t)M * 4);
   w.sim = take((size_t)M * 4);
   w.t0 = take((size_t)M * sh.D * 4);
+  w.z = take((size_t)w.Mpad * sh.D * sh.eb);
   w.q = take((size_t)w.Mpad * sh.D * sh.eb);
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
   w.h = take((size_t)w.Mpad * sh.D * 4);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
-  w.stats_x = take((size_t)w.Mpad * w.stat_stride * 8);
-  w.stats_h = take((size_t)w.Mpad * w.stat_stride * 8);
+  const int split = gemm_geom(sh, G_FC2).ksplit;
+  w.part = split > 1 ? take((size_t)split * w.Mpad * sh.D * 4) : off;
   w.total = off;
   return w;
 }
@@ -245,8 +245,7 @@ struct incvit_handle {
   std::vector<hipEvent_t> pool;
   double prof_ms[INCVIT_K_COUNT] = {};
   int64_t prof_n[INCVIT_K_COUNT] = {};
-  int waves[4] = {0, 0, 0, 0};  // 0 = automatic
-  int cols[4] = {0, 0, 0, 0};   // 0 = automatic
+  int cols[4] = {0, 0, 0, 0};  // 0 = automatic
 };
 
 struct incvit_graph {
@@ -308,12 +307,10 @@ const float* fptr(const incvit_handle* h, size_t off) { return reinterpret_cast<
 
 // Launch the per-layer kernels for the rows of the call (row map in ws).
 incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLayout& wl, char* ws,
-                         int max_rows_per_view, bool step, hipStream_t s) {
+                         int max_rows_per_view, int mmax, bool step, hipStream_t s) {
   const Shape& sh = h->sh;
   const RowInfo* rows = reinterpret_cast<const RowInfo*>(ws + wl.rows);
   const Meta* meta = reinterpret_cast<const Meta*>(ws + wl.meta);
-  float2* stats_x = reinterpret_cast<float2*>(ws + wl.stats_x);
-  float2* stats_h = reinterpret_cast<float2*>(ws + wl.stats_h);
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
     auto gemm = [&](int kind, int epi, int kernel_kind) -> incvit_status {
@@ -327,37 +324,55 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       a.layer = l;
       a.kchunks = g.kchunks;
       a.Nout = g.Nout;
-      a.stat_stride = wl.stat_stride;
       switch (kind) {
         case G_QKV:
+          a.A = ws + wl.z; a.lda = sh.D;
           a.ln_g = fptr(h, P.ln1_g); a.ln_b = fptr(h, P.ln1_b);
           a.W = h->packed + P.w_qkv; a.bias = fptr(h, P.b_qkv);
           a.out = ws + wl.q; a.ldo = sh.D;
-          a.stats_in = stats_x; a.nstat = l == 0 ? 1 : sh.D / 16;
           break;
         case G_OPROJ:
           a.A = ws + wl.o; a.lda = sh.D;
           a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
           a.out = ws + wl.h; a.ldo = sh.D;
-          a.stats_out = stats_h;
+          a.res = ws + wl.z;
           break;
         case G_FC1:
           a.A = ws + wl.h; a.lda = sh.D;
           a.ln_g = fptr(h, P.ln2_g); a.ln_b = fptr(h, P.ln2_b);
           a.W = h->packed + P.w_1; a.bias = fptr(h, P.b_1);
           a.out = ws + wl.g; a.ldo = sh.Fpad;
-          a.stats_in = stats_h; a.nstat = sh.D / 16;
           break;
         default:
           a.A = ws + wl.g; a.lda = sh.Fpad;
           a.W = h->packed + P.w_2; a.bias = fptr(h, P.b_2);
-          a.hres = reinterpret_cast<const float*>(ws + wl.h);
-          a.stats_out = stats_x;
+          a.out = ws + wl.z; a.ldo = sh.D;
+          a.res = ws + wl.h;
+          if (g.ksplit > 1) {  // partial sums; the row kernel adds bias and residual
+            epi = EPI_PART;
+            a.out = ws + wl.part;
+            a.mpad = wl.Mpad;
+          }
           break;
       }
-      const int waves = waves_of(h->waves, g, kind);
+      a.ksplit = g.ksplit;
       const int cols = cols_of(h->cols, g, kind);
-      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, waves, cols, a, s); });
+      incvit_status st = run(h, kernel_kind, s, [&] { return launch_gemm(epi, cols, a, s); });
+      if (st != INCVIT_OK || epi != EPI_PART) return st;
+      FixArgs f;
+      memset(&f, 0, sizeof f);
+      f.meta = meta;
+      f.rows = rows;
+      f.cl = h->cl;
+      f.sh = sh;
+      f.layer = l;
+      f.part = reinterpret_cast<const float*>(ws + wl.part);
+      f.ksplit = g.ksplit;
+      f.mpad = wl.Mpad;
+      f.h = reinterpret_cast<const float*>(ws + wl.h);
+      f.bias = fptr(h, P.b_2);
+      f.z = ws + wl.z;
+      return run(h, INCVIT_K_FC2_FIX, s, [&] { return launch_fix(f, mmax, s); });
     };
 
     incvit_status st;
@@ -548,10 +563,9 @@ incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patch
   ra.t0 = t0;
   ra.init_header = 1;
   ra.hash = h->hash;
-  ra.stats = reinterpret_cast<float2*>(ws + wl.stats_x);
-  ra.stat_stride = wl.stat_stride;
+  ra.z = ws + wl.z;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  if ((st = run_layers(h, views, B, wl, ws, sh.N, false, s)) != INCVIT_OK) return st;
+  if ((st = run_layers(h, views, B, wl, ws, sh.N, mmax, false, s)) != INCVIT_OK) return st;
   ra.init_header = 0;
   ra.g = fptr(h, h->pl.lnf_g);
   ra.b = fptr(h, h->pl.lnf_b);
@@ -611,10 +625,9 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   ra.cl = h->cl;
   ra.sh = sh;
   ra.t0 = t0;
-  ra.stats = reinterpret_cast<float2*>(ws + wl.stats_x);
-  ra.stat_stride = wl.stat_stride;
+  ra.z = ws + wl.z;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  if ((st = run_layers(h, views, B, wl, ws, max_rows, true, s)) != INCVIT_OK) return st;
+  if ((st = run_layers(h, views, B, wl, ws, max_rows, mmax, true, s)) != INCVIT_OK) return st;
   ra.g = fptr(h, h->pl.lnf_g);
   ra.b = fptr(h, h->pl.lnf_b);
   ra.refreshed = refreshed;
@@ -684,14 +697,10 @@ incvit_status incvit_profile_read(incvit_handle* h, double* total_ms, int64_t* l
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
   for (int k = 0; k < 4; ++k) {
-    const int v = t ? t->waves[k] : 0, c = t ? t->cols[k] : 0;
-    if (v != 0 && v != 4 && v != 8) return fail(h, INCVIT_ERR_ARG, "waves must be 0, 4 or 8");
+    const int c = t ? t->cols[k] : 0;
     if (c < 0 || c > 2) return fail(h, INCVIT_ERR_ARG, "cols must be 0, 1 or 2");
   }
-  for (int k = 0; k < 4; ++k) {
-    h->waves[k] = t ? t->waves[k] : 0;
-    h->cols[k] = t ? t->cols[k] : 0;
-  }
+  for (int k = 0; k < 4; ++k) h->cols[k] = t ? t->cols[k] : 0;
   return INCVIT_OK;
 }
 

@@ -1,0 +1,8 @@
+// Instances of the per-layer GEMM with the FC2 epilogue.
+#include "gemm.hpp"
+
+namespace incvit {
+
+hipError_t launch_gemm_fc2(int cols, const GemmArgs& a, hipStream_t s) { return launch_gemm_epi<EPI_FC2>(cols, a, s); }
+
+}  // namespace incvit

@@ -227,7 +227,7 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   for (int j = 0; j < kPer; ++j) t[j] = (lane + 64 * j < D) ? src[lane + 64 * j] : 0.0f;
   float* ref = reinterpret_cast<float*>(cache + a.cl.ref) + (size_t)tok * D;
   T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
-  float s1 = 0.0f, s2 = 0.0f;
+  T* z0 = static_cast<T*>(a.z) + (size_t)r * D;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int d = lane + 64 * j;
@@ -235,17 +235,10 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
       const T o = Elem<T>::cv(t[j]);
       ref[d] = t[j];
       x0[d] = o;
-      const float q = Elem<T>::ld(&o, 0);
-      s1 += q;
-      s2 += q * q;
+      z0[d] = o;
     }
   }
-  s1 = wave_sum(s1);
-  s2 = wave_sum(s2);
-  if (lane == 0) {
-    a.rows[r] = RowInfo{cache, tok, v};
-    a.stats[(size_t)r * a.stat_stride] = make_float2(s1, s2);
-  }
+  if (lane == 0) a.rows[r] = RowInfo{cache, tok, v};
 }
 
 // One wave per compact row: Y[tok] = S(LN_f(X^L[tok])); refreshed[v][j] = Y[tok].
@@ -253,11 +246,11 @@ template <class T>
 __global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
   const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int M = a.meta->m;
-  const RowInfo ri = a.rows[r];  // in bounds for every launched row; used only if r < M
-  if (r >= M) return;
+  // the row map and the compact Z_L rows are padded past every launched row,
+  // so these loads go out before M is known; rows past M are dropped below
+  const RowInfo ri = a.rows[r];
   const int D = a.sh.D;
-  const int j0 = r - a.meta->off[ri.view];
-  const INCVIT_GLOBAL T* x = gbl(x_row<T>(ri.cache, a.cl, a.sh, a.sh.L, ri.tok));
+  const T* x = static_cast<const T*>(a.z) + (size_t)r * D;
   constexpr int kMaxPer = kMaxDim / 64;
   float vals[kMaxPer], gv[kMaxPer], bv[kMaxPer];
 #pragma unroll
@@ -267,6 +260,8 @@ __global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
     gv[j] = d < D ? a.g[d] : 0.0f;
     bv[j] = d < D ? a.b[d] : 0.0f;
   }
+  if (r >= M) return;
+  const int j0 = r - a.meta->off[ri.view];
   float s = 0.0f;
 #pragma unroll
   for (int j = 0; j < kMaxPer; ++j) s += vals[j];
