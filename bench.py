@@ -72,20 +72,34 @@ def stored_traffic(workload: str, kind: str):
     return vals.get(kind)
 
 
-def gemm_bytes(m, M: float, kind: str) -> float:
-    """Algorithmic HBM bytes of one launch of a layer kernel with M refreshed rows."""
-    D, F, N, eb = m.dim, m.mlp_dim, m.n_tokens, (2 if m.dtype == "bf16" else 4)
+def ksplit(m, kind: str) -> int:
+    """K split of the output / MLP-down projections (the library's rule)."""
+    nblocks = m.dim // 16
+    kchunks = (m.dim if kind == "oproj" else -(-m.mlp_dim // 32) * 32) // 32
+    return max(1, min(4, 256 // nblocks, kchunks // 8))
+
+
+def kernel_bytes(m, M: float, kind: str):
+    """Algorithmic HBM bytes of one launch of a layer kernel with M refreshed rows
+    (weights once, each row operand once; partial sums of a split K counted as
+    written and read once).  None for kinds without a figure here."""
+    D, F, eb = m.dim, m.mlp_dim, (2 if m.dtype == "bf16" else 4)
+    so, s2 = ksplit(m, "oproj"), ksplit(m, "fc2")
     if kind == "qkv":
-        return D * 3 * D * eb + M * D * eb + M * 3 * D * eb
+        return 3 * D * D * eb + M * D * eb + 3 * M * D * eb
     if kind == "oproj":
-        return D * D * eb + 2 * M * D * eb + M * D * 4
+        return D * D * eb + M * D * eb + so * M * D * 4
+    if kind == "res_ln2":
+        return so * M * D * 4 + M * D * eb + M * D * 4 + M * D * eb
     if kind == "fc1":
-        return D * F * eb + M * D * 4 + M * F * eb
+        return D * F * eb + M * D * eb + M * F * eb
     if kind == "fc2":
-        return F * D * eb + M * F * eb + M * D * 4 + M * D * eb
+        return F * D * eb + M * F * eb + s2 * M * D * 4
+    if kind == "res_ln1":
+        return s2 * M * D * 4 + M * D * 4 + 3 * M * D * eb
     if kind == "attn":
-        return 2 * M * D * eb  # + K/V of the views, added by the caller
-    raise KeyError(kind)
+        return 2 * M * D * eb  # + K/V of the streams, added by the caller
+    return None
 
 
 def cpu_baseline(wl, frames, seconds: float):
@@ -388,12 +402,9 @@ def main() -> int:
         kinds = {k: v for k, v in prof.items() if v[1] > 0}
         dom = max(kinds, key=lambda k: kinds[k][0])
         avg_us = kinds[dom][0] * 1e3 / kinds[dom][1]
-        if dom in ("qkv", "oproj", "fc1", "fc2"):
-            nbytes = gemm_bytes(m, mean_rows, dom)
-        elif dom == "attn":
-            nbytes = gemm_bytes(m, mean_rows, "attn") + 2 * B * m.n_tokens * m.dim * (2 if m.dtype == "bf16" else 4)
-        else:
-            nbytes = None
+        nbytes = kernel_bytes(m, mean_rows, dom)
+        if dom == "attn":
+            nbytes += 2 * B * m.n_tokens * m.dim * (2 if m.dtype == "bf16" else 4)
         achieved = nbytes / (avg_us * 1e-6) / 1e9 if nbytes else None
         result["roofline"] = {
             "kernel": dom, "bound": "hbm", "achieved": round(achieved, 1) if achieved else None,

@@ -208,17 +208,25 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);
 
 /* Kernel kinds for the per-kernel timers. */
 typedef enum {
-  INCVIT_K_EMBED = 0, INCVIT_K_SIM, INCVIT_K_SELECT, INCVIT_K_COMMIT,
-  INCVIT_K_QKV, INCVIT_K_ATTN, INCVIT_K_OPROJ, INCVIT_K_FC1, INCVIT_K_FC2,
-  INCVIT_K_FINAL, INCVIT_K_FC2_FIX, INCVIT_K_COUNT
+  INCVIT_K_EMBED = 0, /* patch embedding + position, all tokens            */
+  INCVIT_K_SIM,       /* cosine against the cached reference              */
+  INCVIT_K_SELECT,    /* threshold / top-k selection and compaction      */
+  INCVIT_K_COMMIT,    /* ref, X0 of the selected rows; LN1 of layer 0     */
+  INCVIT_K_QKV,       /* QKV projection, K/V scattered into the cache     */
+  INCVIT_K_ATTN,      /* attention of the selected queries                */
+  INCVIT_K_OPROJ,     /* output projection (split-K partial sums)         */
+  INCVIT_K_RES_LN2,   /* + bias + residual -> H; LN2                      */
+  INCVIT_K_FC1,       /* MLP up projection + GELU                         */
+  INCVIT_K_FC2,       /* MLP down projection (split-K partial sums)       */
+  INCVIT_K_RES_LN1,   /* + bias + residual -> X^{l+1}; next LN1 or final LN */
+  INCVIT_K_COUNT
 } incvit_kernel_kind;
 
 /* When enabled, every kernel launch of the encode calls records a start and a
  * stop event with its own dispatch on the call's stream (no extra stream
  * operations); incvit_profile_read synchronises those events and returns, per
  * kind, the summed duration (ms) and the number of launches since the last
- * reset.  INCVIT_K_FC2 counts the MLP down projection's GEMM and
- * INCVIT_K_FC2_FIX the row kernel that finishes it when its K is split. */
+ * reset. */
 incvit_status incvit_profile_enable(incvit_handle* h, int32_t enable);
 incvit_status incvit_profile_read(incvit_handle* h, double* total_ms /* [INCVIT_K_COUNT] */,
                                   int64_t* launches /* [INCVIT_K_COUNT] */, int32_t reset);

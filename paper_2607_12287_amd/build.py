@@ -14,8 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libincvit.so")
-SOURCES = ["incvit_api.hip", "k_embed.hip", "k_select.hip", "k_gemm.hip", "k_gemm_qkv.hip", "k_gemm_oproj.hip",
-           "k_gemm_fc1.hip", "k_gemm_fc2.hip", "k_gemm_part.hip", "k_attn.hip", "k_misc.hip"]
+SOURCES = ["incvit_api.hip", "k_embed.hip", "k_select.hip", "k_gemm.hip", "k_gemm_qkv.hip",
+           "k_gemm_fc1.hip", "k_gemm_part.hip", "k_rows.hip", "k_attn.hip", "k_misc.hip"]
 # the fixed-order fp32 embedding and cosine must not be contracted beyond the
 # explicit fma intrinsics
 NO_CONTRACT = {"k_embed.hip"}

@@ -125,23 +125,23 @@ struct SelectArgs {
   int* count;  // [B]
 };
 
-struct RowsArgs {  // commit (ref/X0 of refreshed rows, row map) and final LayerNorm
+struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map, A1 of layer 0
   RowMap rm;
-  RowInfo* rows;     // commit writes, final reads
-  Meta* meta;        // commit writes, final reads
+  RowInfo* rows;     // commit writes
+  Meta* meta;        // commit writes
   Views caches;
   CacheLayout cl;
   Shape sh;
   const float* t0;
-  const float* g;
+  const float* g;    // LN1 of layer 0
   const float* b;
-  void* refreshed;   // final: optional [B][N][D]
   int init_header;   // commit of a full encode: write header
   uint32_t hash;
-  void* z;           // compact rows [Mpad][D]: commit writes Z_0, final reads Z_L
+  void* z;           // compact Z_0 [Mpad][D]
+  void* a;           // compact S(LN1(Z_0)) [Mpad][D]
 };
 
-enum Epi { EPI_QKV = 0, EPI_OPROJ = 1, EPI_FC1 = 2, EPI_FC2 = 3, EPI_PART = 4 };
+enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2 };
 
 struct GemmArgs {
   const RowInfo* rows;  // row map (cache, token, stream) of each compact row
@@ -149,33 +149,41 @@ struct GemmArgs {
   CacheLayout cl;
   Shape sh;
   int layer;
-  const void* A;      // compact A rows: QKV Z_l, OPROJ O, FC1 H (f32), FC2 G
+  const void* A;      // compact A rows (storage type): QKV A1, FC1 A2, PART O or G
   int lda;
-  const float* ln_g;  // QKV: LN1, FC1: LN2
-  const float* ln_b;
   const void* W;      // packed [Nout/16][kchunks][512]
-  const float* bias;  // [Nout]
+  const float* bias;  // [Nout] (not used by PART)
   int kchunks, Nout;
-  void* out;          // compact output: QKV Q, OPROJ H (f32), FC1 G, FC2 Z_{l+1}
+  void* out;          // QKV Q [Mpad][D]; FC1 G [Mpad][Fpad]; PART f32 [ksplit][mpad][ldo]
   int ldo;
-  const void* res;    // compact residual: OPROJ Z_l, FC2 H (f32); [row][D]
-  int ksplit;         // K is split over gridDim.y = ksplit workgroups (EPI_PART only)
-  int mpad;           // rows of one partial slice of `out` (EPI_PART)
+  int ksplit;         // K is split over gridDim.y = ksplit workgroups (PART)
+  int mpad;           // rows of one partial slice (PART)
 };
 
-// The rows of the MLP down projection when its K is split: Z_{l+1} =
-// S(H + (sum of the split partials, in split order) + b_2).
-struct FixArgs {
+// Row kernels that finish a split-K GEMM, one wave per compact row:
+//   RES_LN2: H = Z_l + (partials + b_o) -> H (f32) and A2 = S(LN2(H));
+//   RES_LN1: Z_{l+1} = S(H + (partials + b_2)) -> compact Z and X^{l+1} of the
+//            cache, then A1 = S(LN1 of layer l+1 (Z_{l+1})), or after the last
+//            layer Y = S(LN_f(Z_L)) into the cache and the refreshed output.
+enum ResMode { RES_LN2 = 0, RES_LN1 = 1 };
+struct ResArgs {
   const Meta* meta;
   const RowInfo* rows;
   CacheLayout cl;
   Shape sh;
   int layer;
+  int last;           // RES_LN1 after the last layer: final LayerNorm
   const float* part;  // [ksplit][mpad][D]
   int ksplit, mpad;
-  const float* h;     // [Mpad][D]
-  const float* bias;  // b_2 [D]
-  void* z;            // compact Z_{l+1} [Mpad][D]
+  const void* res;    // RES_LN2: Z_l (storage type); RES_LN1: H (f32)
+  const float* bias;
+  const float* ln_g;  // the LayerNorm applied to the new rows
+  const float* ln_b;
+  float* h_out;       // RES_LN2: H
+  void* z_out;        // RES_LN1: Z_{l+1}
+  void* a_out;        // normalised rows (not for the final LayerNorm)
+  void* refreshed;    // final: optional [B][N][D]
+  int N;
 };
 
 struct AttnArgs {
@@ -238,9 +246,8 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
-hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
-hipError_t launch_fix(const FixArgs& a, int mmax, hipStream_t s);
+hipError_t launch_res(int mode, const ResArgs& a, int mmax, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);

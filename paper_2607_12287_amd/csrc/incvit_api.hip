@@ -36,7 +36,7 @@ struct CanonLayout {  // element offsets into the canonical buffer
 };
 
 struct WsLayout {
-  size_t meta, rows, count, idx, sim, t0, z, q, o, h, g, part, total;
+  size_t meta, rows, count, idx, sim, t0, z, a, q, o, h, g, part, total;
   int Mpad;
 };
 
@@ -186,12 +186,13 @@ GemmGeom gemm_geom(const Shape& sh, int kind) {
   }
   g.kchunks = round_up(g.K, 32) / 32;
   g.nblocks = g.Nout / 16;
-  // Split K over workgroups when one workgroup's 8 waves would each need more
-  // than 8 chunks in registers (the MLP down projection, K = F): the partial
-  // sums then finish in a row kernel.  The LayerNorm GEMMs have K = D <= 2048,
-  // which never splits (their statistics need whole rows).
-  const int need = (g.kchunks + 7) / 8;
-  g.ksplit = need > 8 ? std::min(4, (need + 5) / 6) : 1;
+  // The output projection and the MLP down projection have D/16 column blocks,
+  // too few to fill 256 CUs: their K is split over up to 4 workgroups (at least
+  // 8 chunks each), and a row kernel adds the partial sums, the bias, the
+  // residual and the next LayerNorm.  QKV and fc1 are not split.
+  g.ksplit = 1;
+  if (kind == G_OPROJ || kind == G_FC2)
+    g.ksplit = std::max(1, std::min(std::min(4, 256 / std::max(g.nblocks, 1)), g.kchunks / 8));
   return g;
 }
 
@@ -216,12 +217,13 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.sim = take((size_t)M * 4);
   w.t0 = take((size_t)M * sh.D * 4);
   w.z = take((size_t)w.Mpad * sh.D * sh.eb);
+  w.a = take((size_t)w.Mpad * sh.D * sh.eb);
   w.q = take((size_t)w.Mpad * sh.D * sh.eb);
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
   w.h = take((size_t)w.Mpad * sh.D * 4);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
-  const int split = gemm_geom(sh, G_FC2).ksplit;
-  w.part = split > 1 ? take((size_t)split * w.Mpad * sh.D * 4) : off;
+  const int split = std::max(gemm_geom(sh, G_OPROJ).ksplit, gemm_geom(sh, G_FC2).ksplit);
+  w.part = take((size_t)split * w.Mpad * sh.D * 4);
   w.total = off;
   return w;
 }
@@ -306,14 +308,16 @@ incvit_status run(incvit_handle* h, int kind, hipStream_t s, F&& launch) {
 const float* fptr(const incvit_handle* h, size_t off) { return reinterpret_cast<const float*>(h->packed + off); }
 
 // Launch the per-layer kernels for the rows of the call (row map in ws).
+// Launch the per-layer kernels for the rows of the call (row map in ws).
+// refreshed: optional output of the last layer's final LayerNorm rows.
 incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLayout& wl, char* ws,
-                         int max_rows_per_view, int mmax, bool step, hipStream_t s) {
+                         int max_rows_per_view, int mmax, bool step, void* refreshed, hipStream_t s) {
   const Shape& sh = h->sh;
   const RowInfo* rows = reinterpret_cast<const RowInfo*>(ws + wl.rows);
   const Meta* meta = reinterpret_cast<const Meta*>(ws + wl.meta);
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
-    auto gemm = [&](int kind, int epi, int kernel_kind) -> incvit_status {
+    auto gemm = [&](int kind, int kernel_kind) -> incvit_status {
       const GemmGeom g = gemm_geom(sh, kind);
       GemmArgs a;
       memset(&a, 0, sizeof a);
@@ -324,59 +328,76 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       a.layer = l;
       a.kchunks = g.kchunks;
       a.Nout = g.Nout;
+      a.ksplit = g.ksplit;
+      a.mpad = wl.Mpad;
+      int epi = EPI_PART;
       switch (kind) {
         case G_QKV:
-          a.A = ws + wl.z; a.lda = sh.D;
-          a.ln_g = fptr(h, P.ln1_g); a.ln_b = fptr(h, P.ln1_b);
+          epi = EPI_QKV;
+          a.A = ws + wl.a; a.lda = sh.D;
           a.W = h->packed + P.w_qkv; a.bias = fptr(h, P.b_qkv);
           a.out = ws + wl.q; a.ldo = sh.D;
           break;
         case G_OPROJ:
           a.A = ws + wl.o; a.lda = sh.D;
-          a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
-          a.out = ws + wl.h; a.ldo = sh.D;
-          a.res = ws + wl.z;
+          a.W = h->packed + P.w_o;
+          a.out = ws + wl.part; a.ldo = sh.D;
           break;
         case G_FC1:
-          a.A = ws + wl.h; a.lda = sh.D;
-          a.ln_g = fptr(h, P.ln2_g); a.ln_b = fptr(h, P.ln2_b);
+          epi = EPI_FC1;
+          a.A = ws + wl.a; a.lda = sh.D;
           a.W = h->packed + P.w_1; a.bias = fptr(h, P.b_1);
           a.out = ws + wl.g; a.ldo = sh.Fpad;
           break;
         default:
           a.A = ws + wl.g; a.lda = sh.Fpad;
-          a.W = h->packed + P.w_2; a.bias = fptr(h, P.b_2);
-          a.out = ws + wl.z; a.ldo = sh.D;
-          a.res = ws + wl.h;
-          if (g.ksplit > 1) {  // partial sums; the row kernel adds bias and residual
-            epi = EPI_PART;
-            a.out = ws + wl.part;
-            a.mpad = wl.Mpad;
-          }
+          a.W = h->packed + P.w_2;
+          a.out = ws + wl.part; a.ldo = sh.D;
           break;
       }
-      a.ksplit = g.ksplit;
       const int cols = cols_of(h->cols, g, kind);
-      incvit_status st = run(h, kernel_kind, s, [&] { return launch_gemm(epi, cols, a, s); });
-      if (st != INCVIT_OK || epi != EPI_PART) return st;
-      FixArgs f;
-      memset(&f, 0, sizeof f);
-      f.meta = meta;
-      f.rows = rows;
-      f.cl = h->cl;
-      f.sh = sh;
-      f.layer = l;
-      f.part = reinterpret_cast<const float*>(ws + wl.part);
-      f.ksplit = g.ksplit;
-      f.mpad = wl.Mpad;
-      f.h = reinterpret_cast<const float*>(ws + wl.h);
-      f.bias = fptr(h, P.b_2);
-      f.z = ws + wl.z;
-      return run(h, INCVIT_K_FC2_FIX, s, [&] { return launch_fix(f, mmax, s); });
+      return run(h, kernel_kind, s, [&] { return launch_gemm(epi, cols, a, s); });
+    };
+    auto rowk = [&](int mode, int kernel_kind) -> incvit_status {
+      const GemmGeom g = gemm_geom(sh, mode == RES_LN2 ? G_OPROJ : G_FC2);
+      ResArgs r;
+      memset(&r, 0, sizeof r);
+      r.meta = meta;
+      r.rows = rows;
+      r.cl = h->cl;
+      r.sh = sh;
+      r.layer = l;
+      r.part = reinterpret_cast<const float*>(ws + wl.part);
+      r.ksplit = g.ksplit;
+      r.mpad = wl.Mpad;
+      r.N = sh.N;
+      if (mode == RES_LN2) {
+        r.res = ws + wl.z;
+        r.bias = fptr(h, P.b_o);
+        r.ln_g = fptr(h, P.ln2_g);
+        r.ln_b = fptr(h, P.ln2_b);
+        r.h_out = reinterpret_cast<float*>(ws + wl.h);
+        r.a_out = ws + wl.a;
+      } else {
+        r.res = ws + wl.h;
+        r.bias = fptr(h, P.b_2);
+        r.z_out = ws + wl.z;
+        r.last = l + 1 == sh.L;
+        if (r.last) {
+          r.ln_g = fptr(h, h->pl.lnf_g);
+          r.ln_b = fptr(h, h->pl.lnf_b);
+          r.refreshed = refreshed;
+        } else {
+          r.ln_g = fptr(h, h->pl.layers[l + 1].ln1_g);
+          r.ln_b = fptr(h, h->pl.layers[l + 1].ln1_b);
+          r.a_out = ws + wl.a;
+        }
+      }
+      return run(h, kernel_kind, s, [&] { return launch_res(mode, r, mmax, s); });
     };
 
     incvit_status st;
-    if ((st = gemm(G_QKV, EPI_QKV, INCVIT_K_QKV)) != INCVIT_OK) return st;
+    if ((st = gemm(G_QKV, INCVIT_K_QKV)) != INCVIT_OK) return st;
     AttnArgs aa;
     memset(&aa, 0, sizeof aa);
     aa.meta = meta;
@@ -391,9 +412,11 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
     aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
     aa.split = step ? 4 : 1;
     if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, s); })) != INCVIT_OK) return st;
-    if ((st = gemm(G_OPROJ, EPI_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
-    if ((st = gemm(G_FC1, EPI_FC1, INCVIT_K_FC1)) != INCVIT_OK) return st;
-    if ((st = gemm(G_FC2, EPI_FC2, INCVIT_K_FC2)) != INCVIT_OK) return st;
+    if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
+    if ((st = rowk(RES_LN2, INCVIT_K_RES_LN2)) != INCVIT_OK) return st;
+    if ((st = gemm(G_FC1, INCVIT_K_FC1)) != INCVIT_OK) return st;
+    if ((st = gemm(G_FC2, INCVIT_K_FC2)) != INCVIT_OK) return st;
+    if ((st = rowk(RES_LN1, INCVIT_K_RES_LN1)) != INCVIT_OK) return st;
   }
   return INCVIT_OK;
 }
@@ -564,13 +587,11 @@ incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patch
   ra.init_header = 1;
   ra.hash = h->hash;
   ra.z = ws + wl.z;
+  ra.a = ws + wl.a;
+  ra.g = fptr(h, h->pl.layers[0].ln1_g);
+  ra.b = fptr(h, h->pl.layers[0].ln1_b);
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  if ((st = run_layers(h, views, B, wl, ws, sh.N, mmax, false, s)) != INCVIT_OK) return st;
-  ra.init_header = 0;
-  ra.g = fptr(h, h->pl.lnf_g);
-  ra.b = fptr(h, h->pl.lnf_b);
-  ra.refreshed = nullptr;
-  return run(h, INCVIT_K_FINAL, s, [&] { return launch_final(ra, mmax, s); });
+  return run_layers(h, views, B, wl, ws, sh.N, mmax, false, nullptr, s);
 }
 
 incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, void* const* caches, float tau,
@@ -626,12 +647,11 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   ra.sh = sh;
   ra.t0 = t0;
   ra.z = ws + wl.z;
+  ra.a = ws + wl.a;
+  ra.g = fptr(h, h->pl.layers[0].ln1_g);
+  ra.b = fptr(h, h->pl.layers[0].ln1_b);
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  if ((st = run_layers(h, views, B, wl, ws, max_rows, mmax, true, s)) != INCVIT_OK) return st;
-  ra.g = fptr(h, h->pl.lnf_g);
-  ra.b = fptr(h, h->pl.lnf_b);
-  ra.refreshed = refreshed;
-  return run(h, INCVIT_K_FINAL, s, [&] { return launch_final(ra, mmax, s); });
+  return run_layers(h, views, B, wl, ws, max_rows, mmax, true, refreshed, s);
 }
 
 incvit_status incvit_cache_export(const incvit_handle* h, const void* cache, void* canonical_dst, void* stream) {

@@ -1,0 +1,164 @@
+// Row kernels that finish the split-K projections of a layer (paper §III-B:
+// the residual additions around the attention output and the MLP, and the
+// LayerNorm that opens the next sublayer), one wave per compact row:
+//
+//   RES_LN2: H  = Z_l + ((P_0 + P_1 + ...) + b_o)          (fp32)
+//            A2 = S(LN2(H))                                 (input of fc1)
+//   RES_LN1: Z' = S(H + ((P_0 + P_1 + ...) + b_2))          (X^{l+1} rows)
+//            A1 = S(LN1 of the next layer (Z'))             (input of QKV)
+//            or, after the last layer, Y = S(LN_f(Z')) into the cache and the
+//            caller's `refreshed` rows.
+//
+// The partial sums are added in split order, then the bias, then the residual,
+// which is the order the unsplit product would use.  LayerNorm: two passes
+// (mean, then mean squared deviation) over the row in fp32, lane partials
+// summed in index order and combined across lanes by a fixed butterfly.
+// Every load is issued before M is known (the compact buffers are padded past
+// every launched row); rows at or past M return before storing anything.
+#include "common.hpp"
+
+namespace incvit {
+
+namespace {
+
+__device__ __forceinline__ float4 ld4(const float* p, int q) { return reinterpret_cast<const float4*>(p)[q]; }
+
+// 4 consecutive storage elements as floats
+__device__ __forceinline__ float4 ld4s(const float* p, int q) { return ld4(p, q); }
+__device__ __forceinline__ float4 ld4s(const uint16_t* p, int q) {
+  const uint2 u = reinterpret_cast<const uint2*>(p)[q];
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+
+__device__ __forceinline__ void st4(float* p, int q, float4 v) { reinterpret_cast<float4*>(p)[q] = v; }
+__device__ __forceinline__ void st4(uint16_t* p, int q, float4 v) {
+  const uint32_t lo = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
+  const uint32_t hi = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  reinterpret_cast<uint2*>(p)[q] = make_uint2(lo, hi);
+}
+
+__device__ __forceinline__ float4 rnd4(float4 v, float*) { return v; }
+__device__ __forceinline__ float4 rnd4(float4 v, uint16_t*) {
+  return make_float4(bf2f(f2bf(v.x)), bf2f(f2bf(v.y)), bf2f(f2bf(v.z)), bf2f(f2bf(v.w)));
+}
+
+__device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w); }
+
+}  // namespace
+
+// KP: float4 slots per lane (D <= 256 * KP); S: K splits.
+template <class T, int MODE, int S, int KP>
+__global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
+  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int M = a.meta->m;
+  const int D = a.sh.D, D4 = D / 4;
+  const RowInfo ri = a.rows[r];
+
+  float4 p[S][KP], res[KP], bias[KP], gam[KP], bet[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = min(lane + 64 * j, D4 - 1);
+#pragma unroll
+    for (int s = 0; s < S; ++s) p[s][j] = ld4(a.part + ((size_t)s * a.mpad + r) * D, q);
+    if constexpr (MODE == RES_LN2)
+      res[j] = ld4s(static_cast<const T*>(a.res) + (size_t)r * D, q);
+    else
+      res[j] = ld4(static_cast<const float*>(a.res) + (size_t)r * D, q);
+    bias[j] = ld4(a.bias, q);
+    gam[j] = ld4(a.ln_g, q);
+    bet[j] = ld4(a.ln_b, q);
+  }
+  if (r >= M) return;
+
+  // the new rows (H, or the rounded Z'), and their sum over the row
+  float4 v[KP];
+  float sum = 0.0f;
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    float4 x = p[0][j];
+#pragma unroll
+    for (int s = 1; s < S; ++s) x = add4(x, p[s][j]);
+    x = add4(x, bias[j]);
+    v[j] = add4(res[j], x);
+    if constexpr (MODE == RES_LN1) v[j] = rnd4(v[j], static_cast<T*>(nullptr));
+    if (lane + 64 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+  }
+  const float mean = wave_sum(sum) / (float)D;
+  float sq = 0.0f;
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    if (lane + 64 * j < D4) {
+      const float dx = v[j].x - mean, dy = v[j].y - mean, dz = v[j].z - mean, dw = v[j].w - mean;
+      sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + a.sh.eps);
+
+  T* xrow = nullptr;
+  T* yrow = nullptr;
+  T* outrow = nullptr;
+  if constexpr (MODE == RES_LN1) {
+    xrow = x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok);
+    if (a.last) {
+      yrow = reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D;
+      if (a.refreshed)
+        outrow = static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + (r - a.meta->off[ri.view])) * D;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = lane + 64 * j;
+    if (q < D4) {
+      const float4 n4 = make_float4((v[j].x - mean) * rstd * gam[j].x + bet[j].x,
+                                    (v[j].y - mean) * rstd * gam[j].y + bet[j].y,
+                                    (v[j].z - mean) * rstd * gam[j].z + bet[j].z,
+                                    (v[j].w - mean) * rstd * gam[j].w + bet[j].w);
+      if constexpr (MODE == RES_LN2) {
+        st4(a.h_out + (size_t)r * D, q, v[j]);
+        st4(static_cast<T*>(a.a_out) + (size_t)r * D, q, n4);
+      } else {
+        st4(static_cast<T*>(a.z_out) + (size_t)r * D, q, v[j]);
+        st4(xrow, q, v[j]);
+        if (a.last) {
+          st4(yrow, q, n4);
+          if (outrow) st4(outrow, q, n4);
+        } else {
+          st4(static_cast<T*>(a.a_out) + (size_t)r * D, q, n4);
+        }
+      }
+    }
+  }
+}
+
+namespace {
+
+template <class T, int MODE, int S>
+hipError_t launch_s(const ResArgs& a, dim3 grid, hipStream_t s) {
+  const int kp = (a.sh.D + 255) / 256;
+  if (kp <= 2) return launch_k(res_kernel<T, MODE, S, 2>, grid, dim3(256), 0, s, a);
+  if (kp <= 5) return launch_k(res_kernel<T, MODE, S, 5>, grid, dim3(256), 0, s, a);
+  return launch_k(res_kernel<T, MODE, S, 8>, grid, dim3(256), 0, s, a);
+}
+
+template <class T, int MODE>
+hipError_t launch_mode(const ResArgs& a, dim3 grid, hipStream_t s) {
+  switch (a.ksplit) {
+    case 1: return launch_s<T, MODE, 1>(a, grid, s);
+    case 2: return launch_s<T, MODE, 2>(a, grid, s);
+    case 3: return launch_s<T, MODE, 3>(a, grid, s);
+    case 4: return launch_s<T, MODE, 4>(a, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_res(int mode, const ResArgs& a, int mmax, hipStream_t s) {
+  const dim3 grid(max(1, (mmax + 3) / 4));
+  if (a.sh.dtype)
+    return mode == RES_LN2 ? launch_mode<uint16_t, RES_LN2>(a, grid, s) : launch_mode<uint16_t, RES_LN1>(a, grid, s);
+  return mode == RES_LN2 ? launch_mode<float, RES_LN2>(a, grid, s) : launch_mode<float, RES_LN1>(a, grid, s);
+}
+
+}  // namespace incvit

@@ -228,6 +228,22 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   float* ref = reinterpret_cast<float*>(cache + a.cl.ref) + (size_t)tok * D;
   T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
   T* z0 = static_cast<T*>(a.z) + (size_t)r * D;
+  T* a0 = static_cast<T*>(a.a) + (size_t)r * D;
+  // Z_0 = S(T0) and the layer-0 QKV input S(LN1(Z_0)), LayerNorm in two passes
+  float zr[kPer], sum = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    zr[j] = Elem<T>::rnd(t[j]);
+    if (lane + 64 * j < D) sum += zr[j];
+  }
+  const float mean = wave_sum(sum) / (float)D;
+  float sq = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const float dv = zr[j] - mean;
+    if (lane + 64 * j < D) sq += dv * dv;
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + a.sh.eps);
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int d = lane + 64 * j;
@@ -236,55 +252,10 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
       ref[d] = t[j];
       x0[d] = o;
       z0[d] = o;
+      a0[d] = Elem<T>::cv((zr[j] - mean) * rstd * a.g[d] + a.b[d]);
     }
   }
   if (lane == 0) a.rows[r] = RowInfo{cache, tok, v};
-}
-
-// One wave per compact row: Y[tok] = S(LN_f(X^L[tok])); refreshed[v][j] = Y[tok].
-template <class T>
-__global__ __launch_bounds__(256) void final_kernel(RowsArgs a) {
-  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int M = a.meta->m;
-  // the row map and the compact Z_L rows are padded past every launched row,
-  // so these loads go out before M is known; rows past M are dropped below
-  const RowInfo ri = a.rows[r];
-  const int D = a.sh.D;
-  const T* x = static_cast<const T*>(a.z) + (size_t)r * D;
-  constexpr int kMaxPer = kMaxDim / 64;
-  float vals[kMaxPer], gv[kMaxPer], bv[kMaxPer];
-#pragma unroll
-  for (int j = 0; j < kMaxPer; ++j) {
-    const int d = lane + 64 * j;
-    vals[j] = d < D ? Elem<T>::f(x[d]) : 0.0f;
-    gv[j] = d < D ? a.g[d] : 0.0f;
-    bv[j] = d < D ? a.b[d] : 0.0f;
-  }
-  if (r >= M) return;
-  const int j0 = r - a.meta->off[ri.view];
-  float s = 0.0f;
-#pragma unroll
-  for (int j = 0; j < kMaxPer; ++j) s += vals[j];
-  const float mean = wave_sum(s) / (float)D;
-  float q = 0.0f;
-#pragma unroll
-  for (int j = 0; j < kMaxPer; ++j) {
-    const int d = lane + 64 * j;
-    const float c = vals[j] - mean;
-    q += d < D ? c * c : 0.0f;
-  }
-  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + a.sh.eps);
-  INCVIT_GLOBAL T* y = gbl(reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D);
-  T* out = a.refreshed ? reinterpret_cast<T*>(a.refreshed) + ((size_t)ri.view * a.rm.N + j0) * D : nullptr;
-#pragma unroll
-  for (int j = 0; j < kMaxPer; ++j) {
-    const int d = lane + 64 * j;
-    if (d < D) {
-      const T o = Elem<T>::cv((vals[j] - mean) * rstd * gv[j] + bv[j]);
-      y[d] = o;
-      if (out) out[d] = o;
-    }
-  }
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
@@ -299,11 +270,6 @@ hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_final(const RowsArgs& a, int mmax, hipStream_t s) {
-  dim3 grid(max(1, (mmax + 3) / 4));
-  if (a.sh.dtype) (void)launch_k(final_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  else (void)launch_k(final_kernel<float>, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
-}
+
 
 }  // namespace incvit

@@ -20,7 +20,7 @@ INCVIT_OK, INCVIT_ERR_ARG, INCVIT_ERR_SHAPE, INCVIT_ERR_UNSUPPORTED, INCVIT_ERR_
 STATUS_NAMES = {0: "INCVIT_OK", -1: "INCVIT_ERR_ARG", -2: "INCVIT_ERR_SHAPE", -3: "INCVIT_ERR_UNSUPPORTED",
                 -4: "INCVIT_ERR_STATE", -5: "INCVIT_ERR_HIP"}
 INCVIT_F32, INCVIT_BF16 = 0, 1
-KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "fc1", "fc2", "final", "fc2_fix")
+KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "res_ln2", "fc1", "fc2", "res_ln1")
 
 # Exported symbols, as declared in include/incvit.h.
 EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "incvit_pack_weights",
