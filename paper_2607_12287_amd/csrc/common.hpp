@@ -197,8 +197,6 @@ struct AttnArgs {
   void* o;        // [Mpad][D]
   int qmax;       // Mpad - 1: last row a clamped load may touch
   float scale_log2;
-  int split;      // 4: one 16-query tile per workgroup, keys split over 4 waves;
-                  // 1: four 16-query tiles per workgroup, one per wave
 };
 
 struct PackArgs {

@@ -410,7 +410,6 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
     aa.o = ws + wl.o;
     aa.qmax = wl.Mpad - 1;
     aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
-    aa.split = step ? 4 : 1;
     if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, s); })) != INCVIT_OK) return st;
     if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
     if ((st = rowk(RES_LN2, INCVIT_K_RES_LN2)) != INCVIT_OK) return st;

@@ -2,13 +2,11 @@
 // (paper §III-B: attention is computed only for the updated tokens; the keys
 // and values are the scattered full K/V -- new rows for U, cached rows for R).
 //
-// One wave owns 16 queries of one head.  Per block of 32 keys it forms
-// S^T = K Q^T with MFMA (so each lane keeps a single query and its softmax
-// state), updates the online softmax in fp32 (exp2 with the 1/sqrt(d_h)
-// scale folded in), and accumulates O^T = V^T P^T with MFMA.  V is cached
-// transposed per head ([d_h][Npad]) so that the P^T operand needs no lane
-// exchange.  For few queries (an incremental step) the 4 waves of a workgroup
-// split the keys and their partial results are merged in a fixed order.
+// Per block of 32 keys and tile of 16 queries a wave forms S^T = K Q^T with
+// MFMA (so each lane keeps a single query and its softmax state), updates the
+// online softmax in fp32 (exp2 with the 1/sqrt(d_h) scale folded in), and
+// accumulates O^T = V^T P^T with MFMA.  V is cached transposed per head
+// ([d_h][Npad]) so that the P^T operand needs no lane exchange.
 #include "common.hpp"
 
 namespace incvit {
@@ -107,20 +105,24 @@ __device__ __forceinline__ void load_vblock(V8<T> (&vop)[NDT], const T* vbase, i
   }
 }
 
-template <class T, int NDC, int NDT>
+// One workgroup: QT query tiles (16 queries each) of one head of one stream;
+// its KW waves split the stream's key blocks into contiguous runs and each
+// wave processes every query tile of the workgroup against its keys, so a
+// key/value block is read once for QT*16 queries.  Key/value loads do not
+// depend on the row offsets, so the first group of them is issued before the
+// offsets are read; the first stream's rows always start at 0, so its query
+// loads are issued early too.  The waves' (max, sum, O) are merged in a fixed
+// two-level tree through LDS.
+template <class T, int NDC, int NDT, int GB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
-  __shared__ float s_m[4][16], s_l[4][16];
-  __shared__ f32x4_t s_o[4][NDT][64];
+  constexpr int KW = 4, QT = 2;
+  __shared__ float s_m[2][QT][16], s_l[2][QT][16];
+  __shared__ f32x4_t s_o[2][QT][NDT][64];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, n = lane & 15;
   const int h = blockIdx.y, v = blockIdx.z;
-  const int rowbase = a.meta->off[v];
-  const int kv = a.meta->off[v + 1] - rowbase;
-  const int qt = a.split == 4 ? (int)blockIdx.x : (int)blockIdx.x * 4 + w;
-  const int q0 = qt * 16;
-  if (a.split == 4 && q0 >= kv) return;
-  const bool active = q0 < kv;
   const int N = a.sh.N, Npad = a.sh.Npad, dh = a.sh.dh, D = a.sh.D;
   const T* kbase = reinterpret_cast<const T*>(a.caches.p[v] + a.cl.k + (size_t)a.layer * a.cl.kv_layer) +
                    (size_t)h * Npad * dh;
@@ -128,136 +130,169 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
                    (size_t)h * dh * Npad;
   const T* Q = static_cast<const T*>(a.q);
 
+  // the stream's row offsets: scalar loads, issued first, waited for last
+  const int off_v = a.meta->off[v], off_next = a.meta->off[v + 1];
   const int nkb = (N + 31) / 32;
-  int kb0 = 0, kb1 = nkb;
-  if (a.split == 4) {
-    kb0 = w * nkb / 4;
-    kb1 = (w + 1) * nkb / 4;
-  }
-  if (!active) kb1 = kb0;
-
-  // one batch: Q, and K/V of the first key block
-  const int qrow = q0 + n;
-  const bool qok = active && qrow < kv;
-  const int qr = min(max(rowbase + min(qrow, kv - 1), 0), a.qmax);
-  V8<T> qop[NDC];
+  const int kb0 = w * nkb / KW, kb1 = (w + 1) * nkb / KW;  // this wave's key blocks
+  V8<T> kop[GB][2][NDC], vop[GB][NDT];
+  auto load_group = [&](int kb) {
 #pragma unroll
-  for (int c = 0; c < NDC; ++c) {
-    const int dd = 32 * c + 8 * g;
-    qop[c].load(Q + (size_t)qr * D + h * dh + (dd < dh ? dd : 0));
-    if (!qok || dd >= dh) qop[c].zero();
-  }
-  V8<T> kop[2][NDC], vop[NDT];
-  load_kblock<T, NDC>(kop, kbase, min(kb0, nkb - 1), N, dh, g, n);
-  load_vblock<T, NDT>(vop, vbase, min(kb0, nkb - 1), N, dh, Npad, g, n);
-
-  float m_run = -INFINITY, l_run = 0.0f;
-  f32x4_t o[NDT];
-#pragma unroll
-  for (int t = 0; t < NDT; ++t) o[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-
-  for (int kb = kb0; kb < kb1; ++kb) {
-    V8<T> kn[2][NDC], vn[NDT];
-    // next block in flight while this one computes (past the end: a repeat)
-    load_kblock<T, NDC>(kn, kbase, min(kb + 1, nkb - 1), N, dh, g, n);
-    load_vblock<T, NDT>(vn, vbase, min(kb + 1, nkb - 1), N, dh, Npad, g, n);
-    const int kbase0 = kb * 32;
-    f32x4_t st[2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      st[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-      for (int c = 0; c < NDC; ++c) mma(st[t], kop[t][c], qop[c]);
+    for (int b = 0; b < GB; ++b) {
+      const int k = min(kb + b, nkb - 1);
+      load_kblock<T, NDC>(kop[b], kbase, k, N, dh, g, n);
+      load_vblock<T, NDT>(vop[b], vbase, k, N, dh, Npad, g, n);
     }
-    // st[t][i] = score of key kbase0 + 16t + 4g + i for query n
-    float s[8];
-    float mloc = -INFINITY;
+  };
+  load_group(kb0);
+
+  const int q0 = blockIdx.x * QT * 16;
+  // Q fragments: dims past d_h read in-bounds data of the same row and are
+  // not zeroed, because the K fragments are zero there (no select on Q, so no
+  // wait right after its loads)
+  V8<T> qop[QT][NDC];
+  auto load_q = [&](int rowbase, int kv) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int qt = 0; qt < QT; ++qt) {
+      const int qr = min(rowbase + min(q0 + 16 * qt + n, max(kv - 1, 0)), a.qmax);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kbase0 + 16 * t + 4 * g + i;
-        const float x = key < N ? st[t][i] * a.scale_log2 : -INFINITY;
-        s[4 * t + i] = x;
-        mloc = fmaxf(mloc, x);
+      for (int c = 0; c < NDC; ++c) {
+        const int dd = 32 * c + 8 * g;
+        qop[qt][c].load(Q + (size_t)qr * D + h * dh + (dd < dh ? dd : 0));
       }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    const bool none = (m_new == -INFINITY);
-    const float alpha = none ? 1.0f : exp2f(m_run - m_new);
-    float p[8], psum = 0.0f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      p[j] = none ? 0.0f : exp2f(s[j] - m_new);
-      psum += p[j];
     }
-    l_run = l_run * alpha + psum;
-    V8<T> pop;
-    pack_p(pop, p);
+  };
+  // the first stream's rows start at 0: its queries are loaded before the
+  // offsets arrive (rows past the stream's count are clamped and never stored)
+  if (v == 0) load_q(0, a.qmax + 1);
+  const int rowbase = off_v;
+  const int kv = off_next - off_v;
+  if (q0 >= kv) return;  // uniform per workgroup
+  if (v != 0) load_q(rowbase, kv);
+
+  float m_run[QT], l_run[QT];
+  f32x4_t o[QT][NDT];
 #pragma unroll
-    for (int t = 0; t < NDT; ++t) {
-      o[t] *= alpha;
-      mma(o[t], vop[t], pop);
-    }
-    m_run = m_new;
+  for (int qt = 0; qt < QT; ++qt) {
+    m_run[qt] = -INFINITY;
+    l_run[qt] = 0.0f;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int c = 0; c < NDC; ++c) kop[t][c] = kn[t][c];
-#pragma unroll
-    for (int t = 0; t < NDT; ++t) vop[t] = vn[t];
+    for (int t = 0; t < NDT; ++t) o[qt][t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
   }
 
-  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-  l_tot = l_tot + __shfl_xor(l_tot, 32, 64);
-
-  if (a.split == 4) {
-    if (g == 0) {
-      s_m[w][n] = m_run;
-      s_l[w][n] = l_tot;
-    }
+  for (int kb = kb0; kb < kb1; kb += GB) {
+    if (kb > kb0) load_group(kb);
 #pragma unroll
-    for (int t = 0; t < NDT; ++t) s_o[w][t][lane] = o[t];
+    for (int b = 0; b < GB; ++b) {
+      if (kb + b < kb1) {  // uniform
+        const int key0 = (kb + b) * 32;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          f32x4_t st[2];
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            st[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int c = 0; c < NDC; ++c) mma(st[t], kop[b][t][c], qop[qt][c]);
+          }
+          // st[t][i] = score of key key0 + 16t + 4g + i for query n of tile qt
+          float sc[8];
+          float mloc = -INFINITY;
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int key = key0 + 16 * t + 4 * g + i;
+              const float x = key < N ? st[t][i] * a.scale_log2 : -INFINITY;
+              sc[4 * t + i] = x;
+              mloc = fmaxf(mloc, x);
+            }
+          mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+          mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+          const float m_new = fmaxf(m_run[qt], mloc);
+          const bool none = (m_new == -INFINITY);
+          const float alpha = none ? 1.0f : exp2f(m_run[qt] - m_new);
+          float p[8], psum = 0.0f;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            p[j] = none ? 0.0f : exp2f(sc[j] - m_new);
+            psum += p[j];
+          }
+          l_run[qt] = l_run[qt] * alpha + psum;
+          V8<T> pop;
+          pack_p(pop, p);
+#pragma unroll
+          for (int t = 0; t < NDT; ++t) {
+            o[qt][t] *= alpha;
+            mma(o[qt][t], vop[b][t], pop);
+          }
+          m_run[qt] = m_new;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    l_run[qt] += __shfl_xor(l_run[qt], 16, 64);
+    l_run[qt] += __shfl_xor(l_run[qt], 32, 64);
+  }
+
+  // merge: waves 2,3 into 0,1, then wave 1 into 0
+#pragma unroll
+  for (int half = 2; half >= 1; half >>= 1) {
+    if (w >= half && w < 2 * half) {
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        if (g == 0) {
+          s_m[w - half][qt][n] = m_run[qt];
+          s_l[w - half][qt][n] = l_run[qt];
+        }
+#pragma unroll
+        for (int t = 0; t < NDT; ++t) s_o[w - half][qt][t][lane] = o[qt][t];
+      }
+    }
     __syncthreads();
-    if (w != 0) return;
-    float mm = -INFINITY;
+    if (w < half) {
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) mm = fmaxf(mm, s_m[ww][n]);
-    float f[4];
-    l_tot = 0.0f;
+      for (int qt = 0; qt < QT; ++qt) {
+        const float mo = s_m[w][qt][n], lo = s_l[w][qt][n];
+        const float mm = fmaxf(m_run[qt], mo);
+        const float fa = m_run[qt] == -INFINITY ? 0.0f : exp2f(m_run[qt] - mm);
+        const float fb = mo == -INFINITY ? 0.0f : exp2f(mo - mm);
+        l_run[qt] = fa * l_run[qt] + fb * lo;
+        m_run[qt] = mm;
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) {
-      f[ww] = s_m[ww][n] == -INFINITY ? 0.0f : exp2f(s_m[ww][n] - mm);
-      l_tot += f[ww] * s_l[ww][n];
+        for (int t = 0; t < NDT; ++t) o[qt][t] = o[qt][t] * fa + s_o[w][qt][t][lane] * fb;
+      }
     }
-#pragma unroll
-    for (int t = 0; t < NDT; ++t) {
-      f32x4_t acc = s_o[0][t][lane] * f[0];
-#pragma unroll
-      for (int ww = 1; ww < 4; ++ww) acc += s_o[ww][t][lane] * f[ww];
-      o[t] = acc;
-    }
+    __syncthreads();
   }
+  if (w != 0) return;
 
-  if (!active || qrow >= kv) return;
-  const float inv = 1.0f / l_tot;
-  T* out = static_cast<T*>(a.o) + (size_t)(rowbase + qrow) * D + h * dh;
 #pragma unroll
-  for (int t = 0; t < NDT; ++t) {
-    const int d0 = 16 * t + 4 * g;
-    if (d0 < dh) {
-      float r[4];
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qrow = q0 + 16 * qt + n;
+    if (qrow < kv) {
+      const float inv = 1.0f / l_run[qt];
+      T* out = static_cast<T*>(a.o) + (size_t)(rowbase + qrow) * D + h * dh;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = o[t][i] * inv;
-      store4<T>(out + d0, r);
+      for (int t = 0; t < NDT; ++t) {
+        const int d0 = 16 * t + 4 * g;
+        if (d0 < dh) {
+          float r[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) r[i] = o[qt][t][i] * inv;
+          store4<T>(out + d0, r);
+        }
+      }
     }
   }
 }
 
 template <class T, int NDC, int NDT>
 static void launch_t(const AttnArgs& a, dim3 grid, hipStream_t s) {
-  (void)launch_k((attn_kernel<T, NDC, NDT>), grid, dim3(256), 0, s, a);
+  // two key blocks in flight per wave where the registers allow
+  if constexpr (NDT <= 6) (void)launch_k((attn_kernel<T, NDC, NDT, 2>), grid, dim3(256), 0, s, a);
+  else (void)launch_k((attn_kernel<T, NDC, NDT, 1>), grid, dim3(256), 0, s, a);
 }
 
 template <class T>
@@ -270,8 +305,7 @@ static void launch_dh(const AttnArgs& a, dim3 grid, hipStream_t s) {
 }
 
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s) {
-  const int qtiles = (max_rows_per_view + 15) / 16;
-  dim3 grid(a.split == 4 ? qtiles : (qtiles + 3) / 4, a.sh.H, a.B);
+  dim3 grid((max_rows_per_view + 31) / 32, a.sh.H, a.B);
   if (grid.x == 0) return hipSuccess;
   if (a.sh.dtype) launch_dh<uint16_t>(a, grid, s);
   else launch_dh<float>(a, grid, s);

@@ -13,10 +13,32 @@
 
 namespace incvit {
 
+// 16 consecutive bytes of weights and their values as floats
+__device__ __forceinline__ void load16(V8<uint16_t>& v, const uint16_t* p) { v.load(p); }
+__device__ __forceinline__ void load16(V8<float>& v, const float* p) {
+  v.a = __builtin_bit_cast(float4, *(const INCVIT_GLOBAL f32x4_t*)p);
+}
+__device__ __forceinline__ void unpack16(float* f, const V8<uint16_t>& v) {
+  const uint32_t q[4] = {v.v.x, v.v.y, v.v.z, v.v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f[2 * e] = __uint_as_float(q[e] << 16);
+    f[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void unpack16(float* f, const V8<float>& v) {
+  f[0] = v.a.x; f[1] = v.a.y; f[2] = v.a.z; f[3] = v.a.w;
+}
+
 // Workgroup: 16 tokens x 64 columns; wave w computes tokens 4w..4w+3 of the
-// tile, lane = column.  k is staged through LDS in tiles of 64; the next
-// tile's global loads are issued before the current tile is computed.
+// tile, lane = column.  k is staged through LDS in tiles of 64.  Every global
+// load is unconditional (clamped addresses; values past P are loaded but never
+// used because the k loop stops at P) and issued two tiles ahead, so a tile's
+// data arrives while the two before it are computed.
+template <class T>
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
+  constexpr int WV = 16 / sizeof(T);  // weights per 16-byte load
+  constexpr int WL = 64 * 64 / (256 * WV);  // weight loads per thread per tile
   __shared__ __align__(16) float sx[64][16];  // [k][token]
   __shared__ __align__(16) float sw[64][64];  // [k][column]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -33,48 +55,61 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 
   const int d = c0 + lane;
   const float* xp = a.patches + (size_t)v * N * P;
-  // this thread's share of a tile: 4 patch values and 16 weights
-  float rx[4], rw[16];
-  auto fetch = [&](int kt) {
+  const T* wp = static_cast<const T*>(a.w_pe);
+  // this thread's share of a tile: 4 patch values (token e/64, k e%64) and WL
+  // 16-byte runs of weights (row k, WV consecutive columns)
+  struct Tile {
+    float x[4];
+    V8<T> wv[WL > 0 ? WL : 1];
+  };
+  auto fetch = [&](Tile& t, int kt) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int e = tid + 256 * j, t = e >> 6, k = kt + (e & 63), tok = tok0 + t;
-      rx[j] = (tok < N && k < P) ? xp[(size_t)tok * P + k] : 0.0f;
+      const int e = tid + 256 * j;
+      const int tok = min(tok0 + (e >> 6), N - 1), k = min(kt + (e & 63), P - 1);
+      t.x[j] = xp[(size_t)tok * P + k];
     }
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int e = tid + 256 * j, k = kt + (e >> 6), col = c0 + (e & 63);
-      float wv = 0.0f;
-      if (k < P && col < D) {
-        const size_t i = (size_t)k * D + col;
-        wv = a.dtype ? bf2f(static_cast<const uint16_t*>(a.w_pe)[i]) : static_cast<const float*>(a.w_pe)[i];
-      }
-      rw[j] = wv;
+    for (int j = 0; j < WL; ++j) {
+      const int e = tid + 256 * j;                 // run index in the tile
+      const int k = min(kt + e / (64 / WV), P - 1);
+      const int col = min(c0 + (e % (64 / WV)) * WV, D - WV);
+      load16(t.wv[j], wp + (size_t)k * D + col);
     }
   };
+  auto stage = [&](const Tile& t) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j;
+      sx[e & 63][e >> 6] = t.x[j];
+    }
+#pragma unroll
+    for (int j = 0; j < WL; ++j) {
+      const int e = tid + 256 * j;
+      float f[WV];
+      unpack16(f, t.wv[j]);
+#pragma unroll
+      for (int q = 0; q < WV; ++q) sw[e / (64 / WV)][(e % (64 / WV)) * WV + q] = f[q];
+    }
+  };
+
   float acc[4];
-  const float bias = d < D ? a.b_pe[d] : 0.0f;
+  const float bias = a.b_pe[min(d, D - 1)];
   float posv[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     acc[r] = bias;
-    const int tok = tok0 + 4 * w + r;
-    posv[r] = (tok < N && d < D) ? a.pos[(size_t)tok * D + d] : 0.0f;
+    const int tok = min(tok0 + 4 * w + r, N - 1);
+    posv[r] = a.pos[(size_t)tok * D + min(d, D - 1)];
   }
-  fetch(0);
+  Tile t0, t1;
+  fetch(t0, 0);
+  fetch(t1, 64);
   for (int kt = 0; kt < P; kt += 64) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = tid + 256 * j;
-      sx[e & 63][e >> 6] = rx[j];
-    }
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int e = tid + 256 * j;
-      sw[e >> 6][e & 63] = rw[j];
-    }
+    stage(t0);
     __syncthreads();
-    if (kt + 64 < P) fetch(kt + 64);  // in flight while this tile computes
+    t0 = t1;
+    fetch(t1, kt + 128);  // two tiles ahead (clamped past the end)
     const int kmax = min(64, P - kt);
 #pragma unroll 8
     for (int kk = 0; kk < kmax; ++kk) {
@@ -135,8 +170,8 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
-  (void)launch_k(embed_kernel, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  if (a.dtype) return launch_k(embed_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  return launch_k(embed_kernel<float>, grid, dim3(256), 0, s, a);
 }
 
 hipError_t launch_sim(const SimArgs& a, hipStream_t s) {
