@@ -1,6 +1,6 @@
 // Row kernels that finish the split-K projections of a layer (paper §III-B:
 // the residual additions around the attention output and the MLP, and the
-// LayerNorm that opens the next sublayer), one wave per compact row:
+// LayerNorm that opens the next sublayer), one workgroup per compact row:
 //
 //   RES_LN2: H  = Z_l + ((P_0 + P_1 + ...) + b_o)          (fp32)
 //            A2 = S(LN2(H))                                 (input of fc1)
@@ -11,8 +11,8 @@
 //
 // The partial sums are added in split order, then the bias, then the residual,
 // which is the order the unsplit product would use.  LayerNorm: two passes
-// (mean, then mean squared deviation) over the row in fp32, lane partials
-// summed in index order and combined across lanes by a fixed butterfly.
+// (mean, then mean squared deviation) over the row in fp32, thread partials
+// summed in index order and combined across the workgroup in a fixed order.
 // Every load is issued before M is known (the compact buffers are padded past
 // every launched row); rows at or past M return before storing anything.
 #include "common.hpp"
@@ -47,18 +47,34 @@ __device__ __forceinline__ float4 add4(float4 a, float4 b) { return make_float4(
 
 }  // namespace
 
-// KP: float4 slots per lane (D <= 256 * KP); S: K splits.
+// Sum over the 4 waves of a 256-thread workgroup in a fixed order (lanes by
+// butterfly, then waves 0..3); every thread gets the total.
+__device__ __forceinline__ float block_sum4(float x, float* s) {
+  x = wave_sum(x);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) s[w] = x;
+  __syncthreads();
+  const float t = (s[0] + s[1]) + (s[2] + s[3]);
+  __syncthreads();
+  return t;
+}
+
+// One 256-thread workgroup per compact row r; thread t owns the float4 slots
+// q = t + 256 j, j < KP (D <= 1024 * KP).  S: K splits.
 template <class T, int MODE, int S, int KP>
 __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
-  const int lane = threadIdx.x & 63, r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  __shared__ float s_red[4];
+  const int tid = threadIdx.x, r = blockIdx.x;
   const int M = a.meta->m;
+  // the first 32 rows load before M is known; later rows (rarely used) check first
+  if (r >= 32 && r >= M) return;
   const int D = a.sh.D, D4 = D / 4;
   const RowInfo ri = a.rows[r];
 
   float4 p[S][KP], res[KP], bias[KP], gam[KP], bet[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
-    const int q = min(lane + 64 * j, D4 - 1);
+    const int q = min(tid + 256 * j, D4 - 1);
 #pragma unroll
     for (int s = 0; s < S; ++s) p[s][j] = ld4(a.part + ((size_t)s * a.mpad + r) * D, q);
     if constexpr (MODE == RES_LN2)
@@ -69,9 +85,9 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     gam[j] = ld4(a.ln_g, q);
     bet[j] = ld4(a.ln_b, q);
   }
-  if (r >= M) return;
+  if (r >= M) return;  // uniform per workgroup
 
-  // the new rows (H, or the rounded Z'), and their sum over the row
+  // the new row (H, or the rounded Z'), and its LayerNorm statistics
   float4 v[KP];
   float sum = 0.0f;
 #pragma unroll
@@ -82,18 +98,18 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     x = add4(x, bias[j]);
     v[j] = add4(res[j], x);
     if constexpr (MODE == RES_LN1) v[j] = rnd4(v[j], static_cast<T*>(nullptr));
-    if (lane + 64 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+    if (tid + 256 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
   }
-  const float mean = wave_sum(sum) / (float)D;
+  const float mean = block_sum4(sum, s_red) / (float)D;
   float sq = 0.0f;
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
-    if (lane + 64 * j < D4) {
+    if (tid + 256 * j < D4) {
       const float dx = v[j].x - mean, dy = v[j].y - mean, dz = v[j].z - mean, dw = v[j].w - mean;
       sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
     }
   }
-  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + a.sh.eps);
+  const float rstd = 1.0f / sqrtf(block_sum4(sq, s_red) / (float)D + a.sh.eps);
 
   T* xrow = nullptr;
   T* yrow = nullptr;
@@ -108,7 +124,7 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
   }
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
-    const int q = lane + 64 * j;
+    const int q = tid + 256 * j;
     if (q < D4) {
       const float4 n4 = make_float4((v[j].x - mean) * rstd * gam[j].x + bet[j].x,
                                     (v[j].y - mean) * rstd * gam[j].y + bet[j].y,
@@ -135,10 +151,8 @@ namespace {
 
 template <class T, int MODE, int S>
 hipError_t launch_s(const ResArgs& a, dim3 grid, hipStream_t s) {
-  const int kp = (a.sh.D + 255) / 256;
-  if (kp <= 2) return launch_k(res_kernel<T, MODE, S, 2>, grid, dim3(256), 0, s, a);
-  if (kp <= 5) return launch_k(res_kernel<T, MODE, S, 5>, grid, dim3(256), 0, s, a);
-  return launch_k(res_kernel<T, MODE, S, 8>, grid, dim3(256), 0, s, a);
+  if (a.sh.D <= 1024) return launch_k(res_kernel<T, MODE, S, 1>, grid, dim3(256), 0, s, a);
+  return launch_k(res_kernel<T, MODE, S, 2>, grid, dim3(256), 0, s, a);
 }
 
 template <class T, int MODE>
@@ -155,7 +169,7 @@ hipError_t launch_mode(const ResArgs& a, dim3 grid, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_res(int mode, const ResArgs& a, int mmax, hipStream_t s) {
-  const dim3 grid(max(1, (mmax + 3) / 4));
+  const dim3 grid(max(1, mmax));
   if (a.sh.dtype)
     return mode == RES_LN2 ? launch_mode<uint16_t, RES_LN2>(a, grid, s) : launch_mode<uint16_t, RES_LN1>(a, grid, s);
   return mode == RES_LN2 ? launch_mode<float, RES_LN2>(a, grid, s) : launch_mode<float, RES_LN1>(a, grid, s);

@@ -182,15 +182,32 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   if (tid == 0) a.count[v] = total_sel;
 }
 
-// One wave per compact row: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]),
-// and the row's entry in the row map with its LayerNorm statistics.  Block 0
-// also publishes M and the per-stream row offsets.
-template <class T>
+// 4 consecutive elements (already representable in T) to storage
+__device__ __forceinline__ void store4v(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void store4v(uint16_t* p, float4 v) {
+  *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
+                                            (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+}
+
+// One workgroup per compact row r: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]),
+// the compact Z0 row and the layer-0 QKV input S(LN1(Z0)), and the row's entry
+// in the row map.  Block 0 also publishes M and the per-stream row offsets.
+// Thread t owns float4 slots t + 256 j of the row (D <= 1024 * KP).
+template <class T, int KP>
 __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   __shared__ int s_cnt[kMaxViews];
   __shared__ int s_off[kMaxViews + 1];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int B = a.rm.B, N = a.rm.N, D = a.sh.D;
+  __shared__ float s_red[4];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int B = a.rm.B, N = a.rm.N, D = a.sh.D, D4 = D / 4;
+  // LN1 parameters do not depend on the row: in flight from the start
+  float4 gv[KP], bv[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = min(tid + 256 * j, D4 - 1);
+    gv[j] = reinterpret_cast<const float4*>(a.g)[q];
+    bv[j] = reinterpret_cast<const float4*>(a.b)[q];
+  }
   if (tid < B) s_cnt[tid] = a.rm.count[tid];
   __syncthreads();
   if (tid == 0) {
@@ -214,48 +231,58 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
       hdr->frames = 0;
     }
   }
-  const int r = blockIdx.x * 4 + (tid >> 6);
-  if (r >= M) return;
+  const int r = blockIdx.x;
+  if (r >= M) return;  // uniform per workgroup
   int v = 0;
   while (v + 1 < B && s_off[v + 1] <= r) ++v;
   const int tok = a.rm.idx[v * N + (r - s_off[v])];
   char* cache = a.caches.p[v];
-  const float* src = a.t0 + ((size_t)v * N + tok) * D;
-  constexpr int kPer = kMaxDim / 64;
-  float t[kPer];
+  const float4* src = reinterpret_cast<const float4*>(a.t0 + ((size_t)v * N + tok) * D);
+  float4 t[KP], zr[KP];
+  float sum = 0.0f;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) t[j] = (lane + 64 * j < D) ? src[lane + 64 * j] : 0.0f;
-  float* ref = reinterpret_cast<float*>(cache + a.cl.ref) + (size_t)tok * D;
+  for (int j = 0; j < KP; ++j) {
+    t[j] = src[min(tid + 256 * j, D4 - 1)];
+    zr[j] = make_float4(Elem<T>::rnd(t[j].x), Elem<T>::rnd(t[j].y), Elem<T>::rnd(t[j].z), Elem<T>::rnd(t[j].w));
+    if (tid + 256 * j < D4) sum += (zr[j].x + zr[j].y) + (zr[j].z + zr[j].w);
+  }
+  // two-pass LayerNorm over the row, fixed reduction order
+  float tot = wave_sum(sum);
+  if (lane == 0) s_red[w] = tot;
+  __syncthreads();
+  const float mean = ((s_red[0] + s_red[1]) + (s_red[2] + s_red[3])) / (float)D;
+  __syncthreads();
+  float sq = 0.0f;
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    if (tid + 256 * j < D4) {
+      const float dx = zr[j].x - mean, dy = zr[j].y - mean, dz = zr[j].z - mean, dw = zr[j].w - mean;
+      sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
+    }
+  }
+  tot = wave_sum(sq);
+  if (lane == 0) s_red[w] = tot;
+  __syncthreads();
+  const float rstd = 1.0f / sqrtf(((s_red[0] + s_red[1]) + (s_red[2] + s_red[3])) / (float)D + a.sh.eps);
+
+  float4* ref = reinterpret_cast<float4*>(cache + a.cl.ref + (size_t)tok * D * 4);
   T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
   T* z0 = static_cast<T*>(a.z) + (size_t)r * D;
   T* a0 = static_cast<T*>(a.a) + (size_t)r * D;
-  // Z_0 = S(T0) and the layer-0 QKV input S(LN1(Z_0)), LayerNorm in two passes
-  float zr[kPer], sum = 0.0f;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    zr[j] = Elem<T>::rnd(t[j]);
-    if (lane + 64 * j < D) sum += zr[j];
-  }
-  const float mean = wave_sum(sum) / (float)D;
-  float sq = 0.0f;
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const float dv = zr[j] - mean;
-    if (lane + 64 * j < D) sq += dv * dv;
-  }
-  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + a.sh.eps);
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int d = lane + 64 * j;
-    if (d < D) {
-      const T o = Elem<T>::cv(t[j]);
-      ref[d] = t[j];
-      x0[d] = o;
-      z0[d] = o;
-      a0[d] = Elem<T>::cv((zr[j] - mean) * rstd * a.g[d] + a.b[d]);
+  for (int j = 0; j < KP; ++j) {
+    const int q = tid + 256 * j;
+    if (q < D4) {
+      ref[q] = t[j];
+      store4v(x0 + 4 * q, zr[j]);
+      store4v(z0 + 4 * q, zr[j]);
+      store4v(a0 + 4 * q, make_float4((zr[j].x - mean) * rstd * gv[j].x + bv[j].x,
+                                      (zr[j].y - mean) * rstd * gv[j].y + bv[j].y,
+                                      (zr[j].z - mean) * rstd * gv[j].z + bv[j].z,
+                                      (zr[j].w - mean) * rstd * gv[j].w + bv[j].w));
     }
   }
-  if (lane == 0) a.rows[r] = RowInfo{cache, tok, v};
+  if (tid == 0) a.rows[r] = RowInfo{cache, tok, v};
 }
 
 hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
@@ -264,10 +291,13 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s) {
-  dim3 grid(max(1, (mmax + 3) / 4));
-  if (a.sh.dtype) (void)launch_k(commit_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  else (void)launch_k(commit_kernel<float>, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  const dim3 grid(max(1, mmax));
+  const bool wide = a.sh.D > 1024;
+  if (a.sh.dtype)
+    return wide ? launch_k(commit_kernel<uint16_t, 2>, grid, dim3(256), 0, s, a)
+                : launch_k(commit_kernel<uint16_t, 1>, grid, dim3(256), 0, s, a);
+  return wide ? launch_k(commit_kernel<float, 2>, grid, dim3(256), 0, s, a)
+              : launch_k(commit_kernel<float, 1>, grid, dim3(256), 0, s, a);
 }
 
 
