@@ -28,6 +28,7 @@ inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
 struct Shape {
   int N, P, D, L, H, dh, F, Fpad, Npad;
+  int ndc;    // 32-wide chunks per head dim: ceil(d_h / 32)
   int dtype;  // 0 = fp32, 1 = bf16
   int eb;     // element bytes of the storage dtype
   float eps;
@@ -349,6 +350,27 @@ __device__ __forceinline__ float wave_max(float x) {
 template <class T>
 __device__ __forceinline__ T* x_row(char* cache, const CacheLayout& cl, const Shape& sh, int layer, int tok) {
   return reinterpret_cast<T*>(cache + cl.x + (size_t)layer * cl.x_layer) + (size_t)tok * sh.D;
+}
+
+// Cached K and V of one layer are stored as the attention's MFMA operands, so
+// that each operand load is one contiguous kilobyte.  Per head, per block of
+// 32 keys (kb), head dims padded to 32 * ndc:
+//   K: [kb][tile t (2)][dim chunk c (ndc)][lane (64)][8]; lane 16g + n of
+//      tile t holds key 8(n/4) + 4t + n%4 of the block, dims 32c + 8g .. +7.
+//      The key order makes the score tile give each lane 8 consecutive keys.
+//   V: [kb][dim tile (2 ndc)][lane (64)][8]; lane 16g + n holds dim 16 tile + n,
+//      keys 8g .. 8g + 7 of the block (the transposed operand).
+// Entries for padded dims or keys past N are never written; readers mask them.
+__host__ __device__ __forceinline__ size_t k_elem(const Shape& sh, int h, int tok, int d) {
+  const int kb = tok >> 5, r = tok & 31;
+  const int t = (r & 7) >> 2, n = 4 * (r >> 3) + (r & 3);
+  const int c = d >> 5, g = (d >> 3) & 3, j = d & 7;
+  return (((((size_t)h * (sh.Npad >> 5) + kb) * 2 + t) * sh.ndc + c) * 64 + (16 * g + n)) * 8 + j;
+}
+__host__ __device__ __forceinline__ size_t v_elem(const Shape& sh, int h, int tok, int d) {
+  const int kb = tok >> 5, r = tok & 31;
+  const int g = r >> 3, j = r & 7, dt = d >> 4, n = d & 15;
+  return ((((size_t)h * (sh.Npad >> 5) + kb) * (2 * sh.ndc) + dt) * 64 + (16 * g + n)) * 8 + j;
 }
 
 }  // namespace incvit

@@ -151,8 +151,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void gemm_kernel(GemmArgs a) {
           } else {
             const int hh = c / a.sh.dh, d = c - hh * a.sh.dh;
             char* base = rinfo.cache + (which == 1 ? a.cl.k : a.cl.v) + (size_t)a.layer * a.cl.kv_layer;
-            const size_t e = which == 1 ? ((size_t)hh * a.sh.Npad + rinfo.tok) * a.sh.dh + d
-                                        : ((size_t)hh * a.sh.dh + d) * a.sh.Npad + rinfo.tok;
+            const size_t e = which == 1 ? k_elem(a.sh, hh, rinfo.tok, d) : v_elem(a.sh, hh, rinfo.tok, d);
             gbl(reinterpret_cast<T*>(base))[e] = o;
           }
         }

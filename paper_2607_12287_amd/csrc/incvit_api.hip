@@ -64,6 +64,7 @@ bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::strin
   sh.F = c->mlp_dim;
   sh.Fpad = round_up(c->mlp_dim, 32);
   sh.Npad = round_up(sh.N, 32);
+  sh.ndc = (sh.dh + 31) / 32;
   sh.dtype = c->dtype;
   sh.eb = c->dtype == INCVIT_BF16 ? 2 : 4;
   sh.eps = c->ln_eps;
@@ -146,7 +147,7 @@ CacheLayout cache_layout(const Shape& sh) {
   size_t off = kAlign;  // header
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
   cl.x_layer = (size_t)sh.N * sh.D * sh.eb;
-  cl.kv_layer = (size_t)sh.H * sh.Npad * sh.dh * sh.eb;
+  cl.kv_layer = (size_t)sh.H * (sh.Npad / 32) * sh.ndc * 1024 * sh.eb;  // see k_elem / v_elem
   cl.ref = take((size_t)sh.N * sh.D * 4);
   cl.x = take(cl.x_layer * (sh.L + 1));
   cl.k = take(cl.kv_layer * sh.L);

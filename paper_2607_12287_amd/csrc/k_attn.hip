@@ -5,47 +5,12 @@
 // Per block of 32 keys and tile of 16 queries a wave forms S^T = K Q^T with
 // MFMA (so each lane keeps a single query and its softmax state), updates the
 // online softmax in fp32 (exp2 with the 1/sqrt(d_h) scale folded in), and
-// accumulates O^T = V^T P^T with MFMA.  V is cached transposed per head
-// ([d_h][Npad]) so that the P^T operand needs no lane exchange.
+// accumulates O^T = V^T P^T with MFMA.  K and V are cached in operand order
+// (transposed V), with a key order that makes the P^T operand need no lane
+// exchange.
 #include "common.hpp"
 
 namespace incvit {
-
-template <class T> struct Half4;
-template <> struct Half4<uint16_t> {  // 4 bf16 = 8 bytes
-  __device__ static uint2 load(const uint16_t* p, int valid) {
-    uint2 r = *reinterpret_cast<const uint2*>(p);
-    if (valid < 4) {
-      if (valid <= 3) r.y &= 0x0000ffffu;
-      if (valid <= 2) r.y = 0;
-      if (valid <= 1) r.x &= 0x0000ffffu;
-      if (valid <= 0) r.x = 0;
-    }
-    return r;
-  }
-};
-
-template <class T>
-__device__ __forceinline__ void load_v(V8<T>& out, const T* row, int k0, int N);
-
-template <>
-__device__ __forceinline__ void load_v<uint16_t>(V8<uint16_t>& out, const uint16_t* row, int k0, int N) {
-  // slots 0..3: keys k0..k0+3, slots 4..7: keys k0+16..k0+19
-  const uint2 lo = Half4<uint16_t>::load(row + k0, N - k0);
-  const uint2 hi = Half4<uint16_t>::load(row + k0 + 16, N - k0 - 16);
-  out.v = make_uint4(lo.x, lo.y, hi.x, hi.y);
-}
-
-template <>
-__device__ __forceinline__ void load_v<float>(V8<float>& out, const float* row, int k0, int N) {
-  float4 lo = *reinterpret_cast<const float4*>(row + k0);
-  float4 hi = *reinterpret_cast<const float4*>(row + k0 + 16);
-  const int a = N - k0, b = N - k0 - 16;
-  if (a < 4) { if (a <= 3) lo.w = 0; if (a <= 2) lo.z = 0; if (a <= 1) lo.y = 0; if (a <= 0) lo.x = 0; }
-  if (b < 4) { if (b <= 3) hi.w = 0; if (b <= 2) hi.z = 0; if (b <= 1) hi.y = 0; if (b <= 0) hi.x = 0; }
-  out.a = lo;
-  out.b = hi;
-}
 
 __device__ __forceinline__ void pack_p(V8<uint16_t>& out, const float* p) {
   out.v = make_uint4((uint32_t)f2bf(p[0]) | ((uint32_t)f2bf(p[1]) << 16),
@@ -72,37 +37,48 @@ __device__ __forceinline__ void store4<float>(float* dst, const float* v) {
 
 constexpr int kMaxDT = kMaxHeadDim / 16;  // 16-wide d tiles
 
-// Loads below are unconditional with clamped addresses (out-of-range values
-// are zeroed by selects afterwards), so the wait before each MFMA covers only
-// the loads it needs.
-
-// K operands of one 32-key block: tile t holds keys kb*32 + 16t + (lane%16).
+// K/V operands of one 32-key block come straight from the cache, which stores
+// them in operand order (k_elem / v_elem): every load is one contiguous
+// kilobyte.  Dims past d_h are zeroed in the K operand (the matching Q values
+// are in-bounds data of the same row); keys past N are masked in the scores
+// and zeroed in the V operand (their cache entries are never written).
 template <class T, int NDC>
-__device__ __forceinline__ void load_kblock(V8<T> (&kop)[2][NDC], const T* kbase, int kb, int N, int dh,
-                                            int g, int n) {
+__device__ __forceinline__ void load_kblock(V8<T> (&kop)[2][NDC], const T* kbase, int kb, int dh, int g, int lane) {
+  const T* blk = kbase + (size_t)kb * 2 * NDC * kChunkElems + lane * 8;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int key = kb * 32 + 16 * t + n;
-    const int kc = min(key, N - 1);
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int c = 0; c < NDC; ++c) {
-      const int dd = 32 * c + 8 * g;
-      kop[t][c].load(kbase + (size_t)kc * dh + (dd < dh ? dd : 0));
-      if (key >= N || dd >= dh) kop[t][c].zero();
+      kop[t][c].load(blk + (t * NDC + c) * kChunkElems);
+      if (32 * c + 8 * g >= dh) kop[t][c].zero();
     }
-  }
 }
 
-// V^T operands of one 32-key block: d tile t, row d = 16t + (lane%16).
 template <class T, int NDT>
-__device__ __forceinline__ void load_vblock(V8<T> (&vop)[NDT], const T* vbase, int kb, int N, int dh, int Npad,
-                                            int g, int n) {
+__device__ __forceinline__ void load_vblock(V8<T> (&vop)[NDT], const T* vbase, int kb, int lane) {
+  const T* blk = vbase + (size_t)kb * NDT * kChunkElems + lane * 8;
 #pragma unroll
-  for (int t = 0; t < NDT; ++t) {
-    const int d = 16 * t + n;
-    load_v<T>(vop[t], vbase + (size_t)min(d, dh - 1) * Npad, kb * 32 + 4 * g, N);
-    if (d >= dh) vop[t].zero();
+  for (int t = 0; t < NDT; ++t) vop[t].load(blk + t * kChunkElems);
+}
+
+// zero the V operand entries of keys >= N (lane group g holds keys 8g..8g+7)
+__device__ __forceinline__ void mask_v(V8<uint16_t>& v, int first_key, int N) {
+  uint32_t q[4] = {v.v.x, v.v.y, v.v.z, v.v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int k0 = first_key + 2 * e;
+    if (k0 >= N) q[e] = 0;
+    else if (k0 + 1 >= N) q[e] &= 0x0000ffffu;
   }
+  v.v = make_uint4(q[0], q[1], q[2], q[3]);
+}
+__device__ __forceinline__ void mask_v(V8<float>& v, int first_key, int N) {
+  float f[8] = {v.a.x, v.a.y, v.a.z, v.a.w, v.b.x, v.b.y, v.b.z, v.b.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (first_key + e >= N) f[e] = 0.0f;
+  v.a = make_float4(f[0], f[1], f[2], f[3]);
+  v.b = make_float4(f[4], f[5], f[6], f[7]);
 }
 
 // One workgroup: QT query tiles (16 queries each) of one head of one stream;
@@ -123,24 +99,24 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, n = lane & 15;
   const int h = blockIdx.y, v = blockIdx.z;
-  const int N = a.sh.N, Npad = a.sh.Npad, dh = a.sh.dh, D = a.sh.D;
+  const int N = a.sh.N, dh = a.sh.dh, D = a.sh.D;
+  const int nkb = (N + 31) / 32;  // = Npad / 32
   const T* kbase = reinterpret_cast<const T*>(a.caches.p[v] + a.cl.k + (size_t)a.layer * a.cl.kv_layer) +
-                   (size_t)h * Npad * dh;
+                   (size_t)h * nkb * 2 * NDC * kChunkElems;
   const T* vbase = reinterpret_cast<const T*>(a.caches.p[v] + a.cl.v + (size_t)a.layer * a.cl.kv_layer) +
-                   (size_t)h * dh * Npad;
+                   (size_t)h * nkb * NDT * kChunkElems;
   const T* Q = static_cast<const T*>(a.q);
 
   // the stream's row offsets: scalar loads, issued first, waited for last
   const int off_v = a.meta->off[v], off_next = a.meta->off[v + 1];
-  const int nkb = (N + 31) / 32;
   const int kb0 = w * nkb / KW, kb1 = (w + 1) * nkb / KW;  // this wave's key blocks
   V8<T> kop[GB][2][NDC], vop[GB][NDT];
   auto load_group = [&](int kb) {
 #pragma unroll
     for (int b = 0; b < GB; ++b) {
       const int k = min(kb + b, nkb - 1);
-      load_kblock<T, NDC>(kop[b], kbase, k, N, dh, g, n);
-      load_vblock<T, NDT>(vop[b], vbase, k, N, dh, Npad, g, n);
+      load_kblock<T, NDC>(kop[b], kbase, k, dh, g, lane);
+      load_vblock<T, NDT>(vop[b], vbase, k, lane);
     }
   };
   load_group(kb0);
@@ -185,6 +161,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int b = 0; b < GB; ++b) {
       if (kb + b < kb1) {  // uniform
         const int key0 = (kb + b) * 32;
+        if (key0 + 32 > N) {  // the stream's last, partial block (uniform)
+#pragma unroll
+          for (int t = 0; t < NDT; ++t) mask_v(vop[b][t], key0 + 8 * g, N);
+        }
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
           f32x4_t st[2];
@@ -194,14 +174,16 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int c = 0; c < NDC; ++c) mma(st[t], kop[b][t][c], qop[qt][c]);
           }
-          // st[t][i] = score of key key0 + 16t + 4g + i for query n of tile qt
+          // st[t][i] = score of key key0 + 8g + 4t + i for query n of tile qt
+          // (the cache's key order within a block), so slot 4t + i of this
+          // lane is key 8g + 4t + i: the P operand order of the V product
           float sc[8];
           float mloc = -INFINITY;
 #pragma unroll
           for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-              const int key = key0 + 16 * t + 4 * g + i;
+              const int key = key0 + 8 * g + 4 * t + i;
               const float x = key < N ? st[t][i] * a.scale_log2 : -INFINITY;
               sc[4 * t + i] = x;
               mloc = fmaxf(mloc, x);

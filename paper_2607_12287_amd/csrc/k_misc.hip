@@ -32,7 +32,7 @@ __global__ void conv_kernel(ConvArgs a) {
 
 // Canonical layout of one cache: ref [N][D] f32 | X [L+1][N][D] | K [L][N][D]
 // | V [L][N][D] | Y [N][D] (storage dtype).  Device layout differs for K
-// ([L][H][Npad][dh]) and V ([L][H][dh][Npad]).
+// and V (attention operand order, k_elem / v_elem).
 template <class T>
 __global__ void export_kernel(ExportArgs a) {
   const Shape& sh = a.sh;
@@ -62,7 +62,7 @@ __global__ void export_kernel(ExportArgs a) {
       const int tok = (int)(rem / sh.D), c = (int)(rem % sh.D);
       const int hh = c / sh.dh, d = c % sh.dh;
       T* base = reinterpret_cast<T*>(cache + (isv ? a.cl.v : a.cl.k) + (size_t)l * a.cl.kv_layer);
-      dev = isv ? base + ((size_t)hh * sh.dh + d) * sh.Npad + tok : base + ((size_t)hh * sh.Npad + tok) * sh.dh + d;
+      dev = base + (isv ? v_elem(sh, hh, tok, d) : k_elem(sh, hh, tok, d));
     } else {
       dev = reinterpret_cast<T*>(cache + a.cl.y) + (f - n_x - 2 * n_kv);
     }
