@@ -29,7 +29,8 @@ METRIC = "incremental ViT frames/sec at 10% refresh (So400m shape); speedup vs f
 HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PROFILES = os.path.join(ROOT, "profiles")
-GEMM_KIND = {"0": "qkv", "1": "oproj", "2": "fc1", "3": "fc2"}
+GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "part"}  # epilogue template argument
+RES_KIND = {"0": "res_ln2", "1": "res_ln1"}
 
 
 def source_hash() -> str:
@@ -45,13 +46,30 @@ def source_hash() -> str:
 
 
 def kernel_kind(name: str):
-    """Kernel kind of a dispatch name in a rocprofv3 trace (None for other kernels)."""
+    """Kernel kind of a dispatch name in a rocprofv3 trace (None for other kernels;
+    "part" for the split-K GEMM, which is the output projection and the MLP down
+    projection in turn: see kinds_in_order)."""
     m = re.search(r"incvit::(\w+)_kernel(?:<([^>]*)>)?", name)
     if not m:
         return None
     if m.group(1) == "gemm":
         return GEMM_KIND.get(m.group(2).split(",")[1].strip())
+    if m.group(1) == "res":
+        return RES_KIND.get(m.group(2).split(",")[1].strip())
     return m.group(1)
+
+
+def kinds_in_order(names):
+    """Kinds of dispatches given in launch order; split-K GEMM dispatches
+    alternate between the output projection and the MLP down projection."""
+    out, part = [], 0
+    for n in names:
+        k = kernel_kind(n)
+        if k == "part":
+            k = "oproj" if part % 2 == 0 else "fc2"
+            part += 1
+        out.append(k)
+    return out
 
 
 def stored_traffic(workload: str, kind: str):
@@ -153,8 +171,7 @@ def summarize_trace(trace_dir: str, bench_log: str, plain_log: str, out: str, co
     plain = _bench_json(plain_log)
     rows = sorted(_csv_rows(trace_dir, "kernel_trace.csv"), key=lambda r: int(r["Dispatch_Id"]))
     by_kind = {}
-    for r in rows:
-        k = kernel_kind(r["Kernel_Name"])
+    for r, k in zip(rows, kinds_in_order([r["Kernel_Name"] for r in rows])):
         if k:
             by_kind.setdefault(k, []).append((r["Kernel_Name"], (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3))
     stats = _csv_rows(trace_dir, "kernel_stats.csv")
@@ -213,18 +230,18 @@ def summarize_pmc(fetch_dir: str, write_dir: str, copy_fetch_dir: str, copy_writ
     per = {}
     for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         by_kind = {}
-        for _, n, v in _pmc_per_dispatch(d, name):
-            k = kernel_kind(n)
+        disp = _pmc_per_dispatch(d, name)
+        for (_, n, v), k in zip(disp, kinds_in_order([n for _, n, _ in disp])):
             if k:
                 by_kind.setdefault(k, []).append(v)
         for k, n in b["kernel_launches"].items():
             vals = by_kind.get(k, [])[-n:]
             if vals:
                 per.setdefault(k, {})[name] = statistics.mean(vals) * 1024.0 * scale[name]
-    lines = [f"# HBM traffic per launch from rocprofv3 --pmc passes over one bench.py run: {b['config']['workload']}",
+    lines = [f"# HBM traffic per launch from rocprofv3 --pmc passes (workload in {b['config']['workload']})",
              f"# commands: {commands}",
              f"# mean rows/step {b['config']['rows_mean']}; per kind: mean over the last n dispatches "
-             "(the bench's event-timed steps)",
+             "(the incremental steps; n from the run's own launch counts)",
              f"# copy calibration ({nbytes} bytes copied): FETCH_SIZE scale {scale['FETCH_SIZE']:.4f}, "
              f"WRITE_SIZE scale {scale['WRITE_SIZE']:.4f}",
              f"source_hash {source_hash()}",
@@ -237,6 +254,28 @@ def summarize_pmc(fetch_dir: str, write_dir: str, copy_fetch_dir: str, copy_writ
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def dump_workload(name: str, rho: float, directory: str, frames: int) -> int:
+    """Write a workload for the native driver (CPU only): config.txt,
+    weights.bin (canonical, storage dtype) and frames.bin ([frames][views][N][P] f32)."""
+    import numpy as np
+    from paper_2607_12287_amd import synth
+    wl = synth.workload(name, rho=rho)
+    m = wl.model
+    os.makedirs(directory, exist_ok=True)
+    w = synth.flatten_weights(m, wl.weights())
+    if m.dtype == "bf16":  # the weights are bf16 values already: keep the high halves
+        w = (w.view(np.uint32) >> 16).astype(np.uint16)
+    w.tofile(os.path.join(directory, "weights.bin"))
+    np.stack(list(wl.patch_frames(frames))).astype(np.float32).tofile(os.path.join(directory, "frames.bin"))
+    fields = [m.img_h, m.img_w, m.channels, m.patch, m.dim, m.depth, m.heads, m.mlp_dim,
+              1 if m.dtype == "bf16" else 0, repr(float(m.ln_eps)), wl.views, frames, repr(float(wl.tau))]
+    fields += list(wl.caps)
+    with open(os.path.join(directory, "config.txt"), "w") as fh:
+        fh.write(" ".join(str(x) for x in fields) + "\n")
+    print(json.dumps({"workload": wl.name, "dir": directory, "frames": frames}))
+    return 0
 
 
 def copy_pass(mib: int) -> int:
@@ -258,6 +297,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--copy-pass", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device (calibration of the HBM counters)")
+    ap.add_argument("--dump-workload", metavar="DIR", help="write the workload for the native driver and exit (CPU)")
     ap.add_argument("--summarize-trace", nargs=5, metavar=("TRACE_DIR", "TRACED_BENCH_LOG", "PLAIN_BENCH_LOG", "OUT",
                                                            "COMMAND"))
     ap.add_argument("--summarize-pmc", nargs=8, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
@@ -282,6 +322,8 @@ def main() -> int:
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
         return 0
+    if args.dump_workload:
+        return dump_workload(args.workload, args.rho, args.dump_workload, args.steps + 1)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the encoder's state is per stream and this build runs "

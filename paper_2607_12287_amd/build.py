@@ -14,6 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libincvit.so")
+DRIVE = os.path.join(HERE, "incvit_drive")
 SOURCES = ["incvit_api.hip", "k_embed.hip", "k_select.hip", "k_gemm.hip", "k_gemm_qkv.hip",
            "k_gemm_fc1.hip", "k_gemm_part.hip", "k_rows.hip", "k_attn.hip", "k_misc.hip"]
 # the fixed-order fp32 embedding and cosine must not be contracted beyond the
@@ -51,8 +52,16 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stderr}")
     os.replace(tmp, LIB)
+    # the native driver (counter passes run it without a Python runtime)
+    tmp = DRIVE + f".tmp{os.getpid()}"
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-O2", "-std=c++17", "-x", "hip", os.path.join(CSRC, "incvit_drive.cpp"),
+           "-I", os.path.join(ROOT, "include"), "-L", HERE, "-lincvit", "-Wl,-rpath,$ORIGIN", "-o", tmp]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"driver build failed:\n{res.stderr}")
+    os.replace(tmp, DRIVE)
     if verbose:
-        print("built", LIB)
+        print("built", LIB, "and", DRIVE)
     return LIB
 
 

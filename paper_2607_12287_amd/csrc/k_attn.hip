@@ -85,9 +85,9 @@ __device__ __forceinline__ void mask_v(V8<float>& v, int first_key, int N) {
 // its KW waves split the stream's key blocks into contiguous runs and each
 // wave processes every query tile of the workgroup against its keys, so a
 // key/value block is read once for QT*16 queries.  Key/value loads do not
-// depend on the row offsets, so the first group of them is issued before the
-// offsets are read; the first stream's rows always start at 0, so its query
-// loads are issued early too.  The waves' (max, sum, O) are merged in a fixed
+// depend on the row offsets, so the first query group issues its first group
+// of them before the offsets are read; the first stream's rows always start at
+// 0, so its query loads are issued early too.  The waves' (max, sum, O) are merged in a fixed
 // two-level tree through LDS.
 template <class T, int NDC, int NDT, int GB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
@@ -119,7 +119,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       load_vblock<T, NDT>(vop[b], vbase, k, lane);
     }
   };
-  load_group(kb0);
+  // Only the first query group of a stream is active for certain (its rows
+  // start the stream's share): it loads before reading the offsets.  The other
+  // groups read them first and leave without loading when they have no rows.
+  const bool first = blockIdx.x == 0;
+  if (first) load_group(kb0);
 
   const int q0 = blockIdx.x * QT * 16;
   // Q fragments: dims past d_h read in-bounds data of the same row and are
@@ -139,11 +143,12 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   };
   // the first stream's rows start at 0: its queries are loaded before the
   // offsets arrive (rows past the stream's count are clamped and never stored)
-  if (v == 0) load_q(0, a.qmax + 1);
+  if (first && v == 0) load_q(0, a.qmax + 1);
   const int rowbase = off_v;
   const int kv = off_next - off_v;
   if (q0 >= kv) return;  // uniform per workgroup
-  if (v != 0) load_q(rowbase, kv);
+  if (!first) load_group(kb0);
+  if (!first || v != 0) load_q(rowbase, kv);
 
   float m_run[QT], l_run[QT];
   f32x4_t o[QT][NDT];

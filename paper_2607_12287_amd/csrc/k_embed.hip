@@ -42,13 +42,24 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
   __shared__ __align__(16) float sx[64][16];  // [k][token]
   __shared__ __align__(16) float sw[64][64];  // [k][column]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int v = blockIdx.z, tok0 = blockIdx.x * 16, c0 = blockIdx.y * 64;
+  // Workgroups are dealt to the 8 XCDs round robin by linear launch index, and
+  // each XCD has its own L2.  Renumber them XCD-major (a bijection) and take
+  // (stream, column block, token group) from the new number, so that the
+  // workgroups of one column block sit on one XCD (at most two): its weights
+  // come from HBM once rather than once per XCD.
+  const int ntg = gridDim.x, ncb = gridDim.y;
+  const int total = ntg * ncb * gridDim.z;
+  const int i = blockIdx.x + ntg * (blockIdx.y + ncb * blockIdx.z);
+  const int x = i % 8, q = total / 8, rem = total % 8;
+  const int pos = x * q + min(x, rem) + i / 8;
+  const int v = pos / (ncb * ntg), cb = (pos / ntg) % ncb, tg = pos % ntg;
+  const int tok0 = tg * 16, c0 = cb * 64;
   const int N = a.N, P = a.P, D = a.D;
 
-  if (blockIdx.x == 0 && blockIdx.y == 0) {
-    for (int i = tid; i < a.nzero && v == 0; i += 256) a.zero[i] = 0;
+  if (tg == 0 && cb == 0) {
+    for (int k = tid; k < a.nzero && v == 0; k += 256) a.zero[k] = 0;
     if (a.ident_idx) {
-      for (int i = tid; i < N; i += 256) a.ident_idx[v * N + i] = i;
+      for (int k = tid; k < N; k += 256) a.ident_idx[v * N + k] = k;
       if (tid == 0) a.ident_count[v] = N;
     }
   }
