@@ -87,13 +87,13 @@ __device__ __forceinline__ void mask_v(V8<float>& v, int first_key, int N) {
 // key/value block is read once for QT*16 queries.  Key/value loads do not
 // depend on the row offsets, so the first query group issues its first group
 // of them before the offsets are read; the first stream's rows always start at
-// 0, so its query loads are issued early too.  The waves' (max, sum, O) are merged in a fixed
-// two-level tree through LDS.
+// 0, so its query loads are issued early too.  The waves' (max, sum, O) are
+// exchanged through LDS once and combined in wave order, each wave finishing
+// a share of the output tiles.
 template <class T, int NDC, int NDT, int GB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int KW = 4, QT = 2;
-  __shared__ float s_m[2][QT][16], s_l[2][QT][16];
-  __shared__ f32x4_t s_o[2][QT][NDT][64];
+  extern __shared__ __align__(16) char attn_smem[];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -223,63 +223,69 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     l_run[qt] += __shfl_xor(l_run[qt], 32, 64);
   }
 
-  // merge: waves 2,3 into 0,1, then wave 1 into 0
-#pragma unroll
-  for (int half = 2; half >= 1; half >>= 1) {
-    if (w >= half && w < 2 * half) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        if (g == 0) {
-          s_m[w - half][qt][n] = m_run[qt];
-          s_l[w - half][qt][n] = l_run[qt];
-        }
-#pragma unroll
-        for (int t = 0; t < NDT; ++t) s_o[w - half][qt][t][lane] = o[qt][t];
-      }
-    }
-    __syncthreads();
-    if (w < half) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        const float mo = s_m[w][qt][n], lo = s_l[w][qt][n];
-        const float mm = fmaxf(m_run[qt], mo);
-        const float fa = m_run[qt] == -INFINITY ? 0.0f : exp2f(m_run[qt] - mm);
-        const float fb = mo == -INFINITY ? 0.0f : exp2f(mo - mm);
-        l_run[qt] = fa * l_run[qt] + fb * lo;
-        m_run[qt] = mm;
-#pragma unroll
-        for (int t = 0; t < NDT; ++t) o[qt][t] = o[qt][t] * fa + s_o[w][qt][t][lane] * fb;
-      }
-    }
-    __syncthreads();
-  }
-  if (w != 0) return;
-
+  // merge: every wave publishes (max, sum, O) of its keys; then each wave
+  // combines the four partials, in wave order, for its share of the output
+  // tiles and stores them
+  float* s_m = reinterpret_cast<float*>(attn_smem);               // [KW][QT][16]
+  float* s_l = s_m + KW * QT * 16;                                 // [KW][QT][16]
+  f32x4_t* s_o = reinterpret_cast<f32x4_t*>(s_l + KW * QT * 16);   // [KW][QT][NDT][64]
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
+    if (g == 0) {
+      s_m[(w * QT + qt) * 16 + n] = m_run[qt];
+      s_l[(w * QT + qt) * 16 + n] = l_run[qt];
+    }
+#pragma unroll
+    for (int t = 0; t < NDT; ++t) s_o[((w * QT + qt) * NDT + t) * 64 + lane] = o[qt][t];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = w; it < QT * NDT; it += KW) {
+    const int qt = it / NDT, t = it % NDT;
     const int qrow = q0 + 16 * qt + n;
-    if (qrow < kv) {
-      const float inv = 1.0f / l_run[qt];
-      T* out = static_cast<T*>(a.o) + (size_t)(rowbase + qrow) * D + h * dh;
+    const int d0 = 16 * t + 4 * g;
+    float mm = -INFINITY;
 #pragma unroll
-      for (int t = 0; t < NDT; ++t) {
-        const int d0 = 16 * t + 4 * g;
-        if (d0 < dh) {
-          float r[4];
+    for (int ww = 0; ww < KW; ++ww) mm = fmaxf(mm, s_m[(ww * QT + qt) * 16 + n]);
+    float lsum = 0.0f;
+    f32x4_t acc = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-          for (int i = 0; i < 4; ++i) r[i] = o[qt][t][i] * inv;
-          store4<T>(out + d0, r);
-        }
-      }
+    for (int ww = 0; ww < KW; ++ww) {
+      const float mw = s_m[(ww * QT + qt) * 16 + n];
+      const float f = mw == -INFINITY ? 0.0f : exp2f(mw - mm);
+      lsum += f * s_l[(ww * QT + qt) * 16 + n];
+      acc += s_o[((ww * QT + qt) * NDT + t) * 64 + lane] * f;
+    }
+    if (qrow < kv && d0 < dh) {
+      const float inv = 1.0f / lsum;
+      float r[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[i] = acc[i] * inv;
+      store4<T>(static_cast<T*>(a.o) + (size_t)(rowbase + qrow) * D + h * dh + d0, r);
     }
   }
+}
+
+template <int NDT>
+constexpr int attn_lds_bytes() {
+  return 4 * 2 * 16 * 4 * 2 + 4 * 2 * NDT * 64 * 16;  // m and l, then O, for KW = 4 and QT = 2
+}
+
+template <class T, int NDC, int NDT, int GB>
+static void launch_g(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, GB>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, attn_lds_bytes<NDT>()) == hipSuccess;
+  }
+  (void)launch_k((attn_kernel<T, NDC, NDT, GB>), grid, dim3(256), (size_t)attn_lds_bytes<NDT>(), s, a);
 }
 
 template <class T, int NDC, int NDT>
 static void launch_t(const AttnArgs& a, dim3 grid, hipStream_t s) {
   // two key blocks in flight per wave where the registers allow
-  if constexpr (NDT <= 6) (void)launch_k((attn_kernel<T, NDC, NDT, 2>), grid, dim3(256), 0, s, a);
-  else (void)launch_k((attn_kernel<T, NDC, NDT, 1>), grid, dim3(256), 0, s, a);
+  if constexpr (NDT <= 6) launch_g<T, NDC, NDT, 2>(a, grid, s);
+  else launch_g<T, NDC, NDT, 1>(a, grid, s);
 }
 
 template <class T>
