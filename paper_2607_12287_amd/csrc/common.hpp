@@ -352,6 +352,15 @@ __device__ __forceinline__ T* x_row(char* cache, const CacheLayout& cl, const Sh
   return reinterpret_cast<T*>(cache + cl.x + (size_t)layer * cl.x_layer) + (size_t)tok * sh.D;
 }
 
+// Compact GEMM inputs (A1/A2, O, G) are stored as MFMA A operands: for row r
+// and column k of a [rows][32 kc] matrix, 16-row tile r/16 and 32-deep chunk
+// k/32 form one kilobyte (bf16) in which lane 16*((k%32)/8) + r%16 holds 8
+// consecutive k; so a GEMM loads each operand fragment as one contiguous
+// block, and a row's 4-aligned runs of 4 columns stay contiguous for writers.
+__host__ __device__ __forceinline__ size_t frag_off(int r, int k, int kc) {
+  return (((size_t)(r >> 4) * kc + (k >> 5)) * 64 + (((k & 31) >> 3) << 4) + (r & 15)) * 8 + (k & 7);
+}
+
 // Cached K and V of one layer are stored as the attention's MFMA operands, so
 // that each operand load is one contiguous kilobyte.  Per head, per block of
 // 32 keys (kb), head dims padded to 32 * ndc:

@@ -5,6 +5,7 @@
 //         row kernel that produced Z_l; Q -> workspace, K and V rows scattered
 //         into the cached K^l, V^l of each stream (eq. 5);
 //   FC1 : G = S(GELU(A2 W_1 + b_1)), A2 = S(LN2(H)) from the row kernel;
+// (A1, A2, O and G are kept in MFMA operand order, frag_off)
 //   PART: raw partial sums of A W over one share of K (the output projection
 //         and the MLP down projection); a row kernel adds the bias, the
 //         residual and the next LayerNorm.
@@ -65,12 +66,13 @@ __global__ __launch_bounds__(kGemmWaves * 64) void gemm_kernel(GemmArgs a) {
   auto kc_of = [&](int round, int c) { return kb + min((round * NW + w) * CPW + c, kc_last); };
   V8<T> ab[CPW][2];
   V8<T> wb[CPW][NB];
+  const int akc = a.lda / 32;  // A is stored in operand order (frag_off)
   auto load_a = [&](int m0, int round) {
 #pragma unroll
     for (int c = 0; c < CPW; ++c)
 #pragma unroll
       for (int r = 0; r < 2; ++r)
-        ab[c][r].load(A + (size_t)(m0 + 16 * r + n) * a.lda + kc_of(round, c) * 32 + 8 * g);
+        ab[c][r].load(A + (((size_t)((m0 >> 4) + r) * akc + kc_of(round, c)) * 64 + lane) * 8);
   };
   auto load_w = [&](int round) {
 #pragma unroll
@@ -157,7 +159,7 @@ __global__ __launch_bounds__(kGemmWaves * 64) void gemm_kernel(GemmArgs a) {
         }
       } else {  // EPI_FC1
         x += biasv[b];
-        if (ok) static_cast<T*>(a.out)[(size_t)row * a.ldo + col] = Elem<T>::cv(gelu_tanh(x));
+        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(gelu_tanh(x));
       }
     }
     __syncthreads();  // red is reused by the next row block

@@ -261,7 +261,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       float r[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) r[i] = acc[i] * inv;
-      store4<T>(static_cast<T*>(a.o) + (size_t)(rowbase + qrow) * D + h * dh + d0, r);
+      store4<T>(static_cast<T*>(a.o) + frag_off(rowbase + qrow, h * dh + d0, D / 32), r);
     }
   }
 }

@@ -130,9 +130,11 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
                                     (v[j].y - mean) * rstd * gam[j].y + bet[j].y,
                                     (v[j].z - mean) * rstd * gam[j].z + bet[j].z,
                                     (v[j].w - mean) * rstd * gam[j].w + bet[j].w);
+      // the normalised row goes out in operand order (frag_off), 4 columns at a time
+      T* arow = static_cast<T*>(a.a_out) + frag_off(r, 4 * q, D / 32);
       if constexpr (MODE == RES_LN2) {
         st4(a.h_out + (size_t)r * D, q, v[j]);
-        st4(static_cast<T*>(a.a_out) + (size_t)r * D, q, n4);
+        st4(arow, 0, n4);
       } else {
         st4(static_cast<T*>(a.z_out) + (size_t)r * D, q, v[j]);
         st4(xrow, q, v[j]);
@@ -140,7 +142,7 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
           st4(yrow, q, n4);
           if (outrow) st4(outrow, q, n4);
         } else {
-          st4(static_cast<T*>(a.a_out) + (size_t)r * D, q, n4);
+          st4(arow, 0, n4);
         }
       }
     }

@@ -268,7 +268,7 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   float4* ref = reinterpret_cast<float4*>(cache + a.cl.ref + (size_t)tok * D * 4);
   T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
   T* z0 = static_cast<T*>(a.z) + (size_t)r * D;
-  T* a0 = static_cast<T*>(a.a) + (size_t)r * D;
+  T* abase = static_cast<T*>(a.a);  // operand order (frag_off)
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     const int q = tid + 256 * j;
@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
       ref[q] = t[j];
       store4v(x0 + 4 * q, zr[j]);
       store4v(z0 + 4 * q, zr[j]);
-      store4v(a0 + 4 * q, make_float4((zr[j].x - mean) * rstd * gv[j].x + bv[j].x,
+      store4v(abase + frag_off(r, 4 * q, D / 32), make_float4((zr[j].x - mean) * rstd * gv[j].x + bv[j].x,
                                       (zr[j].y - mean) * rstd * gv[j].y + bv[j].y,
                                       (zr[j].z - mean) * rstd * gv[j].z + bv[j].z,
                                       (zr[j].w - mean) * rstd * gv[j].w + bv[j].w));
