@@ -29,8 +29,7 @@ METRIC = "incremental ViT frames/sec at 10% refresh (So400m shape); speedup vs f
 HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PROFILES = os.path.join(ROOT, "profiles")
-GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "part"}  # epilogue template argument
-RES_KIND = {"0": "res_ln2", "1": "res_ln1"}
+GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj"}  # epilogue template argument
 
 
 def source_hash() -> str:
@@ -46,30 +45,20 @@ def source_hash() -> str:
 
 
 def kernel_kind(name: str):
-    """Kernel kind of a dispatch name in a rocprofv3 trace (None for other kernels;
-    "part" for the split-K GEMM, which is the output projection and the MLP down
-    projection in turn: see kinds_in_order)."""
+    """Kernel kind of a dispatch name in a rocprofv3 trace (None for other kernels)."""
     m = re.search(r"incvit::(\w+)_kernel(?:<([^>]*)>)?", name)
     if not m:
         return None
     if m.group(1) == "gemm":
         return GEMM_KIND.get(m.group(2).split(",")[1].strip())
     if m.group(1) == "res":
-        return RES_KIND.get(m.group(2).split(",")[1].strip())
+        return "res_ln1"
     return m.group(1)
 
 
 def kinds_in_order(names):
-    """Kinds of dispatches given in launch order; split-K GEMM dispatches
-    alternate between the output projection and the MLP down projection."""
-    out, part = [], 0
-    for n in names:
-        k = kernel_kind(n)
-        if k == "part":
-            k = "oproj" if part % 2 == 0 else "fc2"
-            part += 1
-        out.append(k)
-    return out
+    """Kinds of dispatches given in launch order."""
+    return [kernel_kind(n) for n in names]
 
 
 def stored_traffic(workload: str, kind: str):
@@ -90,10 +79,10 @@ def stored_traffic(workload: str, kind: str):
     return vals.get(kind)
 
 
-def ksplit(m, kind: str) -> int:
-    """K split of the output / MLP-down projections (the library's rule)."""
+def ksplit(m) -> int:
+    """K split of the MLP down projection (the library's rule)."""
     nblocks = m.dim // 16
-    kchunks = (m.dim if kind == "oproj" else -(-m.mlp_dim // 32) * 32) // 32
+    kchunks = -(-m.mlp_dim // 32)
     return max(1, min(4, 256 // nblocks, kchunks // 8))
 
 
@@ -102,15 +91,14 @@ def kernel_bytes(m, M: float, kind: str):
     (weights once, each row operand once; partial sums of a split K counted as
     written and read once).  None for kinds without a figure here."""
     D, F, eb = m.dim, m.mlp_dim, (2 if m.dtype == "bf16" else 4)
-    so, s2 = ksplit(m, "oproj"), ksplit(m, "fc2")
+    s2 = ksplit(m)
+    st = M * (D // 16) * 8  # LN2 block statistics of H
     if kind == "qkv":
         return 3 * D * D * eb + M * D * eb + 3 * M * D * eb
     if kind == "oproj":
-        return D * D * eb + M * D * eb + so * M * D * 4
-    if kind == "res_ln2":
-        return so * M * D * 4 + M * D * eb + M * D * 4 + M * D * eb
+        return D * D * eb + 2 * M * D * eb + M * D * 4 + st
     if kind == "fc1":
-        return D * F * eb + M * D * eb + M * F * eb
+        return D * F * eb + M * D * 4 + st + M * F * eb
     if kind == "fc2":
         return F * D * eb + M * F * eb + s2 * M * D * 4
     if kind == "res_ln1":
@@ -315,6 +303,7 @@ def main() -> int:
                     help="launch kernel by kernel instead of replaying captured HIP graphs")
     ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four comma-separated values "
                                                  "(QKV, O-proj, fc1, fc2; 0 = automatic)")
+    ap.add_argument("--attn-qtiles", type=int, default=0, help="16-query tiles per attention workgroup (0 = automatic)")
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
@@ -346,8 +335,9 @@ def main() -> int:
     torch.cuda.set_device(dev)
     frames = torch.from_numpy(np.stack(frames_np)).to(dev)  # [T][B][N][P], resident in HBM
     enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
-    if args.cols:
-        incvit._check(incvit.incvit_set_tuning(enc.h, [int(x) for x in args.cols.split(",")]), enc.h)
+    if args.cols or args.attn_qtiles:
+        cols = [int(x) for x in args.cols.split(",")] if args.cols else None
+        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),

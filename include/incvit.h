@@ -197,9 +197,12 @@ void incvit_graph_destroy(incvit_graph* g);
  * settings differ only in the order of fp32 partial sums.
  * cols[k]: 16-column blocks per workgroup of GEMM k (0 = QKV, 1 = output
  * projection, 2 = MLP up, 3 = MLP down): 1 or 2 (2 only takes effect when the
- * block count is even); 0 = automatic.  A NULL pointer restores the defaults. */
+ * block count is even); 0 = automatic.
+ * attn_qtiles: 16-query tiles per attention workgroup: 1 or 2; 0 = automatic.
+ * A NULL pointer restores the defaults. */
 typedef struct {
   int32_t cols[4];
+  int32_t attn_qtiles;
 } incvit_tuning;
 
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);
@@ -214,8 +217,7 @@ typedef enum {
   INCVIT_K_COMMIT,    /* ref, X0 of the selected rows; LN1 of layer 0     */
   INCVIT_K_QKV,       /* QKV projection, K/V scattered into the cache     */
   INCVIT_K_ATTN,      /* attention of the selected queries                */
-  INCVIT_K_OPROJ,     /* output projection (split-K partial sums)         */
-  INCVIT_K_RES_LN2,   /* + bias + residual -> H; LN2                      */
+  INCVIT_K_OPROJ,     /* output projection + residual -> H; LN2 statistics */
   INCVIT_K_FC1,       /* MLP up projection + GELU                         */
   INCVIT_K_FC2,       /* MLP down projection (split-K partial sums)       */
   INCVIT_K_RES_LN1,   /* + bias + residual -> X^{l+1}; next LN1 or final LN */

@@ -142,7 +142,7 @@ struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map, A1 of la
   void* a;           // compact S(LN1(Z_0)) [Mpad][D]
 };
 
-enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2 };
+enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3 };
 
 struct GemmArgs {
   const RowInfo* rows;  // row map (cache, token, stream) of each compact row
@@ -150,23 +150,26 @@ struct GemmArgs {
   CacheLayout cl;
   Shape sh;
   int layer;
-  const void* A;      // compact A rows (storage type): QKV A1, FC1 A2, PART O or G
+  const void* A;      // compact A rows in operand order: QKV A1, RES O, FC1 H (fp32), PART G
   int lda;
   const void* W;      // packed [Nout/16][kchunks][512]
   const float* bias;  // [Nout] (not used by PART)
   int kchunks, Nout;
-  void* out;          // QKV Q [Mpad][D]; FC1 G [Mpad][Fpad]; PART f32 [ksplit][mpad][ldo]
+  void* out;          // QKV Q [Mpad][D]; RES H (fp32, operand order); FC1 G; PART f32 [ksplit][mpad][ldo]
   int ldo;
   int ksplit;         // K is split over gridDim.y = ksplit workgroups (PART)
-  int mpad;           // rows of one partial slice (PART)
+  int mpad;           // padded rows (partial slices, statistics)
+  const void* resid;  // RES: Z_l rows [Mpad][D] (storage type)
+  float2* stats;      // RES writes, FC1 reads: (mean, sum of squared deviations) of H per
+                      // 16-column block and row, [D/16][mpad]
+  const float* ln_g;  // FC1: LN2 gamma, beta [D]
+  const float* ln_b;
 };
 
-// Row kernels that finish a split-K GEMM, one wave per compact row:
-//   RES_LN2: H = Z_l + (partials + b_o) -> H (f32) and A2 = S(LN2(H));
-//   RES_LN1: Z_{l+1} = S(H + (partials + b_2)) -> compact Z and X^{l+1} of the
-//            cache, then A1 = S(LN1 of layer l+1 (Z_{l+1})), or after the last
-//            layer Y = S(LN_f(Z_L)) into the cache and the refreshed output.
-enum ResMode { RES_LN2 = 0, RES_LN1 = 1 };
+// Row kernel that finishes the split-K MLP down projection, one workgroup per
+// compact row: Z_{l+1} = S(H + (partials + b_2)) -> compact Z and X^{l+1} of
+// the cache, then A1 = S(LN1 of layer l+1 (Z_{l+1})), or after the last layer
+// Y = S(LN_f(Z_L)) into the cache and the refreshed output.
 struct ResArgs {
   const Meta* meta;
   const RowInfo* rows;
@@ -176,12 +179,11 @@ struct ResArgs {
   int last;           // RES_LN1 after the last layer: final LayerNorm
   const float* part;  // [ksplit][mpad][D]
   int ksplit, mpad;
-  const void* res;    // RES_LN2: Z_l (storage type); RES_LN1: H (f32)
+  const float* res;   // H (fp32, operand order)
   const float* bias;
   const float* ln_g;  // the LayerNorm applied to the new rows
   const float* ln_b;
-  float* h_out;       // RES_LN2: H
-  void* z_out;        // RES_LN1: Z_{l+1}
+  void* z_out;        // Z_{l+1}
   void* a_out;        // normalised rows (not for the final LayerNorm)
   void* refreshed;    // final: optional [B][N][D]
   int N;
@@ -198,6 +200,7 @@ struct AttnArgs {
   void* o;        // [Mpad][D]
   int qmax;       // Mpad - 1: last row a clamped load may touch
   float scale_log2;
+  int nspec;      // query groups that load keys before reading the row offsets
 };
 
 struct PackArgs {
@@ -246,8 +249,8 @@ hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
-hipError_t launch_res(int mode, const ResArgs& a, int mmax, hipStream_t s);
-hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s);
+hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, int qtiles, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);
 hipError_t launch_export(const ExportArgs& a, hipStream_t s);
@@ -277,12 +280,14 @@ __device__ __forceinline__ const INCVIT_GLOBAL T* gbl(const T* p) {
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// fp32 -> bf16 bits, round to nearest even (inputs are finite here; NaN kept NaN).
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+// fp32 -> bf16 bits, round to nearest even: gfx950's v_cvt_pk_bf16_f32 (two
+// conversions per instruction; NaN stays NaN).
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// two values packed, the first in the low half
+__device__ __forceinline__ uint32_t f2bf2(float a, float b) {
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 template <class T> struct Elem;
@@ -299,6 +304,21 @@ template <> struct Elem<float> {
   __device__ static float rnd(float f) { return f; }
 };
 
+// Buffer resources: a wave-uniform base and byte size in SGPRs, so that a
+// load needs one 32-bit lane offset (shared by every load of a wave) plus a
+// wave-uniform offset instead of a 64-bit address per load; reads past the
+// size return zero.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+__device__ __forceinline__ Rsrc make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(Rsrc r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ float4 bload16f(Rsrc r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
 // 8 consecutive elements of one lane: one MFMA operand for a 32-deep chunk.
 template <class T> struct V8;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -306,6 +326,8 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 template <> struct V8<uint16_t> {
   uint4 v;
   __device__ void load(const uint16_t* p) { v = __builtin_bit_cast(uint4, *(const INCVIT_GLOBAL u32x4_t*)p); }
+  // lane offset voff (16 bytes per lane), wave-uniform offset soff, in bytes
+  __device__ void bload(Rsrc r, uint32_t voff, uint32_t soff) { v = bload16(r, voff, soff); }
   __device__ void zero() { v = make_uint4(0, 0, 0, 0); }
 };
 template <> struct V8<float> {
@@ -313,6 +335,11 @@ template <> struct V8<float> {
   __device__ void load(const float* p) {
     a = __builtin_bit_cast(float4, ((const INCVIT_GLOBAL f32x4_t*)p)[0]);
     b = __builtin_bit_cast(float4, ((const INCVIT_GLOBAL f32x4_t*)p)[1]);
+  }
+  // lane offset voff (32 bytes per lane), wave-uniform offset soff, in bytes
+  __device__ void bload(Rsrc r, uint32_t voff, uint32_t soff) {
+    a = bload16f(r, voff, soff);
+    b = bload16f(r, voff + 16, soff);
   }
   __device__ void zero() { a = make_float4(0, 0, 0, 0); b = a; }
 };

@@ -36,7 +36,7 @@ struct CanonLayout {  // element offsets into the canonical buffer
 };
 
 struct WsLayout {
-  size_t meta, rows, count, idx, sim, t0, z, a, q, o, h, g, part, total;
+  size_t meta, rows, count, idx, sim, t0, z, a, q, o, h, g, part, stats, total;
   int Mpad;
 };
 
@@ -187,12 +187,13 @@ GemmGeom gemm_geom(const Shape& sh, int kind) {
   }
   g.kchunks = round_up(g.K, 32) / 32;
   g.nblocks = g.Nout / 16;
-  // The output projection and the MLP down projection have D/16 column blocks,
-  // too few to fill 256 CUs: their K is split over up to 4 workgroups (at least
-  // 8 chunks each), and a row kernel adds the partial sums, the bias, the
-  // residual and the next LayerNorm.  QKV and fc1 are not split.
+  // The MLP down projection has D/16 column blocks over a long K = F: its K is
+  // split over up to 4 workgroups (at least 8 chunks each), and a row kernel
+  // adds the partial sums, the bias, the residual and the next LayerNorm.  The
+  // output projection (K = D) is not split: its epilogue adds the residual
+  // itself and leaves the LN2 block statistics for fc1.
   g.ksplit = 1;
-  if (kind == G_OPROJ || kind == G_FC2)
+  if (kind == G_FC2)
     g.ksplit = std::max(1, std::min(std::min(4, 256 / std::max(g.nblocks, 1)), g.kchunks / 8));
   return g;
 }
@@ -203,6 +204,15 @@ int cols_of(const int* tuned, const GemmGeom& g, int kind) {
   const int t = tuned ? tuned[kind] : 0;
   if (t > 0) return t;
   return g.nblocks > 256 ? 2 : 1;
+}
+
+// Query tiles per attention workgroup: one tile per workgroup while two-tile
+// workgroups would leave most CUs idle (few streams and heads), otherwise
+// two, which halves the K/V reads when a stream has many refreshed rows.
+int attn_qtiles_of(int tuned, int B, int H, int max_rows_per_view) {
+  if (tuned > 0) return tuned;
+  const int groups2 = (max_rows_per_view + 31) / 32;
+  return std::min(groups2, 2) * B * H < 128 ? 1 : 2;
 }
 
 WsLayout ws_layout(const Shape& sh, int B) {
@@ -223,8 +233,8 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
   w.h = take((size_t)w.Mpad * sh.D * 4);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
-  const int split = std::max(gemm_geom(sh, G_OPROJ).ksplit, gemm_geom(sh, G_FC2).ksplit);
-  w.part = take((size_t)split * w.Mpad * sh.D * 4);
+  w.part = take((size_t)gemm_geom(sh, G_FC2).ksplit * w.Mpad * sh.D * 4);
+  w.stats = take((size_t)(sh.D / 16) * w.Mpad * 8);
   w.total = off;
   return w;
 }
@@ -249,6 +259,7 @@ struct incvit_handle {
   double prof_ms[INCVIT_K_COUNT] = {};
   int64_t prof_n[INCVIT_K_COUNT] = {};
   int cols[4] = {0, 0, 0, 0};  // 0 = automatic
+  int attn_qtiles = 0;         // 0 = automatic
 };
 
 struct incvit_graph {
@@ -340,14 +351,19 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           a.out = ws + wl.q; a.ldo = sh.D;
           break;
         case G_OPROJ:
+          epi = EPI_RES;
           a.A = ws + wl.o; a.lda = sh.D;
-          a.W = h->packed + P.w_o;
-          a.out = ws + wl.part; a.ldo = sh.D;
+          a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
+          a.resid = ws + wl.z;
+          a.out = ws + wl.h; a.ldo = sh.D;
+          a.stats = reinterpret_cast<float2*>(ws + wl.stats);
           break;
         case G_FC1:
           epi = EPI_FC1;
-          a.A = ws + wl.a; a.lda = sh.D;
+          a.A = ws + wl.h; a.lda = sh.D;
           a.W = h->packed + P.w_1; a.bias = fptr(h, P.b_1);
+          a.stats = reinterpret_cast<float2*>(ws + wl.stats);
+          a.ln_g = fptr(h, P.ln2_g); a.ln_b = fptr(h, P.ln2_b);
           a.out = ws + wl.g; a.ldo = sh.Fpad;
           break;
         default:
@@ -359,8 +375,8 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       const int cols = cols_of(h->cols, g, kind);
       return run(h, kernel_kind, s, [&] { return launch_gemm(epi, cols, a, s); });
     };
-    auto rowk = [&](int mode, int kernel_kind) -> incvit_status {
-      const GemmGeom g = gemm_geom(sh, mode == RES_LN2 ? G_OPROJ : G_FC2);
+    auto rowk = [&](int kernel_kind) -> incvit_status {
+      const GemmGeom g = gemm_geom(sh, G_FC2);
       ResArgs r;
       memset(&r, 0, sizeof r);
       r.meta = meta;
@@ -372,29 +388,20 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       r.ksplit = g.ksplit;
       r.mpad = wl.Mpad;
       r.N = sh.N;
-      if (mode == RES_LN2) {
-        r.res = ws + wl.z;
-        r.bias = fptr(h, P.b_o);
-        r.ln_g = fptr(h, P.ln2_g);
-        r.ln_b = fptr(h, P.ln2_b);
-        r.h_out = reinterpret_cast<float*>(ws + wl.h);
-        r.a_out = ws + wl.a;
+      r.res = reinterpret_cast<const float*>(ws + wl.h);
+      r.bias = fptr(h, P.b_2);
+      r.z_out = ws + wl.z;
+      r.last = l + 1 == sh.L;
+      if (r.last) {
+        r.ln_g = fptr(h, h->pl.lnf_g);
+        r.ln_b = fptr(h, h->pl.lnf_b);
+        r.refreshed = refreshed;
       } else {
-        r.res = ws + wl.h;
-        r.bias = fptr(h, P.b_2);
-        r.z_out = ws + wl.z;
-        r.last = l + 1 == sh.L;
-        if (r.last) {
-          r.ln_g = fptr(h, h->pl.lnf_g);
-          r.ln_b = fptr(h, h->pl.lnf_b);
-          r.refreshed = refreshed;
-        } else {
-          r.ln_g = fptr(h, h->pl.layers[l + 1].ln1_g);
-          r.ln_b = fptr(h, h->pl.layers[l + 1].ln1_b);
-          r.a_out = ws + wl.a;
-        }
+        r.ln_g = fptr(h, h->pl.layers[l + 1].ln1_g);
+        r.ln_b = fptr(h, h->pl.layers[l + 1].ln1_b);
+        r.a_out = ws + wl.a;
       }
-      return run(h, kernel_kind, s, [&] { return launch_res(mode, r, mmax, s); });
+      return run(h, kernel_kind, s, [&] { return launch_res(r, mmax, s); });
     };
 
     incvit_status st;
@@ -411,12 +418,13 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
     aa.o = ws + wl.o;
     aa.qmax = wl.Mpad - 1;
     aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
-    if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, s); })) != INCVIT_OK) return st;
+    const int qtiles = attn_qtiles_of(h->attn_qtiles, B, sh.H, max_rows_per_view);
+    if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, qtiles, s); })) != INCVIT_OK)
+      return st;
     if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
-    if ((st = rowk(RES_LN2, INCVIT_K_RES_LN2)) != INCVIT_OK) return st;
     if ((st = gemm(G_FC1, INCVIT_K_FC1)) != INCVIT_OK) return st;
     if ((st = gemm(G_FC2, INCVIT_K_FC2)) != INCVIT_OK) return st;
-    if ((st = rowk(RES_LN1, INCVIT_K_RES_LN1)) != INCVIT_OK) return st;
+    if ((st = rowk(INCVIT_K_RES_LN1)) != INCVIT_OK) return st;
   }
   return INCVIT_OK;
 }
@@ -720,7 +728,10 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
     const int c = t ? t->cols[k] : 0;
     if (c < 0 || c > 2) return fail(h, INCVIT_ERR_ARG, "cols must be 0, 1 or 2");
   }
+  const int q = t ? t->attn_qtiles : 0;
+  if (q < 0 || q > 2) return fail(h, INCVIT_ERR_ARG, "attn_qtiles must be 0, 1 or 2");
   for (int k = 0; k < 4; ++k) h->cols[k] = t ? t->cols[k] : 0;
+  h->attn_qtiles = q;
   return INCVIT_OK;
 }
 

@@ -194,10 +194,10 @@ int main(int argc, char** argv) {
   for (long m : rows) mean += (double)m / (rows.empty() ? 1 : rows.size());
   const long L = cfg.depth;
   printf("{\"steps\": %d, \"rows_mean\": %.3f, \"kernel_launches\": {\"embed\": %d, \"sim\": %d, \"select\": %d, "
-         "\"commit\": %ld, \"qkv\": %ld, \"attn\": %ld, \"oproj\": %ld, \"res_ln2\": %ld, \"fc1\": %ld, \"fc2\": %ld, "
+         "\"commit\": %ld, \"qkv\": %ld, \"attn\": %ld, \"oproj\": %ld, \"fc1\": %ld, \"fc2\": %ld, "
          "\"res_ln1\": %ld}, \"config\": {\"workload\": \"%s\", \"rows_mean\": %.3f}}\n",
          steps, mean, steps, steps, steps, active, active * L, active * L, active * L, active * L, active * L,
-         active * L, active * L, dir.c_str(), mean);
+         active * L, dir.c_str(), mean);
   incvit_destroy(h);
   return 0;
 }

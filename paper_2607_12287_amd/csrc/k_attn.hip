@@ -13,10 +13,7 @@
 namespace incvit {
 
 __device__ __forceinline__ void pack_p(V8<uint16_t>& out, const float* p) {
-  out.v = make_uint4((uint32_t)f2bf(p[0]) | ((uint32_t)f2bf(p[1]) << 16),
-                     (uint32_t)f2bf(p[2]) | ((uint32_t)f2bf(p[3]) << 16),
-                     (uint32_t)f2bf(p[4]) | ((uint32_t)f2bf(p[5]) << 16),
-                     (uint32_t)f2bf(p[6]) | ((uint32_t)f2bf(p[7]) << 16));
+  out.v = make_uint4(f2bf2(p[0], p[1]), f2bf2(p[2], p[3]), f2bf2(p[4], p[5]), f2bf2(p[6], p[7]));
 }
 __device__ __forceinline__ void pack_p(V8<float>& out, const float* p) {
   out.a = make_float4(p[0], p[1], p[2], p[3]);
@@ -27,8 +24,7 @@ template <class T>
 __device__ __forceinline__ void store4(T* dst, const float* v);
 template <>
 __device__ __forceinline__ void store4<uint16_t>(uint16_t* dst, const float* v) {
-  *reinterpret_cast<uint2*>(dst) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                                              (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+  *reinterpret_cast<uint2*>(dst) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
 }
 template <>
 __device__ __forceinline__ void store4<float>(float* dst, const float* v) {
@@ -81,18 +77,22 @@ __device__ __forceinline__ void mask_v(V8<float>& v, int first_key, int N) {
   v.b = make_float4(f[4], f[5], f[6], f[7]);
 }
 
-// One workgroup: QT query tiles (16 queries each) of one head of one stream;
-// its KW waves split the stream's key blocks into contiguous runs and each
-// wave processes every query tile of the workgroup against its keys, so a
-// key/value block is read once for QT*16 queries.  Key/value loads do not
-// depend on the row offsets, so the first query group issues its first group
-// of them before the offsets are read; the first stream's rows always start at
-// 0, so its query loads are issued early too.  The waves' (max, sum, O) are
-// exchanged through LDS once and combined in wave order, each wave finishing
-// a share of the output tiles.
-template <class T, int NDC, int NDT, int GB>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
-  constexpr int KW = 4, QT = 2;
+// One workgroup: QT query tiles (16 queries each) of one head of one stream.
+// Its KW = 8 waves split the stream's key blocks into contiguous runs (one
+// 32-key block per wave at N = 256), so the K/V of a head are pulled through
+// the CU by eight waves at once and each wave's chain of dependent MFMA and
+// softmax steps is short; every wave processes all QT query tiles against
+// its keys.  Key/value loads do not depend on the row offsets, so the first
+// `a.nspec` query groups issue their first key blocks before the offsets are
+// read; the first stream's rows always start at 0, so its query loads are
+// issued early too.  The waves' (max, sum, O) are exchanged through LDS once
+// and combined in wave order, each wave finishing a share of the output
+// tiles.
+constexpr int kAttnWaves = 8;
+
+template <class T, int NDC, int NDT, int GB, int QT>
+__global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(AttnArgs a) {
+  constexpr int KW = kAttnWaves;
   extern __shared__ __align__(16) char attn_smem[];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 
   // the stream's row offsets: scalar loads, issued first, waited for last
   const int off_v = a.meta->off[v], off_next = a.meta->off[v + 1];
-  const int kb0 = w * nkb / KW, kb1 = (w + 1) * nkb / KW;  // this wave's key blocks
+  const int kb0 = w * nkb / KW, kb1 = (w + 1) * nkb / KW;  // this wave's key blocks (may be none)
   V8<T> kop[GB][2][NDC], vop[GB][NDT];
   auto load_group = [&](int kb) {
 #pragma unroll
@@ -119,11 +119,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       load_vblock<T, NDT>(vop[b], vbase, k, lane);
     }
   };
-  // Only the first query group of a stream is active for certain (its rows
-  // start the stream's share): it loads before reading the offsets.  The other
-  // groups read them first and leave without loading when they have no rows.
-  const bool first = blockIdx.x == 0;
-  if (first) load_group(kb0);
+  // The first query groups of a stream are the likely active ones: they load
+  // before reading the offsets.  The other groups read them first and leave
+  // without loading when they have no rows.
+  const bool spec = (int)blockIdx.x < a.nspec;
+  if (spec && kb0 < kb1) load_group(kb0);
 
   const int q0 = blockIdx.x * QT * 16;
   // Q fragments: dims past d_h read in-bounds data of the same row and are
@@ -143,12 +143,12 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   };
   // the first stream's rows start at 0: its queries are loaded before the
   // offsets arrive (rows past the stream's count are clamped and never stored)
-  if (first && v == 0) load_q(0, a.qmax + 1);
+  if (spec && v == 0) load_q(0, a.qmax + 1);
   const int rowbase = off_v;
   const int kv = off_next - off_v;
   if (q0 >= kv) return;  // uniform per workgroup
-  if (!first) load_group(kb0);
-  if (!first || v != 0) load_q(rowbase, kv);
+  if (!spec && kb0 < kb1) load_group(kb0);
+  if (!spec || v != 0) load_q(rowbase, kv);
 
   float m_run[QT], l_run[QT];
   f32x4_t o[QT][NDT];
@@ -223,9 +223,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     l_run[qt] += __shfl_xor(l_run[qt], 32, 64);
   }
 
-  // merge: every wave publishes (max, sum, O) of its keys; then each wave
-  // combines the four partials, in wave order, for its share of the output
-  // tiles and stores them
+  // merge: every wave publishes (max, sum, O) of its keys (a wave without keys
+  // publishes max = -inf, sum = 0, O = 0); then each wave combines the KW
+  // partials, in wave order, for its share of the output tiles and stores them
   float* s_m = reinterpret_cast<float*>(attn_smem);               // [KW][QT][16]
   float* s_l = s_m + KW * QT * 16;                                 // [KW][QT][16]
   f32x4_t* s_o = reinterpret_cast<f32x4_t*>(s_l + KW * QT * 16);   // [KW][QT][NDT][64]
@@ -239,7 +239,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int t = 0; t < NDT; ++t) s_o[((w * QT + qt) * NDT + t) * 64 + lane] = o[qt][t];
   }
   __syncthreads();
-#pragma unroll
   for (int it = w; it < QT * NDT; it += KW) {
     const int qt = it / NDT, t = it % NDT;
     const int qrow = q0 + 16 * qt + n;
@@ -266,42 +265,51 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
-template <int NDT>
+template <int NDT, int QT>
 constexpr int attn_lds_bytes() {
-  return 4 * 2 * 16 * 4 * 2 + 4 * 2 * NDT * 64 * 16;  // m and l, then O, for KW = 4 and QT = 2
+  return kAttnWaves * QT * 16 * 4 * 2 + kAttnWaves * QT * NDT * 64 * 16;  // m and l, then O
 }
 
-template <class T, int NDC, int NDT, int GB>
+template <class T, int NDC, int NDT, int GB, int QT>
 static void launch_g(const AttnArgs& a, dim3 grid, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, GB>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, attn_lds_bytes<NDT>()) == hipSuccess;
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, GB, QT>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, attn_lds_bytes<NDT, QT>()) == hipSuccess;
   }
-  (void)launch_k((attn_kernel<T, NDC, NDT, GB>), grid, dim3(256), (size_t)attn_lds_bytes<NDT>(), s, a);
+  (void)launch_k((attn_kernel<T, NDC, NDT, GB, QT>), grid, dim3(kAttnWaves * 64), (size_t)attn_lds_bytes<NDT, QT>(),
+                 s, a);
 }
 
-template <class T, int NDC, int NDT>
+template <class T, int NDC, int NDT, int QT>
 static void launch_t(const AttnArgs& a, dim3 grid, hipStream_t s) {
   // two key blocks in flight per wave where the registers allow
-  if constexpr (NDT <= 6) launch_g<T, NDC, NDT, 2>(a, grid, s);
-  else launch_g<T, NDC, NDT, 1>(a, grid, s);
+  constexpr int kGB = NDT <= (sizeof(T) == 2 ? 6 : 4) ? 2 : 1;
+  launch_g<T, NDC, NDT, kGB, QT>(a, grid, s);
 }
 
-template <class T>
+template <class T, int QT>
 static void launch_dh(const AttnArgs& a, dim3 grid, hipStream_t s) {
   const int dh = a.sh.dh;
-  if (dh <= 32) launch_t<T, 1, 2>(a, grid, s);
-  else if (dh <= 64) launch_t<T, 2, 4>(a, grid, s);
-  else if (dh <= 96) launch_t<T, 3, 6>(a, grid, s);
-  else launch_t<T, 4, 8>(a, grid, s);
+  if (dh <= 32) launch_t<T, 1, 2, QT>(a, grid, s);
+  else if (dh <= 64) launch_t<T, 2, 4, QT>(a, grid, s);
+  else if (dh <= 96) launch_t<T, 3, 6, QT>(a, grid, s);
+  else launch_t<T, 4, 8, QT>(a, grid, s);
 }
 
-hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, hipStream_t s) {
-  dim3 grid((max_rows_per_view + 31) / 32, a.sh.H, a.B);
+// qtiles: 16-query tiles per workgroup (1 or 2).  One tile per workgroup
+// doubles the workgroups (and the K/V reads) for short per-stream row counts;
+// two halve the K/V traffic when there are many rows.
+hipError_t launch_attn(const AttnArgs& a0, int max_rows_per_view, int qtiles, hipStream_t s) {
+  AttnArgs a = a0;
+  if (!a.sh.dtype) qtiles = 1;
+  const int qrows = 16 * qtiles;
+  dim3 grid((max_rows_per_view + qrows - 1) / qrows, a.sh.H, a.B);
   if (grid.x == 0) return hipSuccess;
-  if (a.sh.dtype) launch_dh<uint16_t>(a, grid, s);
-  else launch_dh<float>(a, grid, s);
+  a.nspec = qtiles == 1 ? 2 : 1;
+  if (!a.sh.dtype) launch_dh<float, 1>(a, grid, s);  // fp32 operands: one tile (registers)
+  else if (qtiles == 1) launch_dh<uint16_t, 1>(a, grid, s);
+  else launch_dh<uint16_t, 2>(a, grid, s);
   return hipGetLastError();
 }
 

@@ -1,13 +1,11 @@
-// Row kernels that finish the split-K projections of a layer (paper §III-B:
-// the residual additions around the attention output and the MLP, and the
-// LayerNorm that opens the next sublayer), one workgroup per compact row:
+// Row kernel that finishes the split-K MLP down projection of a layer (paper
+// §III-B: the residual addition after the MLP, and the LayerNorm that opens
+// the next layer), one workgroup per compact row:
 //
-//   RES_LN2: H  = Z_l + ((P_0 + P_1 + ...) + b_o)          (fp32)
-//            A2 = S(LN2(H))                                 (input of fc1)
-//   RES_LN1: Z' = S(H + ((P_0 + P_1 + ...) + b_2))          (X^{l+1} rows)
-//            A1 = S(LN1 of the next layer (Z'))             (input of QKV)
-//            or, after the last layer, Y = S(LN_f(Z')) into the cache and the
-//            caller's `refreshed` rows.
+//   Z' = S(H + ((P_0 + P_1 + ...) + b_2))          (X^{l+1} rows)
+//   A1 = S(LN1 of the next layer (Z'))             (input of QKV)
+//   or, after the last layer, Y = S(LN_f(Z')) into the cache and the caller's
+//   `refreshed` rows.
 //
 // The partial sums are added in split order, then the bias, then the residual,
 // which is the order the unsplit product would use.  LayerNorm: two passes
@@ -23,18 +21,10 @@ namespace {
 
 __device__ __forceinline__ float4 ld4(const float* p, int q) { return reinterpret_cast<const float4*>(p)[q]; }
 
-// 4 consecutive storage elements as floats
-__device__ __forceinline__ float4 ld4s(const float* p, int q) { return ld4(p, q); }
-__device__ __forceinline__ float4 ld4s(const uint16_t* p, int q) {
-  const uint2 u = reinterpret_cast<const uint2*>(p)[q];
-  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
-                     __uint_as_float(u.y & 0xffff0000u));
-}
-
 __device__ __forceinline__ void st4(float* p, int q, float4 v) { reinterpret_cast<float4*>(p)[q] = v; }
 __device__ __forceinline__ void st4(uint16_t* p, int q, float4 v) {
-  const uint32_t lo = (uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16);
-  const uint32_t hi = (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16);
+  const uint32_t lo = f2bf2(v.x, v.y);
+  const uint32_t hi = f2bf2(v.z, v.w);
   reinterpret_cast<uint2*>(p)[q] = make_uint2(lo, hi);
 }
 
@@ -61,7 +51,7 @@ __device__ __forceinline__ float block_sum4(float x, float* s) {
 
 // One 256-thread workgroup per compact row r; thread t owns the float4 slots
 // q = t + 256 j, j < KP (D <= 1024 * KP).  S: K splits.
-template <class T, int MODE, int S, int KP>
+template <class T, int S, int KP>
 __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
   __shared__ float s_red[4];
   const int tid = threadIdx.x, r = blockIdx.x;
@@ -77,10 +67,7 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     const int q = min(tid + 256 * j, D4 - 1);
 #pragma unroll
     for (int s = 0; s < S; ++s) p[s][j] = ld4(a.part + ((size_t)s * a.mpad + r) * D, q);
-    if constexpr (MODE == RES_LN2)
-      res[j] = ld4s(static_cast<const T*>(a.res) + (size_t)r * D, q);
-    else
-      res[j] = ld4(static_cast<const float*>(a.res) + (size_t)r * D, q);
+    res[j] = ld4(a.res + frag_off(r, 4 * q, D / 32), 0);  // H is in operand order
     bias[j] = ld4(a.bias, q);
     gam[j] = ld4(a.ln_g, q);
     bet[j] = ld4(a.ln_b, q);
@@ -96,8 +83,7 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
 #pragma unroll
     for (int s = 1; s < S; ++s) x = add4(x, p[s][j]);
     x = add4(x, bias[j]);
-    v[j] = add4(res[j], x);
-    if constexpr (MODE == RES_LN1) v[j] = rnd4(v[j], static_cast<T*>(nullptr));
+    v[j] = rnd4(add4(res[j], x), static_cast<T*>(nullptr));
     if (tid + 256 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
   }
   const float mean = block_sum4(sum, s_red) / (float)D;
@@ -111,16 +97,13 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
   }
   const float rstd = 1.0f / sqrtf(block_sum4(sq, s_red) / (float)D + a.sh.eps);
 
-  T* xrow = nullptr;
+  T* xrow = x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok);
   T* yrow = nullptr;
   T* outrow = nullptr;
-  if constexpr (MODE == RES_LN1) {
-    xrow = x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok);
-    if (a.last) {
-      yrow = reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D;
-      if (a.refreshed)
-        outrow = static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + (r - a.meta->off[ri.view])) * D;
-    }
+  if (a.last) {
+    yrow = reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D;
+    if (a.refreshed)
+      outrow = static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + (r - a.meta->off[ri.view])) * D;
   }
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
@@ -132,18 +115,13 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
                                     (v[j].w - mean) * rstd * gam[j].w + bet[j].w);
       // the normalised row goes out in operand order (frag_off), 4 columns at a time
       T* arow = static_cast<T*>(a.a_out) + frag_off(r, 4 * q, D / 32);
-      if constexpr (MODE == RES_LN2) {
-        st4(a.h_out + (size_t)r * D, q, v[j]);
-        st4(arow, 0, n4);
+      st4(static_cast<T*>(a.z_out) + (size_t)r * D, q, v[j]);
+      st4(xrow, q, v[j]);
+      if (a.last) {
+        st4(yrow, q, n4);
+        if (outrow) st4(outrow, q, n4);
       } else {
-        st4(static_cast<T*>(a.z_out) + (size_t)r * D, q, v[j]);
-        st4(xrow, q, v[j]);
-        if (a.last) {
-          st4(yrow, q, n4);
-          if (outrow) st4(outrow, q, n4);
-        } else {
-          st4(arow, 0, n4);
-        }
+        st4(arow, 0, n4);
       }
     }
   }
@@ -151,30 +129,28 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
 
 namespace {
 
-template <class T, int MODE, int S>
+template <class T, int S>
 hipError_t launch_s(const ResArgs& a, dim3 grid, hipStream_t s) {
-  if (a.sh.D <= 1024) return launch_k(res_kernel<T, MODE, S, 1>, grid, dim3(256), 0, s, a);
-  return launch_k(res_kernel<T, MODE, S, 2>, grid, dim3(256), 0, s, a);
+  if (a.sh.D <= 1024) return launch_k(res_kernel<T, S, 1>, grid, dim3(256), 0, s, a);
+  return launch_k(res_kernel<T, S, 2>, grid, dim3(256), 0, s, a);
 }
 
-template <class T, int MODE>
-hipError_t launch_mode(const ResArgs& a, dim3 grid, hipStream_t s) {
+template <class T>
+hipError_t launch_t(const ResArgs& a, dim3 grid, hipStream_t s) {
   switch (a.ksplit) {
-    case 1: return launch_s<T, MODE, 1>(a, grid, s);
-    case 2: return launch_s<T, MODE, 2>(a, grid, s);
-    case 3: return launch_s<T, MODE, 3>(a, grid, s);
-    case 4: return launch_s<T, MODE, 4>(a, grid, s);
+    case 1: return launch_s<T, 1>(a, grid, s);
+    case 2: return launch_s<T, 2>(a, grid, s);
+    case 3: return launch_s<T, 3>(a, grid, s);
+    case 4: return launch_s<T, 4>(a, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 }  // namespace
 
-hipError_t launch_res(int mode, const ResArgs& a, int mmax, hipStream_t s) {
+hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s) {
   const dim3 grid(max(1, mmax));
-  if (a.sh.dtype)
-    return mode == RES_LN2 ? launch_mode<uint16_t, RES_LN2>(a, grid, s) : launch_mode<uint16_t, RES_LN1>(a, grid, s);
-  return mode == RES_LN2 ? launch_mode<float, RES_LN2>(a, grid, s) : launch_mode<float, RES_LN1>(a, grid, s);
+  return a.sh.dtype ? launch_t<uint16_t>(a, grid, s) : launch_t<float>(a, grid, s);
 }
 
 }  // namespace incvit

@@ -185,8 +185,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
 // 4 consecutive elements (already representable in T) to storage
 __device__ __forceinline__ void store4v(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
 __device__ __forceinline__ void store4v(uint16_t* p, float4 v) {
-  *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f2bf(v.x) | ((uint32_t)f2bf(v.y) << 16),
-                                            (uint32_t)f2bf(v.z) | ((uint32_t)f2bf(v.w) << 16));
+  *reinterpret_cast<uint2*>(p) = make_uint2(f2bf2(v.x, v.y), f2bf2(v.z, v.w));
 }
 
 // One workgroup per compact row r: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]),

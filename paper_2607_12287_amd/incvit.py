@@ -20,7 +20,7 @@ INCVIT_OK, INCVIT_ERR_ARG, INCVIT_ERR_SHAPE, INCVIT_ERR_UNSUPPORTED, INCVIT_ERR_
 STATUS_NAMES = {0: "INCVIT_OK", -1: "INCVIT_ERR_ARG", -2: "INCVIT_ERR_SHAPE", -3: "INCVIT_ERR_UNSUPPORTED",
                 -4: "INCVIT_ERR_STATE", -5: "INCVIT_ERR_HIP"}
 INCVIT_F32, INCVIT_BF16 = 0, 1
-KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "res_ln2", "fc1", "fc2", "res_ln1")
+KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "fc1", "fc2", "res_ln1")
 
 # Exported symbols, as declared in include/incvit.h.
 EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "incvit_pack_weights",
@@ -39,7 +39,7 @@ class incvit_config(ctypes.Structure):
 
 
 class incvit_tuning(ctypes.Structure):
-    _fields_ = [("cols", ctypes.c_int32 * 4)]
+    _fields_ = [("cols", ctypes.c_int32 * 4), ("attn_qtiles", ctypes.c_int32)]
 
 
 class IncvitError(RuntimeError):
@@ -198,10 +198,10 @@ def incvit_graph_destroy(g) -> None:
     lib().incvit_graph_destroy(g)
 
 
-def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None) -> int:
-    if cols is None:
+def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None, attn_qtiles: int = 0) -> int:
+    if cols is None and not attn_qtiles:
         return lib().incvit_set_tuning(h, None)
-    t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in cols]))
+    t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in (cols or (0, 0, 0, 0))]), int(attn_qtiles))
     return lib().incvit_set_tuning(h, ctypes.byref(t))
 
 
