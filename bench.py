@@ -96,13 +96,13 @@ def kernel_bytes(m, M: float, kind: str):
     if kind == "qkv":
         return 3 * D * D * eb + M * D * eb + 3 * M * D * eb
     if kind == "oproj":
-        return D * D * eb + 2 * M * D * eb + M * D * 4 + st
+        return D * D * eb + 3 * M * D * eb + st
     if kind == "fc1":
-        return D * F * eb + M * D * 4 + st + M * F * eb
+        return D * F * eb + M * D * eb + st + M * F * eb
     if kind == "fc2":
         return F * D * eb + M * F * eb + s2 * M * D * 4
     if kind == "res_ln1":
-        return s2 * M * D * 4 + M * D * 4 + 3 * M * D * eb
+        return s2 * M * D * 4 + 4 * M * D * eb
     if kind == "attn":
         return 2 * M * D * eb  # + K/V of the streams, added by the caller
     return None

@@ -26,11 +26,14 @@ in the paper; they are the readings this build takes.
 
 Arithmetic: everything is float64 except the patch embedding and the cosine,
 which follow a fixed fp32 order (``pinned.c``) so that the selection is
-reproducible bit for bit.  ``S(.)`` rounds to the storage precision (bf16 with
+reproducible bit for bit. ``S(.)`` rounds to the storage precision (bf16 with
 ties to even, fp32, or nothing for the "f64" mode used by the pins) at the
-points where a stored or GEMM-operand value is formed: Q/K/V, the LN outputs
-fed to a GEMM, the attention output, the GELU output, each layer's output rows,
-the final output and the layer-0 input rows.  The residual H stays unrounded.
+points where a value between two operations is formed, as a half-precision
+inference pipeline stores every tensor between its operations (the paper runs
+its encoder in FP16 under PyTorch, Appendix A, hardware table): Q/K/V, the LN
+outputs fed to a GEMM, the attention output, the residual H after the
+attention, the GELU output, each layer's output rows, the final output and the
+layer-0 input rows.
 
 Parity: pinned (see tests/test_oracle_*.py) by library routines (torch fp64
 functional ops), closed forms, brute-force selection, and the invariants the
@@ -189,7 +192,7 @@ def layer_rows(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray
     K[U] = k
     V[U] = v
     O = S(attention(q, K, V, m.heads), dt)
-    Hres = Z + (O @ model.p(l, "w_o") + model.p(l, "b_o"))
+    Hres = S(Z + (O @ model.p(l, "w_o") + model.p(l, "b_o")), dt)
     if trace is not None:
         trace.setdefault("O", []).append(O)
         trace.setdefault("H", []).append(Hres)

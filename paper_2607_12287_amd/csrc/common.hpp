@@ -150,18 +150,18 @@ struct GemmArgs {
   CacheLayout cl;
   Shape sh;
   int layer;
-  const void* A;      // compact A rows in operand order: QKV A1, RES O, FC1 H (fp32), PART G
+  const void* A;      // compact A rows in operand order: QKV A1, RES O, FC1 H, PART G
   int lda;
   const void* W;      // packed [Nout/16][kchunks][512]
   const float* bias;  // [Nout] (not used by PART)
   int kchunks, Nout;
-  void* out;          // QKV Q [Mpad][D]; RES H (fp32, operand order); FC1 G; PART f32 [ksplit][mpad][ldo]
+  void* out;          // QKV Q [Mpad][D]; RES H (operand order); FC1 G; PART f32 [ksplit][mpad][ldo]
   int ldo;
   int ksplit;         // K is split over gridDim.y = ksplit workgroups (PART)
   int mpad;           // padded rows (partial slices, statistics)
   const void* resid;  // RES: Z_l rows [Mpad][D] (storage type)
   float2* stats;      // RES writes, FC1 reads: (mean, sum of squared deviations) of H per
-                      // 16-column block and row, [D/16][mpad]
+                      // row and 16-column block, [mpad][D/16]
   const float* ln_g;  // FC1: LN2 gamma, beta [D]
   const float* ln_b;
 };
@@ -179,7 +179,7 @@ struct ResArgs {
   int last;           // RES_LN1 after the last layer: final LayerNorm
   const float* part;  // [ksplit][mpad][D]
   int ksplit, mpad;
-  const float* res;   // H (fp32, operand order)
+  const void* res;    // H (storage type, operand order)
   const float* bias;
   const float* ln_g;  // the LayerNorm applied to the new rows
   const float* ln_b;

@@ -4,16 +4,16 @@
 //   QKV : [Q K V] = S(A1 W_qkv + b), A1 = S(LN1(Z_l)) already normalised by the
 //         row kernel that produced Z_l; Q -> workspace, K and V rows scattered
 //         into the cached K^l, V^l of each stream (eq. 5);
-//   RES : the output projection with its residual, H = Z_l + (O W_o + b_o)
-//         (fp32), plus LayerNorm partial statistics of H over each 16-column
-//         block (mean and sum of squared deviations);
+//   RES : the output projection with its residual, H = S(Z_l + (O W_o + b_o)),
+//         plus LayerNorm partial statistics of H over each 16-column block
+//         (mean and sum of squared deviations);
 //   FC1 : G = S(GELU(A2 W_1 + b_1)) with A2 = S(LN2(H)) formed while the
 //         operand is loaded: the block statistics of H are merged in a fixed
 //         order into the row mean and variance first;
 //   PART: raw partial sums of A W over one share of K (the MLP down
 //         projection); a row kernel adds the bias, the residual and the next
 //         LayerNorm.
-// A1, O, G and H are kept in MFMA operand order (frag_off; H in fp32).
+// A1, O, G and H are kept in MFMA operand order (frag_off).
 //
 // With M a few dozen rows these are weight-streaming problems whose time is set
 // by memory latency, so a workgroup issues every load it needs for its first
@@ -29,6 +29,8 @@
 // waves' partial tiles are summed in wave order through LDS and the epilogue
 // is spread over the first 8 waves.  No atomics: results are deterministic.
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace incvit {
@@ -81,23 +83,28 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
 }
 
-// Chan et al.'s pairwise update of (count, mean, sum of squared deviations).
-struct Moments {
-  float n, mean, m2;
-};
-__device__ __forceinline__ Moments merge_moments(const Moments& a, const Moments& b) {
-  if (b.n == 0.0f) return a;
-  if (a.n == 0.0f) return b;
-  const float n = a.n + b.n;
-  const float d = b.mean - a.mean;
-  return Moments{n, a.mean + d * (b.n / n), a.m2 + b.m2 + d * d * (a.n * (b.n / n))};
+// Row statistics from the 16-column block statistics (block mean m_b, sum of
+// squared deviations q_b; every block has 16 columns): mean = sum_b m_b / nblk,
+// M2 = sum_b (q_b + 16 (m_b - mean)^2).  Lane `part` of a row's 16 lanes sums
+// blocks part, part + 16, ... in order, then the lanes are combined by a fixed
+// butterfly.
+__device__ __forceinline__ float sum16(float x) {
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) x += __shfl_xor(x, off, 64);
+  return x;
 }
 
-// A2 operand from 8 fp32 values of H: S(((h - mean) * rstd) * gamma + beta),
+// A2 operand from 8 values of H: S(((h - mean) * rstd) * gamma + beta),
 // evaluated as fma(fma(h, rstd, -mean * rstd), gamma, beta) (nm = -mean * rstd)
-__device__ __forceinline__ void ln_operand(V8<uint16_t>& out, const V8<float>& h, float rstd, float nm,
+__device__ __forceinline__ void ln_operand(V8<uint16_t>& out, const V8<uint16_t>& h, float rstd, float nm,
                                            const V8<float>& gm, const V8<float>& bt) {
-  const float x[8] = {h.a.x, h.a.y, h.a.z, h.a.w, h.b.x, h.b.y, h.b.z, h.b.w};
+  const uint32_t hq[4] = {h.v.x, h.v.y, h.v.z, h.v.w};
+  float x[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(hq[e] << 16);
+    x[2 * e + 1] = __uint_as_float(hq[e] & 0xffff0000u);
+  }
   const float g8[8] = {gm.a.x, gm.a.y, gm.a.z, gm.a.w, gm.b.x, gm.b.y, gm.b.z, gm.b.w};
   const float b8[8] = {bt.a.x, bt.a.y, bt.a.z, bt.a.w, bt.b.x, bt.b.y, bt.b.z, bt.b.w};
   uint32_t q[4];
@@ -149,14 +156,14 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   // operand loads are buffer loads: one lane offset for all of them, the
   // chunk's position as a wave-uniform offset.  A is stored in operand order
   // (frag_off): row tile t, chunk kc is the kilobyte (t * akc + kc) (bf16;
-  // two kilobytes for fp32).  FC1 reads H (fp32), normalised below with
-  // gamma/beta staged in LDS.
+  // two kilobytes for fp32).  FC1 reads H, normalised below with gamma/beta
+  // staged in LDS.
   const int akc = a.lda / 32;
-  constexpr uint32_t kAeb = EPI == EPI_FC1 ? 4 : sizeof(T);
+  constexpr uint32_t kAeb = sizeof(T);
   const Rsrc rA = make_rsrc(a.A, (uint32_t)a.mpad * a.lda * kAeb);
   const Rsrc rW = make_rsrc(a.W, (uint32_t)(a.Nout / 16) * a.kchunks * kChunkElems * sizeof(T));
   const uint32_t voffA = lane * 8 * kAeb, voffW = lane * 8 * sizeof(T);
-  V8<float> hf[EPI == EPI_FC1 ? CPW : 1][2];
+  V8<T> hf[EPI == EPI_FC1 ? CPW : 1][2];
   auto load_a = [&](int m0, int round) {
 #pragma unroll
     for (int c = 0; c < CPW; ++c) {
@@ -176,9 +183,9 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       for (int b = 0; b < NB; ++b)
         wb[c][b].bload(rW, voffW, (uint32_t)((cb0 + b) * a.kchunks + kc_of(round, c)) * kChunkElems * sizeof(T));
   };
-  // FC1: block statistics of the rows of this block; thread t < 512 merges
-  // blocks part, part + 16, ... of row t / 16 (blocks past the last read zero
-  // and are not merged)
+  // FC1: block statistics of the rows of this block ([row][block]); thread
+  // t < 512 merges blocks part, part + 16, ... of row t / 16 (blocks past the
+  // last are not merged; those past the buffer read zero)
   const int st_row = (tid >> 4) & (kGemmRB - 1), st_part = tid & (kStatParts - 1);
   const int nblk = D / 16;
   float2 sv[EPI == EPI_FC1 ? kStatMax : 1];
@@ -186,8 +193,8 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   auto load_stats = [&](int m0) {
 #pragma unroll
     for (int i = 0; i < kStatMax; ++i) {
-      const auto v = __builtin_amdgcn_raw_buffer_load_b64(rS, (uint32_t)(st_part * a.mpad + st_row) * 8,
-                                                          (uint32_t)(kStatParts * i * a.mpad + m0) * 8, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(rS, (uint32_t)(st_row * nblk + st_part) * 8,
+                                                          (uint32_t)(m0 * nblk + kStatParts * i) * 8, 0);
       sv[i] = make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
     }
   };
@@ -234,13 +241,12 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   if constexpr (EPI == EPI_QKV) rinfo = a.rows[16 * re + 4 * g + ie];
   if constexpr (EPI == EPI_RES) load_res(0);
 
-  // The first row block runs whatever M is (with M = 0 it stores nothing), so
-  // the loads above are never held back behind the read of M.
-  int m0 = 0;
-  do {
-    if (m0 > 0) {
-      // the same issue order as the first block (statistics first), so that
-      // the waits at the join count the same loads
+  // One 32-row block.  The first block is a copy of its own (FIRST), which
+  // runs whatever M is (with M = 0 it stores nothing), so the loads above are
+  // never held back behind the read of M, and its waits count exactly the
+  // loads issued above instead of the fewer a later block reloads.
+  auto row_block = [&](const int m0, auto first) {
+    if constexpr (!decltype(first)::value) {
       if constexpr (EPI == EPI_FC1) load_stats(m0);
       load_a(m0, 0);
       if (rounds > 1) load_w(0);
@@ -252,16 +258,19 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       // row statistics: a fixed merge order over the 16-column blocks (the
       // first 8 waves; a scalar branch)
       if (w < kGemmRB * kStatParts / 64) {
-        Moments mo{0.0f, 0.0f, 0.0f};
+        float s1 = 0.0f;
 #pragma unroll
         for (int i = 0; i < kStatMax; ++i)
-          if (st_part + kStatParts * i < nblk) mo = merge_moments(mo, Moments{16.0f, sv[i].x, sv[i].y});
+          if (st_part + kStatParts * i < nblk) s1 += sv[i].x;
+        const float mean = sum16(s1) / (float)nblk;
+        float s2 = 0.0f;
 #pragma unroll
-        for (int off = 1; off < kStatParts; off <<= 1) {
-          const Moments o{__shfl_xor(mo.n, off, 64), __shfl_xor(mo.mean, off, 64), __shfl_xor(mo.m2, off, 64)};
-          mo = (st_part & off) ? merge_moments(o, mo) : merge_moments(mo, o);
+        for (int i = 0; i < kStatMax; ++i) {
+          const float d = sv[i].x - mean;
+          if (st_part + kStatParts * i < nblk) s2 += sv[i].y + 16.0f * (d * d);
         }
-        if (st_part == 0) s_st[st_row] = make_float2(mo.mean, 1.0f / sqrtf(mo.m2 / (float)D + a.sh.eps));
+        const float m2 = sum16(s2);
+        if (st_part == 0) s_st[st_row] = make_float2(mean, 1.0f / sqrtf(m2 / (float)D + a.sh.eps));
       }
       lds_barrier();
 #pragma unroll
@@ -325,8 +334,8 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       if constexpr (EPI == EPI_PART) {
         if (ok) static_cast<float*>(a.out)[((size_t)blockIdx.y * a.mpad + row) * a.ldo + col] = x;
       } else if constexpr (EPI == EPI_RES) {
-        // H = Z + (O W_o + b_o), and the moments of this row's 16 columns
-        const float hv = resv[b] + (x + biasv[b]);
+        // H = S(Z + (O W_o + b_o)), and the moments of this row's 16 columns
+        const float hv = Elem<T>::rnd(resv[b] + (x + biasv[b]));
         float s = hv;
 #pragma unroll
         for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off, 64);
@@ -335,8 +344,8 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
 #pragma unroll
         for (int off = 1; off < 16; off <<= 1) q += __shfl_xor(q, off, 64);
         if (ok) {
-          static_cast<float*>(a.out)[frag_off(row, col, a.ldo / 32)] = hv;
-          if (n == 0) a.stats[(size_t)(cb0 + b) * a.mpad + row] = make_float2(bm, q);
+          static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(hv);
+          if (n == 0) a.stats[(size_t)row * (D / 16) + cb0 + b] = make_float2(bm, q);
         }
       } else if constexpr (EPI == EPI_QKV) {
         x += biasv[b];
@@ -358,8 +367,9 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       }
     }
     __syncthreads();  // red and the row statistics are reused by the next row block
-    m0 += kGemmRB;
-  } while (m0 < M);
+  };
+  row_block(0, std::true_type{});
+  for (int m0 = kGemmRB; m0 < M; m0 += kGemmRB) row_block(m0, std::false_type{});
 }
 
 template <class T, int EPI, int NB, int CPW>

@@ -231,7 +231,7 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.a = take((size_t)w.Mpad * sh.D * sh.eb);
   w.q = take((size_t)w.Mpad * sh.D * sh.eb);
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
-  w.h = take((size_t)w.Mpad * sh.D * 4);
+  w.h = take((size_t)w.Mpad * sh.D * sh.eb);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
   w.part = take((size_t)gemm_geom(sh, G_FC2).ksplit * w.Mpad * sh.D * 4);
   w.stats = take((size_t)(sh.D / 16) * w.Mpad * 8);
@@ -388,7 +388,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       r.ksplit = g.ksplit;
       r.mpad = wl.Mpad;
       r.N = sh.N;
-      r.res = reinterpret_cast<const float*>(ws + wl.h);
+      r.res = ws + wl.h;
       r.bias = fptr(h, P.b_2);
       r.z_out = ws + wl.z;
       r.last = l + 1 == sh.L;

@@ -21,6 +21,14 @@ namespace {
 
 __device__ __forceinline__ float4 ld4(const float* p, int q) { return reinterpret_cast<const float4*>(p)[q]; }
 
+// 4 consecutive storage elements as floats
+__device__ __forceinline__ float4 ld4s(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4s(const uint16_t* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+
 __device__ __forceinline__ void st4(float* p, int q, float4 v) { reinterpret_cast<float4*>(p)[q] = v; }
 __device__ __forceinline__ void st4(uint16_t* p, int q, float4 v) {
   const uint32_t lo = f2bf2(v.x, v.y);
@@ -67,7 +75,7 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     const int q = min(tid + 256 * j, D4 - 1);
 #pragma unroll
     for (int s = 0; s < S; ++s) p[s][j] = ld4(a.part + ((size_t)s * a.mpad + r) * D, q);
-    res[j] = ld4(a.res + frag_off(r, 4 * q, D / 32), 0);  // H is in operand order
+    res[j] = ld4s(static_cast<const T*>(a.res) + frag_off(r, 4 * q, D / 32));  // H is in operand order
     bias[j] = ld4(a.bias, q);
     gam[j] = ld4(a.ln_g, q);
     bet[j] = ld4(a.ln_b, q);

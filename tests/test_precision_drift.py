@@ -39,7 +39,7 @@ def _encode_fp32_gemms(model, t0):
         A = S(vit.layer_norm(Z, p("ln1_g"), p("ln1_b"), m.ln_eps))
         qkv = S(mm(A, p("w_qkv")) + p("b_qkv"))
         O = S(vit.attention(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], H))
-        Hr = Z + (mm(O, p("w_o")) + p("b_o"))
+        Hr = S(Z + (mm(O, p("w_o")) + p("b_o")))
         A2 = S(vit.layer_norm(Hr, p("ln2_g"), p("ln2_b"), m.ln_eps))
         G = S(vit.gelu_tanh(mm(A2, p("w_1")) + p("b_1")))
         Z = S(Hr + (mm(G, p("w_2")) + p("b_2")))
