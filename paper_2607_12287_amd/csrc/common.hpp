@@ -126,7 +126,7 @@ struct SelectArgs {
   int* count;  // [B]
 };
 
-struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map, A1 of layer 0
+struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map
   RowMap rm;
   RowInfo* rows;     // commit writes
   Meta* meta;        // commit writes
@@ -134,12 +134,9 @@ struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map, A1 of la
   CacheLayout cl;
   Shape sh;
   const float* t0;
-  const float* g;    // LN1 of layer 0
-  const float* b;
   int init_header;   // commit of a full encode: write header
   uint32_t hash;
-  void* z;           // compact Z_0 [Mpad][D]
-  void* a;           // compact S(LN1(Z_0)) [Mpad][D]
+  void* z;           // compact Z_0 [Mpad][D] (operand order)
 };
 
 enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3 };
@@ -150,7 +147,7 @@ struct GemmArgs {
   CacheLayout cl;
   Shape sh;
   int layer;
-  const void* A;      // compact A rows in operand order: QKV A1, RES O, FC1 H, PART G
+  const void* A;      // compact A rows in operand order: QKV Z_l, RES O, FC1 H, PART G
   int lda;
   const void* W;      // packed [Nout/16][kchunks][512]
   const float* bias;  // [Nout] (not used by PART)
@@ -159,32 +156,29 @@ struct GemmArgs {
   int ldo;
   int ksplit;         // K is split over gridDim.y = ksplit workgroups (PART)
   int mpad;           // padded rows (partial slices, statistics)
-  const void* resid;  // RES: Z_l rows [Mpad][D] (storage type)
-  float2* stats;      // RES writes, FC1 reads: (mean, sum of squared deviations) of H per
-                      // row and 16-column block, [mpad][D/16]
-  const float* ln_g;  // FC1: LN2 gamma, beta [D]
-  const float* ln_b;
+  const void* resid;  // RES: Z_l rows (operand order)
+  const float* c1;    // QKV, FC1: column sums of the LayerNorm-folded weights; `bias`
+                      // then holds beta^T W + b (see FoldArgs)
 };
 
 // Row kernel that finishes the split-K MLP down projection, one workgroup per
-// compact row: Z_{l+1} = S(H + (partials + b_2)) -> compact Z and X^{l+1} of
-// the cache, then A1 = S(LN1 of layer l+1 (Z_{l+1})), or after the last layer
-// Y = S(LN_f(Z_L)) into the cache and the refreshed output.
+// compact row: Z_{l+1} = S(H + (partials + b_2)) -> compact Z (operand order)
+// and X^{l+1} of the cache; after the last layer also Y = S(LN_f(Z_L)) into
+// the cache and the refreshed output.
 struct ResArgs {
   const Meta* meta;
   const RowInfo* rows;
   CacheLayout cl;
   Shape sh;
   int layer;
-  int last;           // RES_LN1 after the last layer: final LayerNorm
+  int last;           // after the last layer: final LayerNorm
   const float* part;  // [ksplit][mpad][D]
   int ksplit, mpad;
   const void* res;    // H (storage type, operand order)
   const float* bias;
-  const float* ln_g;  // the LayerNorm applied to the new rows
+  const float* ln_g;  // the final LayerNorm (last layer)
   const float* ln_b;
-  void* z_out;        // Z_{l+1}
-  void* a_out;        // normalised rows (not for the final LayerNorm)
+  void* z_out;        // Z_{l+1} (operand order)
   void* refreshed;    // final: optional [B][N][D]
   int N;
 };
@@ -206,6 +200,20 @@ struct AttnArgs {
 struct PackArgs {
   const void* src;  // canonical [K][Ncols] storage dtype
   void* dst;        // packed
+  int K, Ncols, kchunks, nblocks, dtype;
+};
+
+// Folding a LayerNorm (gamma, beta) into the packed weights W that follow it:
+// W' = S(gamma_k W[k][n]) in the packed layout, c1[n] = sum_k W'[k][n] and
+// c2b[n] = sum_k beta_k W[k][n] + b[n] (fp32, columns up to nblocks * 16).
+struct FoldArgs {
+  const void* src;    // canonical W [K][Ncols] storage dtype
+  const void* gamma;  // canonical [K] storage dtype
+  const void* beta;
+  const void* bias;   // canonical [Ncols] storage dtype
+  void* dst;          // packed W (written by pack_kernel first)
+  float* c1;
+  float* c2b;
   int K, Ncols, kchunks, nblocks, dtype;
 };
 
@@ -252,6 +260,7 @@ hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, int qtiles, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+hipError_t launch_fold(const FoldArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);
 hipError_t launch_export(const ExportArgs& a, hipStream_t s);
 

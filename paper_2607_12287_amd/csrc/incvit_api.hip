@@ -23,6 +23,9 @@ thread_local std::string g_error;
 
 struct PackedLayer {
   size_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o, ln2_g, ln2_b, w_1, b_1, w_2, b_2;
+  // LN1 folded into W_qkv and LN2 into W_1 (packed only): column sums of the
+  // folded weights and beta^T W + b
+  size_t qkv_c1, qkv_c2b, fc1_c1, fc1_c2b;
 };
 
 struct PackedLayout {
@@ -36,7 +39,7 @@ struct CanonLayout {  // element offsets into the canonical buffer
 };
 
 struct WsLayout {
-  size_t meta, rows, count, idx, sim, t0, z, a, q, o, h, g, part, stats, total;
+  size_t meta, rows, count, idx, sim, t0, z, q, o, h, g, part, total;
   int Mpad;
 };
 
@@ -104,6 +107,10 @@ PackedLayout packed_layout(const Shape& sh) {
     L.b_1 = take((size_t)sh.Fpad * 4);
     L.w_2 = take(packed_gemm_bytes(sh.Fpad, D, eb));
     L.b_2 = take(D * 4);
+    L.qkv_c1 = take(3 * D * 4);
+    L.qkv_c2b = take(3 * D * 4);
+    L.fc1_c1 = take((size_t)sh.Fpad * 4);
+    L.fc1_c2b = take((size_t)sh.Fpad * 4);
     p.layers.push_back(L);
   }
   p.lnf_g = take(D * 4);
@@ -228,13 +235,11 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.sim = take((size_t)M * 4);
   w.t0 = take((size_t)M * sh.D * 4);
   w.z = take((size_t)w.Mpad * sh.D * sh.eb);
-  w.a = take((size_t)w.Mpad * sh.D * sh.eb);
   w.q = take((size_t)w.Mpad * sh.D * sh.eb);
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
   w.h = take((size_t)w.Mpad * sh.D * sh.eb);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
   w.part = take((size_t)gemm_geom(sh, G_FC2).ksplit * w.Mpad * sh.D * 4);
-  w.stats = take((size_t)(sh.D / 16) * w.Mpad * 8);
   w.total = off;
   return w;
 }
@@ -346,8 +351,8 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       switch (kind) {
         case G_QKV:
           epi = EPI_QKV;
-          a.A = ws + wl.a; a.lda = sh.D;
-          a.W = h->packed + P.w_qkv; a.bias = fptr(h, P.b_qkv);
+          a.A = ws + wl.z; a.lda = sh.D;
+          a.W = h->packed + P.w_qkv; a.bias = fptr(h, P.qkv_c2b); a.c1 = fptr(h, P.qkv_c1);
           a.out = ws + wl.q; a.ldo = sh.D;
           break;
         case G_OPROJ:
@@ -356,14 +361,11 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
           a.resid = ws + wl.z;
           a.out = ws + wl.h; a.ldo = sh.D;
-          a.stats = reinterpret_cast<float2*>(ws + wl.stats);
           break;
         case G_FC1:
           epi = EPI_FC1;
           a.A = ws + wl.h; a.lda = sh.D;
-          a.W = h->packed + P.w_1; a.bias = fptr(h, P.b_1);
-          a.stats = reinterpret_cast<float2*>(ws + wl.stats);
-          a.ln_g = fptr(h, P.ln2_g); a.ln_b = fptr(h, P.ln2_b);
+          a.W = h->packed + P.w_1; a.bias = fptr(h, P.fc1_c2b); a.c1 = fptr(h, P.fc1_c1);
           a.out = ws + wl.g; a.ldo = sh.Fpad;
           break;
         default:
@@ -396,10 +398,6 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
         r.ln_g = fptr(h, h->pl.lnf_g);
         r.ln_b = fptr(h, h->pl.lnf_b);
         r.refreshed = refreshed;
-      } else {
-        r.ln_g = fptr(h, h->pl.layers[l + 1].ln1_g);
-        r.ln_b = fptr(h, h->pl.layers[l + 1].ln1_b);
-        r.a_out = ws + wl.a;
       }
       return run(h, kernel_kind, s, [&] { return launch_res(r, mmax, s); });
     };
@@ -495,6 +493,15 @@ incvit_status incvit_pack_weights(const incvit_config* cfg, const void* canonica
     PackArgs a{src + coff * eb, dst + poff, K, Ncols, round_up(Kpad, 32) / 32, round_up(Npadc, 16) / 16, sh.dtype};
     e = launch_pack(a, s);
   };
+  // the LayerNorm (gamma, beta) before a GEMM folded into its packed weights
+  auto fold = [&](size_t coff, size_t poff, size_t g, size_t b, size_t bias, size_t c1, size_t c2b, int K, int Ncols,
+                  int Npadc) {
+    if (e != hipSuccess) return;
+    FoldArgs a{src + coff * eb, src + g * eb, src + b * eb, src + bias * eb, dst + poff,
+               reinterpret_cast<float*>(dst + c1), reinterpret_cast<float*>(dst + c2b),
+               K, Ncols, round_up(K, 32) / 32, round_up(Npadc, 16) / 16, sh.dtype};
+    e = launch_fold(a, s);
+  };
   const int D = sh.D;
   e = hipMemcpyAsync(dst + pl.w_pe, src + cn.w_pe * eb, (size_t)sh.P * D * eb, hipMemcpyDeviceToDevice, s);
   conv(cn.b_pe, pl.b_pe, D, D);
@@ -505,12 +512,14 @@ incvit_status incvit_pack_weights(const incvit_config* cfg, const void* canonica
     conv(C.ln1_g, P.ln1_g, D, D);
     conv(C.ln1_b, P.ln1_b, D, D);
     pack(C.w_qkv, P.w_qkv, D, 3 * D, D, 3 * D);
+    fold(C.w_qkv, P.w_qkv, C.ln1_g, C.ln1_b, C.b_qkv, P.qkv_c1, P.qkv_c2b, D, 3 * D, 3 * D);
     conv(C.b_qkv, P.b_qkv, 3 * D, 3 * D);
     pack(C.w_o, P.w_o, D, D, D, D);
     conv(C.b_o, P.b_o, D, D);
     conv(C.ln2_g, P.ln2_g, D, D);
     conv(C.ln2_b, P.ln2_b, D, D);
     pack(C.w_1, P.w_1, D, sh.F, D, sh.Fpad);
+    fold(C.w_1, P.w_1, C.ln2_g, C.ln2_b, C.b_1, P.fc1_c1, P.fc1_c2b, D, sh.F, sh.Fpad);
     conv(C.b_1, P.b_1, sh.F, sh.Fpad);
     pack(C.w_2, P.w_2, sh.F, D, sh.Fpad, D);
     conv(C.b_2, P.b_2, D, D);
@@ -595,9 +604,6 @@ incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patch
   ra.init_header = 1;
   ra.hash = h->hash;
   ra.z = ws + wl.z;
-  ra.a = ws + wl.a;
-  ra.g = fptr(h, h->pl.layers[0].ln1_g);
-  ra.b = fptr(h, h->pl.layers[0].ln1_b);
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
   return run_layers(h, views, B, wl, ws, sh.N, mmax, false, nullptr, s);
 }
@@ -655,9 +661,6 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   ra.sh = sh;
   ra.t0 = t0;
   ra.z = ws + wl.z;
-  ra.a = ws + wl.a;
-  ra.g = fptr(h, h->pl.layers[0].ln1_g);
-  ra.b = fptr(h, h->pl.layers[0].ln1_b);
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
   return run_layers(h, views, B, wl, ws, max_rows, mmax, true, refreshed, s);
 }

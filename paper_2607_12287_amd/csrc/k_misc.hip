@@ -22,6 +22,33 @@ __global__ void pack_kernel(PackArgs a) {
   }
 }
 
+// One thread per packed column: the folded weights of the column (rounded to
+// the storage type), their sum, and beta^T W + b, both accumulated in fp64.
+template <class T>
+__global__ void fold_kernel(FoldArgs a) {
+  const int col = blockIdx.x * blockDim.x + threadIdx.x;
+  if (col >= a.nblocks * 16) return;
+  const T* src = static_cast<const T*>(a.src);
+  const T* gm = static_cast<const T*>(a.gamma);
+  const T* bt = static_cast<const T*>(a.beta);
+  T* dst = static_cast<T*>(a.dst);
+  double c1 = 0.0, c2 = 0.0;
+  if (col < a.Ncols) {
+    const int nb = col / 16, cl = col % 16;
+    for (int k = 0; k < a.K; ++k) {
+      const float w = Elem<T>::f(src[(size_t)k * a.Ncols + col]);
+      const float wf = Elem<T>::rnd(Elem<T>::f(gm[k]) * w);
+      const int kc = k / 32, kk = k % 32;
+      dst[(((size_t)nb * a.kchunks + kc) * 64 + 16 * (kk / 8) + cl) * 8 + kk % 8] = Elem<T>::cv(wf);
+      c1 += (double)wf;
+      c2 += (double)Elem<T>::f(bt[k]) * (double)w;
+    }
+    c2 += (double)Elem<T>::f(static_cast<const T*>(a.bias)[col]);
+  }
+  a.c1[col] = (float)c1;
+  a.c2b[col] = (float)c2;
+}
+
 __global__ void conv_kernel(ConvArgs a) {
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < a.npad; i += (long)gridDim.x * blockDim.x) {
     float x = 0.0f;
@@ -80,6 +107,13 @@ __global__ void export_kernel(ExportArgs a) {
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
   if (a.dtype) (void)launch_k(pack_kernel<uint16_t>, dim3(1024), dim3(256), 0, s, a);
   else (void)launch_k(pack_kernel<float>, dim3(1024), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fold(const FoldArgs& a, hipStream_t s) {
+  const dim3 grid((a.nblocks * 16 + 63) / 64);
+  if (a.dtype) (void)launch_k(fold_kernel<uint16_t>, grid, dim3(64), 0, s, a);
+  else (void)launch_k(fold_kernel<float>, grid, dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1,10 +1,9 @@
 // Row kernel that finishes the split-K MLP down projection of a layer (paper
-// §III-B: the residual addition after the MLP, and the LayerNorm that opens
-// the next layer), one workgroup per compact row:
+// §III-B: the residual addition after the MLP), one workgroup per compact row:
 //
-//   Z' = S(H + ((P_0 + P_1 + ...) + b_2))          (X^{l+1} rows)
-//   A1 = S(LN1 of the next layer (Z'))             (input of QKV)
-//   or, after the last layer, Y = S(LN_f(Z')) into the cache and the caller's
+//   Z' = S(H + ((P_0 + P_1 + ...) + b_2))   (X^{l+1} rows, and the next
+//                                           layer's input in operand order)
+//   after the last layer also Y = S(LN_f(Z')) into the cache and the caller's
 //   `refreshed` rows.
 //
 // The partial sums are added in split order, then the bias, then the residual,
@@ -77,12 +76,15 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     for (int s = 0; s < S; ++s) p[s][j] = ld4(a.part + ((size_t)s * a.mpad + r) * D, q);
     res[j] = ld4s(static_cast<const T*>(a.res) + frag_off(r, 4 * q, D / 32));  // H is in operand order
     bias[j] = ld4(a.bias, q);
-    gam[j] = ld4(a.ln_g, q);
-    bet[j] = ld4(a.ln_b, q);
+    gam[j] = bet[j] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (a.last) {  // uniform: the final LayerNorm's parameters
+      gam[j] = ld4(a.ln_g, q);
+      bet[j] = ld4(a.ln_b, q);
+    }
   }
   if (r >= M) return;  // uniform per workgroup
 
-  // the new row (H, or the rounded Z'), and its LayerNorm statistics
+  // the new row Z' and, after the last layer, its LayerNorm statistics
   float4 v[KP];
   float sum = 0.0f;
 #pragma unroll
@@ -94,6 +96,17 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     v[j] = rnd4(add4(res[j], x), static_cast<T*>(nullptr));
     if (tid + 256 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
   }
+  T* xrow = x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok);
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = tid + 256 * j;
+    if (q < D4) {
+      st4(static_cast<T*>(a.z_out) + frag_off(r, 4 * q, D / 32), 0, v[j]);
+      st4(xrow, q, v[j]);
+    }
+  }
+  if (!a.last) return;  // uniform
+
   const float mean = block_sum4(sum, s_red) / (float)D;
   float sq = 0.0f;
 #pragma unroll
@@ -104,15 +117,9 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     }
   }
   const float rstd = 1.0f / sqrtf(block_sum4(sq, s_red) / (float)D + a.sh.eps);
-
-  T* xrow = x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok);
-  T* yrow = nullptr;
-  T* outrow = nullptr;
-  if (a.last) {
-    yrow = reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D;
-    if (a.refreshed)
-      outrow = static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + (r - a.meta->off[ri.view])) * D;
-  }
+  T* yrow = reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D;
+  T* outrow = a.refreshed ? static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + (r - a.meta->off[ri.view])) * D
+                          : nullptr;
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     const int q = tid + 256 * j;
@@ -121,16 +128,8 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
                                     (v[j].y - mean) * rstd * gam[j].y + bet[j].y,
                                     (v[j].z - mean) * rstd * gam[j].z + bet[j].z,
                                     (v[j].w - mean) * rstd * gam[j].w + bet[j].w);
-      // the normalised row goes out in operand order (frag_off), 4 columns at a time
-      T* arow = static_cast<T*>(a.a_out) + frag_off(r, 4 * q, D / 32);
-      st4(static_cast<T*>(a.z_out) + (size_t)r * D, q, v[j]);
-      st4(xrow, q, v[j]);
-      if (a.last) {
-        st4(yrow, q, n4);
-        if (outrow) st4(outrow, q, n4);
-      } else {
-        st4(arow, 0, n4);
-      }
+      st4(yrow, q, n4);
+      if (outrow) st4(outrow, q, n4);
     }
   }
 }

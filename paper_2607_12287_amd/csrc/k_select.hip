@@ -189,24 +189,15 @@ __device__ __forceinline__ void store4v(uint16_t* p, float4 v) {
 }
 
 // One workgroup per compact row r: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]),
-// the compact Z0 row and the layer-0 QKV input S(LN1(Z0)), and the row's entry
-// in the row map.  Block 0 also publishes M and the per-stream row offsets.
+// the compact Z0 row (operand order, the layer-0 input), and the row's entry in
+// the row map.  Block 0 also publishes M and the per-stream row offsets.
 // Thread t owns float4 slots t + 256 j of the row (D <= 1024 * KP).
 template <class T, int KP>
 __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   __shared__ int s_cnt[kMaxViews];
   __shared__ int s_off[kMaxViews + 1];
-  __shared__ float s_red[4];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x;
   const int B = a.rm.B, N = a.rm.N, D = a.sh.D, D4 = D / 4;
-  // LN1 parameters do not depend on the row: in flight from the start
-  float4 gv[KP], bv[KP];
-#pragma unroll
-  for (int j = 0; j < KP; ++j) {
-    const int q = min(tid + 256 * j, D4 - 1);
-    gv[j] = reinterpret_cast<const float4*>(a.g)[q];
-    bv[j] = reinterpret_cast<const float4*>(a.b)[q];
-  }
   if (tid < B) s_cnt[tid] = a.rm.count[tid];
   __syncthreads();
   if (tid == 0) {
@@ -237,48 +228,18 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   const int tok = a.rm.idx[v * N + (r - s_off[v])];
   char* cache = a.caches.p[v];
   const float4* src = reinterpret_cast<const float4*>(a.t0 + ((size_t)v * N + tok) * D);
-  float4 t[KP], zr[KP];
-  float sum = 0.0f;
-#pragma unroll
-  for (int j = 0; j < KP; ++j) {
-    t[j] = src[min(tid + 256 * j, D4 - 1)];
-    zr[j] = make_float4(Elem<T>::rnd(t[j].x), Elem<T>::rnd(t[j].y), Elem<T>::rnd(t[j].z), Elem<T>::rnd(t[j].w));
-    if (tid + 256 * j < D4) sum += (zr[j].x + zr[j].y) + (zr[j].z + zr[j].w);
-  }
-  // two-pass LayerNorm over the row, fixed reduction order
-  float tot = wave_sum(sum);
-  if (lane == 0) s_red[w] = tot;
-  __syncthreads();
-  const float mean = ((s_red[0] + s_red[1]) + (s_red[2] + s_red[3])) / (float)D;
-  __syncthreads();
-  float sq = 0.0f;
-#pragma unroll
-  for (int j = 0; j < KP; ++j) {
-    if (tid + 256 * j < D4) {
-      const float dx = zr[j].x - mean, dy = zr[j].y - mean, dz = zr[j].z - mean, dw = zr[j].w - mean;
-      sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
-    }
-  }
-  tot = wave_sum(sq);
-  if (lane == 0) s_red[w] = tot;
-  __syncthreads();
-  const float rstd = 1.0f / sqrtf(((s_red[0] + s_red[1]) + (s_red[2] + s_red[3])) / (float)D + a.sh.eps);
-
   float4* ref = reinterpret_cast<float4*>(cache + a.cl.ref + (size_t)tok * D * 4);
   T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
-  T* z0 = static_cast<T*>(a.z) + (size_t)r * D;
-  T* abase = static_cast<T*>(a.a);  // operand order (frag_off)
+  T* z0 = static_cast<T*>(a.z);  // operand order (frag_off)
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     const int q = tid + 256 * j;
     if (q < D4) {
-      ref[q] = t[j];
-      store4v(x0 + 4 * q, zr[j]);
-      store4v(z0 + 4 * q, zr[j]);
-      store4v(abase + frag_off(r, 4 * q, D / 32), make_float4((zr[j].x - mean) * rstd * gv[j].x + bv[j].x,
-                                      (zr[j].y - mean) * rstd * gv[j].y + bv[j].y,
-                                      (zr[j].z - mean) * rstd * gv[j].z + bv[j].z,
-                                      (zr[j].w - mean) * rstd * gv[j].w + bv[j].w));
+      const float4 t = src[q];
+      const float4 zr = make_float4(Elem<T>::rnd(t.x), Elem<T>::rnd(t.y), Elem<T>::rnd(t.z), Elem<T>::rnd(t.w));
+      ref[q] = t;
+      store4v(x0 + 4 * q, zr);
+      store4v(z0 + frag_off(r, 4 * q, D / 32), zr);
     }
   }
   if (tid == 0) a.rows[r] = RowInfo{cache, tok, v};
