@@ -92,17 +92,16 @@ def kernel_bytes(m, M: float, kind: str):
     written and read once).  None for kinds without a figure here."""
     D, F, eb = m.dim, m.mlp_dim, (2 if m.dtype == "bf16" else 4)
     s2 = ksplit(m)
-    st = M * (D // 16) * 8  # LN2 block statistics of H
     if kind == "qkv":
         return 3 * D * D * eb + M * D * eb + 3 * M * D * eb
     if kind == "oproj":
-        return D * D * eb + 3 * M * D * eb + st
+        return D * D * eb + 3 * M * D * eb
     if kind == "fc1":
-        return D * F * eb + M * D * eb + st + M * F * eb
+        return D * F * eb + M * D * eb + M * F * eb
     if kind == "fc2":
         return F * D * eb + M * F * eb + s2 * M * D * 4
-    if kind == "res_ln1":
-        return s2 * M * D * 4 + 4 * M * D * eb
+    if kind == "res_ln1":  # partials + residual -> X^{l+1} (and Y after the last layer)
+        return s2 * M * D * 4 + 3 * M * D * eb
     if kind == "attn":
         return 2 * M * D * eb  # + K/V of the streams, added by the caller
     return None
