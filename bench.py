@@ -107,6 +107,81 @@ def kernel_bytes(m, M: float, kind: str):
     return None
 
 
+def torch_full_forward(m, w, patches, repeats: int):
+    """Context for the full-encode baseline: the same model's full forward over
+    every token written with plain torch ops (hipBLASLt GEMMs in the storage
+    type, fp32 LayerNorm/softmax/GELU).  Returns (median ms, launch mode): a
+    HIP-graph replay when capturing works and every replay equals the eager
+    result, else eager."""
+    import torch
+    import torch.nn.functional as F
+    dev = patches.device
+    dt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+    B, N, D, H = patches.shape[0], m.n_tokens, m.dim, m.heads
+    dh = D // H
+    T = {k: torch.from_numpy(v).to(dev) for k, v in w.items()}
+    Wd = {k: v.to(dt) for k, v in T.items()}
+
+    def fwd():
+        x = torch.matmul(patches, T["w_pe"]) + T["b_pe"] + T["pos"]       # fp32 embedding
+        h = x.to(dt)
+        for l in range(m.depth):
+            g = lambda n: Wd[f"l{l}.{n}"]  # noqa: E731
+            a = F.layer_norm(h.float(), (D,), T[f"l{l}.ln1_g"], T[f"l{l}.ln1_b"], m.ln_eps).to(dt)
+            qkv = torch.matmul(a, g("w_qkv")) + g("b_qkv")
+            q, k, v = (t.reshape(B, N, H, dh).permute(0, 2, 1, 3).contiguous() for t in qkv.split(D, dim=-1))
+            sc = torch.matmul(q, k.transpose(-1, -2).contiguous()).float() * (dh ** -0.5)
+            o = torch.matmul(torch.softmax(sc, dim=-1).to(dt), v)
+            o = o.permute(0, 2, 1, 3).reshape(B, N, D)
+            h = h + (torch.matmul(o, g("w_o")) + g("b_o"))
+            a2 = F.layer_norm(h.float(), (D,), T[f"l{l}.ln2_g"], T[f"l{l}.ln2_b"], m.ln_eps).to(dt)
+            f = F.gelu((torch.matmul(a2, g("w_1")) + g("b_1")).float(), approximate="tanh").to(dt)
+            h = h + (torch.matmul(f, g("w_2")) + g("b_2"))
+        return F.layer_norm(h.float(), (D,), T["lnf_g"], T["lnf_b"], m.ln_eps)
+
+    def timed(run):
+        for _ in range(3):
+            run()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(repeats):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            run()
+            e1.record()
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return statistics.median(ms)
+
+    with torch.no_grad():
+        ref = fwd()
+        torch.cuda.synchronize()
+        eager_ms = timed(fwd)
+        try:
+            st = torch.cuda.Stream()
+            st.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(st):
+                fwd()
+            torch.cuda.current_stream().wait_stream(st)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                out = fwd()
+            ok = True
+            for _ in range(3):  # replays with eager work in between, each checked
+                graph.replay()
+                torch.cuda.synchronize()
+                ok = ok and bool(torch.equal(out, ref))
+                fwd()
+                torch.cuda.synchronize()
+            if ok:
+                graph_ms = timed(graph.replay)
+                if graph_ms < eager_ms:
+                    return graph_ms, "hip-graph"
+        except Exception:  # capture not available: the eager time stands
+            pass
+    return eager_ms, "eager"
+
+
 def cpu_baseline(wl, frames, seconds: float):
     """The oracle as it is, on this host: full encode of frame 0, then steps of
     the same stream until about `seconds` of step time have been spent."""
@@ -297,12 +372,14 @@ def main() -> int:
     ap.add_argument("--full-repeats", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-torch-full", action="store_true", help="skip the torch full forward (context)")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel events")
     ap.add_argument("--eager", dest="graph", action="store_false",
                     help="launch kernel by kernel instead of replaying captured HIP graphs")
     ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four comma-separated values "
                                                  "(QKV, O-proj, fc1, fc2; 0 = automatic)")
     ap.add_argument("--attn-qtiles", type=int, default=0, help="16-query tiles per attention workgroup (0 = automatic)")
+    ap.add_argument("--row-groups", type=int, default=0, help="GEMM row groups of threshold steps (0 = 1)")
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
@@ -334,9 +411,9 @@ def main() -> int:
     torch.cuda.set_device(dev)
     frames = torch.from_numpy(np.stack(frames_np)).to(dev)  # [T][B][N][P], resident in HBM
     enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
-    if args.cols or args.attn_qtiles:
+    if args.cols or args.attn_qtiles or args.row_groups:
         cols = [int(x) for x in args.cols.split(",")] if args.cols else None
-        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles), enc.h)
+        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles, args.row_groups), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),
@@ -426,6 +503,13 @@ def main() -> int:
         "full_encode_frames_per_s": round(B * 1e3 / full_med, 2),
         "speedup_vs_full_encode": round(full_med / step_ms, 3),
     }
+    if not args.no_torch_full:
+        tms, tmode = torch_full_forward(m, wl.weights(), frames[0], max(5, args.full_repeats // 2))
+        best = min(full_med, tms)
+        result["torch_full_forward_ms"] = round(tms, 5)
+        result["torch_full_forward_launch"] = tmode
+        # the speedup against the faster of the two full re-encodes
+        result["speedup_vs_best_full"] = round(best / step_ms, 3)
 
     if not args.no_profile:
         prof = incvit.incvit_profile_read(enc.h, reset=True)

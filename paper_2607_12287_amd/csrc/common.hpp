@@ -141,24 +141,25 @@ struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map
 
 enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3 };
 
+// Fields in the order the kernel's prologue needs them, so that its argument
+// loads go out together.
 struct GemmArgs {
-  const RowInfo* rows;  // row map (cache, token, stream) of each compact row
-  const Meta* meta;
-  CacheLayout cl;
-  Shape sh;
-  int layer;
   const void* A;      // compact A rows in operand order: QKV Z_l, RES O, FC1 H, PART G
-  int lda;
   const void* W;      // packed [Nout/16][kchunks][512]
   const float* bias;  // [Nout] (not used by PART)
-  int kchunks, Nout;
-  void* out;          // QKV Q [Mpad][D]; RES H (operand order); FC1 G; PART f32 [ksplit][mpad][ldo]
-  int ldo;
-  int ksplit;         // K is split over gridDim.y = ksplit workgroups (PART)
-  int mpad;           // padded rows (partial slices, statistics)
-  const void* resid;  // RES: Z_l rows (operand order)
   const float* c1;    // QKV, FC1: column sums of the LayerNorm-folded weights; `bias`
                       // then holds beta^T W + b (see FoldArgs)
+  const RowInfo* rows;  // row map (cache, token, stream) of each compact row
+  const Meta* meta;
+  const void* resid;  // RES: Z_l rows (operand order)
+  void* out;          // QKV Q [Mpad][D]; RES H (operand order); FC1 G; PART f32 [ksplit][mpad][ldo]
+  int lda, kchunks, Nout, ldo;
+  int ksplit;         // K is split over ksplit workgroups (PART)
+  int rgroups;        // 32-row groups launched: enough for the largest M of the call
+  int mpad;           // padded rows (partial slices)
+  int layer;
+  Shape sh;
+  CacheLayout cl;
 };
 
 // Row kernel that finishes the split-K MLP down projection, one workgroup per

@@ -21,14 +21,19 @@
 // order in the epilogue (mean = sum / D, var = sumsq / D - mean^2).
 //
 // With M a few dozen rows these are weight-streaming problems whose time is set
-// by memory latency, so a workgroup issues every load it needs for its first
-// 32 rows at once, before it knows M: the A fragments of rows 0..31 (the padded
-// workspace keeps that in bounds), all of its waves' weight chunks and the
-// epilogue operands.  Weights go straight into MFMA operand registers (the
+// by memory latency, so a workgroup of the first row group issues every load
+// it needs at once, before it knows M: the A fragments of rows 0..31 (the
+// padded workspace keeps that in bounds), all of its waves' weight chunks and
+// the epilogue operands.  Weights go straight into MFMA operand registers (the
 // packed layout makes one 32-deep chunk of a 16-column block one 16-byte load
-// per lane) and stay there for later row blocks.  Operands are read with buffer
-// loads: one lane offset shared by all of them and the chunk's position as a
-// wave-uniform offset.
+// per lane).  Operands are read with buffer loads: one lane offset shared by
+// all of them and the chunk's position as a wave-uniform offset.
+//
+// Grid: (column groups) x (K splits) x (row groups: up to 8, enough for the
+// call's largest M).  Row group z owns the 32-row blocks z, z + nz, ...; row
+// groups past M leave after reading M.  Workgroups are renumbered XCD-major (the hardware deals
+// them to the 8 XCDs round robin), with the row group fastest, so the row
+// groups of one column block share an XCD and its L2 holds their weights.
 //
 // Workgroup: NW = 8 waves, NB 16-column blocks; wave w owns a
 // contiguous run of CPW chunks of this workgroup's share of K (rounds of
@@ -93,11 +98,27 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, n = lane & 15;
   const int D = a.sh.D;
+  // (column group, K split, row group) of this workgroup, XCD-major; the
+  // grid's shape comes from the arguments (no load of the dispatch packet)
+  const int nz = a.rgroups, ny = a.ksplit, nx = a.Nout / 16 / NB;
+  int zg = 0, ks = blockIdx.y, cg = blockIdx.x;  // one row group: launch order
+  if (nz > 1) {                                   // uniform
+    const int total = nx * ny * nz;
+    const int lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
+    const int xcd = lin % 8, per = total / 8, rem = total % 8;
+    const int pos = xcd * per + min(xcd, rem) + lin / 8;
+    zg = pos % nz;
+    ks = (pos / nz) % ny;
+    cg = pos / (nz * ny);
+  }
+  if (zg > 0) {  // a later row group reads M first and leaves when it has no rows (uniform)
+    if (zg * kGemmRB >= *static_cast<const volatile int*>(&a.meta->m)) return;
+  }
   const int M = a.meta->m;
-  const int cb0 = blockIdx.x * NB;
+  const int cb0 = cg * NB;
   // this workgroup's share of K: chunks [kb, kb + kn)
   const int kper = (a.kchunks + a.ksplit - 1) / a.ksplit;
-  const int kb = blockIdx.y * kper, kn = min(kper, a.kchunks - kb);
+  const int kb = ks * kper, kn = min(kper, a.kchunks - kb);
   const int kc_last = kn - 1;
   const int rounds = (kn + NW * CPW - 1) / (NW * CPW);
 
@@ -135,20 +156,22 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
           static_cast<const T*>(a.resid)[frag_off(m0 + 16 * re + 4 * g + ie, (cb0 + b) * 16 + n, D / 32)]);
   };
 
-  load_a(0, 0);
+  // the first row group runs whatever M is (with M = 0 it stores nothing),
+  // so its loads are never held back behind the read of M
+  const int mfirst = zg * kGemmRB, mstep = nz * kGemmRB;
+  load_a(mfirst, 0);
   load_w(0);
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     biasv[b] = EPI == EPI_PART ? 0.0f : a.bias[(cb0 + b) * 16 + n];
     c1v[b] = LNA ? a.c1[(cb0 + b) * 16 + n] : 0.0f;
   }
-  if constexpr (EPI == EPI_QKV) rinfo = a.rows[16 * re + 4 * g + ie];
-  if constexpr (EPI == EPI_RES) load_res(0);
+  if constexpr (EPI == EPI_QKV) rinfo = a.rows[mfirst + 16 * re + 4 * g + ie];
+  if constexpr (EPI == EPI_RES) load_res(mfirst);
 
-  // One 32-row block.  The first block is a copy of its own (FIRST), which
-  // runs whatever M is (with M = 0 it stores nothing), so the loads above are
-  // never held back behind the read of M, and its waits count exactly the
-  // loads issued above instead of the fewer a later block reloads.
+  // One 32-row block.  The group's first block is a copy of its own (FIRST),
+  // so its waits count exactly the loads issued above instead of the fewer a
+  // later block reloads (the weights stay in registers).
   auto row_block = [&](const int m0, auto first) {
     if constexpr (!decltype(first)::value) {
       load_a(m0, 0);
@@ -230,7 +253,7 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) x += redf[(((ww * 2 + re) * NB + b) * 64 + lane) * 4 + ie];
       if constexpr (EPI == EPI_PART) {
-        if (ok) static_cast<float*>(a.out)[((size_t)blockIdx.y * a.mpad + row) * a.ldo + col] = x;
+        if (ok) static_cast<float*>(a.out)[((size_t)ks * a.mpad + row) * a.ldo + col] = x;
       } else if constexpr (EPI == EPI_RES) {  // H = S(Z + (O W_o + b_o))
         if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resv[b] + (x + biasv[b]));
       } else if constexpr (EPI == EPI_QKV) {
@@ -254,14 +277,14 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
     }
     __syncthreads();  // red and the row partials are reused by the next row block
   };
-  row_block(0, std::true_type{});
-  for (int m0 = kGemmRB; m0 < M; m0 += kGemmRB) row_block(m0, std::false_type{});
+  row_block(mfirst, std::true_type{});
+  for (int m0 = mfirst + mstep; m0 < M; m0 += mstep) row_block(m0, std::false_type{});
 }
 
 template <class T, int EPI, int NB, int CPW>
 hipError_t launch_gemm_cfg(const GemmArgs& a, hipStream_t s) {
-  return launch_k(gemm_kernel<T, EPI, NB, CPW>, dim3(a.Nout / 16 / NB, a.ksplit), dim3(gemm_waves<EPI>() * 64),
-                  (size_t)gemm_lds_bytes<EPI, NB>(), s, a);
+  return launch_k(gemm_kernel<T, EPI, NB, CPW>, dim3(a.Nout / 16 / NB, a.ksplit, a.rgroups),
+                  dim3(gemm_waves<EPI>() * 64), (size_t)gemm_lds_bytes<EPI, NB>(), s, a);
 }
 
 // Chunks per wave: the smallest instantiated count that covers this

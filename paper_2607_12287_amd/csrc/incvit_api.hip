@@ -265,6 +265,7 @@ struct incvit_handle {
   int64_t prof_n[INCVIT_K_COUNT] = {};
   int cols[4] = {0, 0, 0, 0};  // 0 = automatic
   int attn_qtiles = 0;         // 0 = automatic
+  int row_groups = 1;          // GEMM row groups of threshold steps
 };
 
 struct incvit_graph {
@@ -328,7 +329,13 @@ const float* fptr(const incvit_handle* h, size_t off) { return reinterpret_cast<
 // Launch the per-layer kernels for the rows of the call (row map in ws).
 // refreshed: optional output of the last layer's final LayerNorm rows.
 incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLayout& wl, char* ws,
-                         int max_rows_per_view, int mmax, bool step, void* refreshed, hipStream_t s) {
+                         int max_rows_per_view, int mmax, bool exact_m, void* refreshed, hipStream_t s) {
+  // GEMM row groups: when the call's row count M is known on the host (a full
+  // encode, or a pure top-k step where M is the sum of the caps), one 32-row
+  // block per workgroup (up to 8 groups); otherwise one group, which loops over
+  // the row blocks (idle groups cost about a microsecond each per launch)
+  const int need = std::max(1, (mmax + 31) / 32);
+  const int rgroups = std::min(exact_m ? need : std::max(1, std::min(need, h->row_groups)), 8);
   const Shape& sh = h->sh;
   const RowInfo* rows = reinterpret_cast<const RowInfo*>(ws + wl.rows);
   const Meta* meta = reinterpret_cast<const Meta*>(ws + wl.meta);
@@ -346,6 +353,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       a.kchunks = g.kchunks;
       a.Nout = g.Nout;
       a.ksplit = g.ksplit;
+      a.rgroups = rgroups;
       a.mpad = wl.Mpad;
       int epi = EPI_PART;
       switch (kind) {
@@ -605,7 +613,7 @@ incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patch
   ra.hash = h->hash;
   ra.z = ws + wl.z;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  return run_layers(h, views, B, wl, ws, sh.N, mmax, false, nullptr, s);
+  return run_layers(h, views, B, wl, ws, sh.N, mmax, true, nullptr, s);
 }
 
 incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, void* const* caches, float tau,
@@ -662,7 +670,8 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   ra.t0 = t0;
   ra.z = ws + wl.z;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  return run_layers(h, views, B, wl, ws, max_rows, mmax, true, refreshed, s);
+  // with the threshold disabled every stream refreshes exactly its cap
+  return run_layers(h, views, B, wl, ws, max_rows, mmax, std::isinf(tau) && tau > 0, refreshed, s);
 }
 
 incvit_status incvit_cache_export(const incvit_handle* h, const void* cache, void* canonical_dst, void* stream) {
@@ -733,8 +742,11 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   }
   const int q = t ? t->attn_qtiles : 0;
   if (q < 0 || q > 2) return fail(h, INCVIT_ERR_ARG, "attn_qtiles must be 0, 1 or 2");
+  const int rg = t ? t->row_groups : 0;
+  if (rg < 0 || rg > 8) return fail(h, INCVIT_ERR_ARG, "row_groups must be in [0, 8]");
   for (int k = 0; k < 4; ++k) h->cols[k] = t ? t->cols[k] : 0;
   h->attn_qtiles = q;
+  h->row_groups = rg > 0 ? rg : 1;
   return INCVIT_OK;
 }
 
