@@ -90,6 +90,10 @@ size_t incvit_packed_weights_bytes(const incvit_config* cfg);
 
 /* Repack canonical weights (device) into the kernels' layout (device):
  * GEMM weights in 16-column x 32-row MFMA operand chunks, vectors in fp32.
+ * The LayerNorm before the QKV and MLP-up projections is folded into their
+ * packed weights: W' = S(gamma * W) row by row, with the column sums of W' and
+ * beta^T W + b stored beside them (the encoder then computes
+ * LN(x) W + b = rstd (x W') - rstd mean colsum(W') + beta^T W + b).
  * The two buffers must not overlap.  Asynchronous on `stream`. */
 incvit_status incvit_pack_weights(const incvit_config* cfg, const void* canonical,
                                   void* packed, void* stream);
@@ -220,12 +224,12 @@ typedef enum {
   INCVIT_K_SIM,       /* cosine against the cached reference              */
   INCVIT_K_SELECT,    /* threshold / top-k selection and compaction      */
   INCVIT_K_COMMIT,    /* ref, X0 of the selected rows; LN1 of layer 0     */
-  INCVIT_K_QKV,       /* QKV projection, K/V scattered into the cache     */
+  INCVIT_K_QKV,       /* LN1 + QKV projection, K/V scattered into cache   */
   INCVIT_K_ATTN,      /* attention of the selected queries                */
-  INCVIT_K_OPROJ,     /* output projection + residual -> H; LN2 statistics */
-  INCVIT_K_FC1,       /* MLP up projection + GELU                         */
+  INCVIT_K_OPROJ,     /* output projection + residual -> H                */
+  INCVIT_K_FC1,       /* LN2 + MLP up projection + GELU                   */
   INCVIT_K_FC2,       /* MLP down projection (split-K partial sums)       */
-  INCVIT_K_RES_LN1,   /* + bias + residual -> X^{l+1}; next LN1 or final LN */
+  INCVIT_K_RES_LN1,   /* + bias + residual -> X^{l+1}; final LN (last)    */
   INCVIT_K_COUNT
 } incvit_kernel_kind;
 
