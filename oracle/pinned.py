@@ -39,6 +39,8 @@ def _load():
             lib.oracle_embed_f32.restype = None
             lib.oracle_cosine_f32.argtypes = [f, f, i32, i32, f]
             lib.oracle_cosine_f32.restype = None
+            lib.oracle_key_score_f32.argtypes = [f, f, f, f, f, i32, i32, ctypes.c_float, i32, f]
+            lib.oracle_key_score_f32.restype = None
             _lib = lib
     return _lib
 
@@ -70,4 +72,23 @@ def cosine_f32(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     assert a.shape == b.shape and a.ndim == 2
     out = np.empty((a.shape[0],), dtype=np.float32)
     lib.oracle_cosine_f32(_fp(a), _fp(b), a.shape[0], a.shape[1], _fp(out))
+    return out
+
+
+def key_score_f32(t0: np.ndarray, ln_g: np.ndarray, ln_b: np.ndarray, w_k: np.ndarray, b_k: np.ndarray,
+                  eps: float, bf16: bool) -> np.ndarray:
+    """First-layer keys of every token in the fixed fp32 order of pinned.c:
+    LayerNorm 1 of layer 0 on S(t0), then the key projection; [N][D] float32."""
+    lib = _load()
+    t0 = np.ascontiguousarray(t0, dtype=np.float32)
+    n, d = t0.shape
+    assert d <= 4096
+    ln_g = np.ascontiguousarray(ln_g, dtype=np.float32)
+    ln_b = np.ascontiguousarray(ln_b, dtype=np.float32)
+    w_k = np.ascontiguousarray(w_k, dtype=np.float32)
+    b_k = np.ascontiguousarray(b_k, dtype=np.float32)
+    assert ln_g.shape == (d,) and ln_b.shape == (d,) and w_k.shape == (d, d) and b_k.shape == (d,)
+    out = np.empty((n, d), dtype=np.float32)
+    lib.oracle_key_score_f32(_fp(t0), _fp(ln_g), _fp(ln_b), _fp(w_k), _fp(b_k), n, d, float(eps),
+                             1 if bf16 else 0, _fp(out))
     return out

@@ -24,9 +24,19 @@ linear layers, LayerNorm with biased variance, tanh-form GELU, softmax
 attention scaled by 1/sqrt(d_h), and a final LayerNorm.  These details are not
 in the paper; they are the readings this build takes.
 
-Arithmetic: everything is float64 except the patch embedding and the cosine,
-which follow a fixed fp32 order (``pinned.c``) so that the selection is
-reproducible bit for bit. ``S(.)`` rounds to the storage precision (bf16 with
+What the cosine compares (``Model.score``): "embed" scores the layer-1 input
+token (patch embedding + position) against its value at the token's last
+refresh; "key" scores the first layer's key projection of that token, as eq. 3
+states it ("cosine similarity between current and previously cached keys").
+Either way the vector is kept per token as the reference for later frames.
+
+The paper's odd/even chunk schedule (a full forward on odd chunks whose keys
+become the reference, incremental encoding on even chunks) is
+``run_schedule`` with period 2; other periods generalise it.
+
+Arithmetic: everything is float64 except the patch embedding, the key score
+and the cosine, which follow a fixed fp32 order (``pinned.c``) so that the
+selection is reproducible bit for bit. ``S(.)`` rounds to the storage precision (bf16 with
 ties to even, fp32, or nothing for the "f64" mode used by the pins) at the
 points where a value between two operations is formed, as a half-precision
 inference pipeline stores every tensor between its operations (the paper runs
@@ -126,16 +136,33 @@ def select(sim: np.ndarray, tau: float, cap: int) -> np.ndarray:
 # ----------------------------------------------------------------------------
 
 
-class Model:
-    """Weights of the encoder as float64 arrays (values as stored)."""
+SCORES = ("embed", "key")
 
-    def __init__(self, shape, weights: Dict[str, np.ndarray], dtype: Optional[str] = None):
+
+class Model:
+    """Weights of the encoder as float64 arrays (values as stored).
+
+    score: "embed" (cosine of the embedded tokens) or "key" (cosine of the
+    first layer's keys, eq. 3)."""
+
+    def __init__(self, shape, weights: Dict[str, np.ndarray], dtype: Optional[str] = None,
+                 score: str = "embed"):
+        if score not in SCORES:
+            raise ValueError(f"score must be one of {SCORES}")
         self.shape = shape
         self.dtype = dtype or shape.dtype
+        self.score = score
         self.eps = float(shape.ln_eps)
         self.w = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
         self.w32 = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in
                     (("w_pe", weights["w_pe"]), ("b_pe", weights["b_pe"]), ("pos", weights["pos"]))}
+        if score == "key":
+            D = shape.dim
+            self.w32.update({
+                "ln1_g": np.ascontiguousarray(weights["l0.ln1_g"], dtype=np.float32),
+                "ln1_b": np.ascontiguousarray(weights["l0.ln1_b"], dtype=np.float32),
+                "w_k": np.ascontiguousarray(np.asarray(weights["l0.w_qkv"])[:, D:2 * D], dtype=np.float32),
+                "b_k": np.ascontiguousarray(np.asarray(weights["l0.b_qkv"])[D:2 * D], dtype=np.float32)})
 
     def p(self, l: int, name: str) -> np.ndarray:
         return self.w[f"l{l}.{name}"]
@@ -145,8 +172,9 @@ class Model:
 class ViewCache:
     """Everything one stream keeps between frames, canonical layout.
 
-    ref: [N][D] fp32, each token's embedding at its last refresh (the
-    reference the cosine is taken against);
+    ref: [N][D] fp32, each token's score vector (embedding or first-layer
+    key, per Model.score) at its last refresh: the reference the cosine is
+    taken against;
     X: [L+1][N][D] layer inputs (X[0] = embedded tokens, X[l+1] = layer l out);
     K, V: [L][N][D] per-layer keys and values;  Y: [N][D] final output."""
 
@@ -166,6 +194,7 @@ class StepResult:
     sim: np.ndarray        # float32 [N], fixed-order cosine
     refreshed: np.ndarray  # [k][D] = Y[idx]
     t0: np.ndarray         # float32 [N][D] embedded tokens of this frame
+    sv: Optional[np.ndarray] = None  # float32 [N][D] score vectors (t0 or first-layer keys)
 
     @property
     def count(self) -> int:
@@ -176,6 +205,22 @@ def embed(model: Model, patches: np.ndarray) -> np.ndarray:
     """Patch embedding + Pos for all tokens, fixed fp32 order; [N][D] fp32."""
     w = model.w32
     return pinned.embed_f32(patches, w["w_pe"], w["b_pe"], w["pos"])
+
+
+def key_score(model: Model, t0: np.ndarray) -> np.ndarray:
+    """First-layer keys of every token, fixed fp32 order: LayerNorm 1 of layer
+    0 on the stored layer input S(t0), then the key projection (eq. 3 compares
+    these keys); [N][D] fp32."""
+    w = model.w32
+    return pinned.key_score_f32(t0, w["ln1_g"], w["ln1_b"], w["w_k"], w["b_k"], model.eps,
+                                model.dtype == "bf16")
+
+
+def score_vectors(model: Model, t0: np.ndarray) -> np.ndarray:
+    """The per-token vectors the cosine of eq. 3 compares, [N][D] fp32."""
+    if model.score == "key":
+        return key_score(model, t0)
+    return t0
 
 
 def layer_rows(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
@@ -206,14 +251,15 @@ def final_rows(model: Model, Z: np.ndarray) -> np.ndarray:
     return S(layer_norm(Z, model.w["lnf_g"], model.w["lnf_b"], model.eps), model.dtype)
 
 
-def _encode_rows(model: Model, cache: ViewCache, U: np.ndarray, t0: np.ndarray,
+def _encode_rows(model: Model, cache: ViewCache, U: np.ndarray, t0: np.ndarray, sv: np.ndarray,
                  trace: Optional[dict] = None) -> None:
     """Recompute rows U through every layer against the cached rows R.
 
     The caller has already decided U; the same rows are recomputed in every
-    layer.  `trace`, if given, collects the per-layer attention outputs and
-    residuals of the rows U (for tests)."""
-    cache.ref[U] = t0[U]
+    layer, and their score vectors `sv` become their new references.  `trace`,
+    if given, collects the per-layer attention outputs and residuals of the
+    rows U (for tests)."""
+    cache.ref[U] = sv[U]
     Z = S(t0[U].astype(np.float64), model.dtype)
     cache.X[0][U] = Z
     for l in range(model.shape.depth):
@@ -233,7 +279,7 @@ def full_encode(model: Model, patches: np.ndarray) -> ViewCache:
     """Full forward of one frame; fills every cache row (the paper's odd chunk)."""
     cache = empty_cache(model)
     t0 = embed(model, patches)
-    _encode_rows(model, cache, np.arange(model.shape.n_tokens), t0)
+    _encode_rows(model, cache, np.arange(model.shape.n_tokens), t0, score_vectors(model, t0))
     return cache
 
 
@@ -241,11 +287,36 @@ def step(model: Model, patches: np.ndarray, cache: ViewCache, tau: float, cap: i
          trace: Optional[dict] = None) -> StepResult:
     """Incremental encode of one frame; updates `cache` in place."""
     t0 = embed(model, patches)
-    sim = pinned.cosine_f32(t0, cache.ref)
+    sv = score_vectors(model, t0)
+    sim = pinned.cosine_f32(sv, cache.ref)
     U = select(sim, tau, cap)
     if U.size:
-        _encode_rows(model, cache, U, t0, trace)
-    return StepResult(idx=U, sim=sim, refreshed=cache.Y[U].copy(), t0=t0)
+        _encode_rows(model, cache, U, t0, sv, trace)
+    return StepResult(idx=U, sim=sim, refreshed=cache.Y[U].copy(), t0=t0, sv=sv)
+
+
+def run_schedule(model: Model, frames: Sequence[np.ndarray], period: int, tau: float, cap: int,
+                 cache: Optional[ViewCache] = None, first: int = 0):
+    """Encode one stream frame by frame under a refresh period (§III-B): frame
+    t (counted from `first`) is encoded in full when t % period == 0, which
+    replaces every cached row and reference, and incrementally otherwise.
+    Period 2 is the paper's odd/even chunk schedule: the incremental frames
+    compare against the keys of the preceding full pass.  A full frame reports
+    every token as refreshed.  Returns (cache, [StepResult per frame])."""
+    if period < 1:
+        raise ValueError("period must be >= 1")
+    out = []
+    for j, patches in enumerate(frames):
+        t = first + j
+        if t % period == 0 or cache is None:
+            cache = full_encode(model, patches)
+            n = model.shape.n_tokens
+            t0 = embed(model, patches)
+            out.append(StepResult(idx=np.arange(n, dtype=np.int32), sim=np.full(n, np.nan, np.float32),
+                                  refreshed=cache.Y.copy(), t0=t0, sv=cache.ref.copy()))
+        else:
+            out.append(step(model, patches, cache, tau, cap))
+    return cache, out
 
 
 def full_forward_dense(model: Model, patches: np.ndarray) -> np.ndarray:

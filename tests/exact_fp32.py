@@ -90,3 +90,47 @@ def cosine(a, b):
     dot, na, nb = partials(a, b), partials(a, a), partials(b, b)
     denom = mul(sqrt(na), sqrt(nb))
     return np.float32(div(dot, max(denom, f32(1e-8))))
+
+
+def _tree64(s):
+    s = list(s)
+    off = 32
+    while off >= 1:
+        for j in range(off):
+            s[j] = add(s[j], s[j + off])
+        off //= 2
+    return s[0]
+
+
+def key_token(x, ln_g, ln_b, w_k, b_k, eps):
+    """One token of the fixed-order first-layer key score, every fmaf exact.
+
+    x: the stored layer-0 input (already rounded to the storage type);
+    LayerNorm with 64 lane partials and the halving tree, then the key
+    projection as one fmaf chain per output in increasing input index."""
+    D = len(x)
+    x = [float(v) for v in x]
+    s = []
+    for j in range(64):
+        acc = 0.0
+        for d in range(j, D, 64):
+            acc = add(acc, x[d])
+        s.append(acc)
+    mean = div(_tree64(s), float(D))
+    c = [add(v, -mean) for v in x]
+    s = []
+    for j in range(64):
+        acc = 0.0
+        for d in range(j, D, 64):
+            acc = fmaf(c[d], c[d], acc)
+        s.append(acc)
+    var = div(_tree64(s), float(D))
+    rstd = div(1.0, sqrt(add(var, f32(eps))))
+    n = [fmaf(mul(c[d], rstd), float(ln_g[d]), float(ln_b[d])) for d in range(D)]
+    out = []
+    for e in range(D):
+        acc = float(b_k[e])
+        for d in range(D):
+            acc = fmaf(n[d], float(w_k[d, e]), acc)
+        out.append(acc)
+    return np.array(out, dtype=np.float32)
