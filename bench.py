@@ -27,6 +27,8 @@ import time
 
 METRIC = "incremental ViT frames/sec at 10% refresh (So400m shape); speedup vs full encode"
 HBM_PEAK_GBS = 8000.0
+# non-packed fp32 FMA: 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz (packed fp32 is compiled out)
+ALU_PEAK_TFLOPS = 78.6
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PROFILES = os.path.join(ROOT, "profiles")
 GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj"}  # epilogue template argument
@@ -180,6 +182,85 @@ def torch_full_forward(m, w, patches, repeats: int):
         except Exception:  # capture not available: the eager time stands
             pass
     return eager_ms, "eager"
+
+
+def measure_variant(wl, frames, score: str, period: int, steps: int, warmup: int, full_repeats: int):
+    """Frames/s of the same stream with another score (embedding or first-layer
+    keys) and, for period >= 1, under a refresh period: frame t is fully
+    encoded when t % period == 0 (HIP-graph replays of the full encode), else
+    incrementally (the step graph).  Period 0 = the rolling stream (one full
+    encode of frame 0 only).  Also the per-kernel times of an eager pass."""
+    import torch
+    from paper_2607_12287_amd import incvit, synth
+    m, B = wl.model, wl.views
+    dev = frames.device
+    enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B, score=score)
+    buf, caches = enc.new_caches(B)
+    out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
+           torch.empty((B,), dtype=torch.int32, device=dev),
+           torch.empty((B, m.n_tokens, m.dim), dtype=enc.dtype, device=dev))
+    inp = torch.empty_like(frames[0])
+    inp.copy_(frames[0])
+    gfull = enc.full_graph(inp, caches)
+    full_ms = []
+    for i in range(full_repeats + 3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        enc.launch(gfull)
+        e1.record()
+        e1.synchronize()
+        if i >= 3:
+            full_ms.append(e0.elapsed_time(e1))
+    enc.launch(gfull)  # frame 0 encoded in full
+    gstep = enc.step_graph(inp, caches, wl.tau, wl.caps, out)
+    counts = torch.zeros((steps, B), dtype=torch.int32, device=dev)
+
+    def frame(t):
+        inp.copy_(frames[t])
+        if period >= 1 and t % period == 0:
+            enc.launch(gfull)
+        else:
+            enc.launch(gstep)
+
+    for t in range(1, warmup + 1):
+        frame(t)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for j, t in enumerate(range(warmup + 1, warmup + 1 + steps)):
+        frame(t)
+        counts[j].copy_(out[1])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    enc.drop_graph(gstep)
+    enc.drop_graph(gfull)
+    k = counts.float().cpu().numpy()
+    inc = [j for j, t in enumerate(range(warmup + 1, warmup + 1 + steps)) if not (period >= 1 and t % period == 0)]
+    # per-kernel times: eager steps of the rolling stream with per-launch events
+    enc.full_encode(frames[0], caches)
+    incvit.incvit_profile_read(enc.h, reset=True)
+    incvit.incvit_profile_enable(enc.h, True)
+    n_prof = min(steps, 50)
+    for t in range(1, n_prof + 1):
+        enc.step(frames[t], caches, wl.tau, wl.caps, out=out)
+    torch.cuda.synchronize()
+    prof = incvit.incvit_profile_read(enc.h, reset=True)
+    incvit.incvit_profile_enable(enc.h, False)
+    enc.close()
+    full_med = statistics.median(full_ms)
+    res = {"score": score, "period": period, "frames_per_s": round(steps * B / wall, 2),
+           "ms_per_frame": round(wall * 1e3 / steps, 5), "full_encode_ms": round(full_med, 5),
+           "speedup_vs_full_encode": round(full_med / (wall * 1e3 / steps), 3),
+           "rows_mean_incremental": round(float(k[inc].sum(axis=1).mean()), 2) if inc else None,
+           "kernel_us_per_launch": {kk: round(v[0] * 1e3 / v[1], 3) for kk, v in prof.items() if v[1] > 0}}
+    kp = prof.get("key_proj")
+    if kp and kp[1] > 0:
+        us = kp[0] * 1e3 / kp[1]
+        flop = 2.0 * B * m.n_tokens * m.dim * m.dim
+        res["key_proj_roofline"] = {"bound": "alu", "achieved": round(flop / (us * 1e-6) / 1e12, 3),
+                                    "peak": ALU_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                    "frac": round(flop / (us * 1e-6) / 1e12 / ALU_PEAK_TFLOPS, 4),
+                                    "avg_launch_us": round(us, 3)}
+    return res
 
 
 def cpu_baseline(wl, frames, seconds: float):
@@ -374,6 +455,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-torch-full", action="store_true", help="skip the torch full forward (context)")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel events")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the key-score and odd/even-schedule measurements")
     ap.add_argument("--eager", dest="graph", action="store_false",
                     help="launch kernel by kernel instead of replaying captured HIP graphs")
     ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four comma-separated values "
@@ -532,6 +615,13 @@ def main() -> int:
         result["kernel_us_per_launch"] = {k: round(v[0] * 1e3 / v[1], 3) for k, v in kinds.items()}
         result["kernel_ms_per_step"] = {k: round(v[0] / args.steps, 5) for k, v in kinds.items()}
     del buf2, caches2
+
+    if not args.no_variants:
+        # the paper's own score (first-layer keys, eq. 3) on the rolling stream,
+        # and its odd/even chunk schedule (period 2) with that score
+        vsteps, vwarm = min(args.steps, 200), min(args.warmup, 20)
+        result["variants"] = [measure_variant(wl, frames, "key", p, vsteps, vwarm, args.full_repeats)
+                              for p in (0, 2)]
 
     if not args.no_cpu_baseline:
         n_cpu = min(len(frames_np), 64)

@@ -12,9 +12,15 @@
  *
  * Readings taken where the paper is silent (each is an argument of this API or
  * fixed here):
- *   - the score is the cosine of the layer-1 input token (patch embedding +
- *     position) against that token's value at its last refresh, computed in a
- *     fixed fp32 order so that selection is reproducible bit for bit;
+ *   - the score is the cosine of a per-token vector against that token's
+ *     vector at its last refresh, computed in a fixed fp32 order so that
+ *     selection is reproducible bit for bit.  The vector is, per config
+ *     (incvit_score), either the layer-1 input token (patch embedding +
+ *     position) or the first layer's key of that token, as eq. 3 states it;
+ *   - the paper's odd/even chunks (a full pass on odd chunks whose keys become
+ *     the reference, incremental encoding on even chunks) are
+ *     incvit_encode_frame with period 2; between full passes every refreshed
+ *     token's vector becomes its new reference;
  *   - "top rho*N lowest similarities" is generalised to: U = {i : sim_i < tau}
  *     (strict), and if |U| > cap only the cap lowest similarities are kept,
  *     equal similarities going to the lower token index.  tau = +INFINITY with
@@ -56,6 +62,18 @@ typedef enum {
 
 typedef enum { INCVIT_F32 = 0, INCVIT_BF16 = 1 } incvit_dtype;
 
+/* What the cosine of eq. 3 compares, per token (both in fp32, fixed order):
+ *   INCVIT_SCORE_EMBED: T[i] = patch embedding + position (the layer-1 input);
+ *   INCVIT_SCORE_KEY:   the first layer's key, LN1(S(T[i])) W_K + b_K with
+ *     layer 0's LayerNorm and key columns, S = rounding to the storage type:
+ *     mean and variance from 64 lane partials (lane j takes d = j, j+64, ...
+ *     in increasing d; the sum with adds, the squares of x - mean with fma)
+ *     combined by the halving tree 32,16,..,1, each divided by D;
+ *     rstd = 1 / sqrt(var + eps); n_d = fma((x_d - mean) * rstd, gamma_d, beta_d);
+ *     key_e = fma chain over d = 0..D-1 of n_d * W_K[d][e] started at b_K[e].
+ *     Costs D*D fma per token more than the embedding score. */
+typedef enum { INCVIT_SCORE_EMBED = 0, INCVIT_SCORE_KEY = 1 } incvit_score;
+
 /* Model and limits.  N = (img_h/patch)*(img_w/patch) tokens, P = channels*patch^2
  * patch features, D = dim, L = depth, h = heads, d_h = D/h, F = mlp_dim.
  * Supported: img_h, img_w multiples of patch; D % 32 == 0; D % h == 0;
@@ -68,6 +86,7 @@ typedef struct {
   int32_t dtype;       /* incvit_dtype */
   float ln_eps;        /* e.g. 1e-6 */
   int32_t max_streams; /* largest B accepted by a call */
+  int32_t score;       /* incvit_score; part of the cache identity */
 } incvit_config;
 
 typedef struct incvit_handle incvit_handle;
@@ -109,9 +128,10 @@ incvit_status incvit_create(const incvit_config* cfg, const void* packed_weights
 void incvit_destroy(incvit_handle* h);
 
 /* Bytes of one stream's cache (device layout, 256-byte aligned parts): a header
- * (magic, config hash, status word), ref [N][D] fp32 (each token's embedding
- * at its last refresh), X [L+1][N][D] (layer inputs), K and V of every layer,
- * Y [N][D] (final output).  Base addresses must be 256-byte aligned. */
+ * (magic, config hash, status word), ref [N][D] fp32 (each token's score
+ * vector -- embedding or first-layer key, per cfg.score -- at its last
+ * refresh), X [L+1][N][D] (layer inputs), K and V of every layer, Y [N][D]
+ * (final output).  Base addresses must be 256-byte aligned. */
 size_t incvit_cache_bytes(const incvit_handle* h);
 
 /* Bytes of one stream's cache in the canonical (export) layout:
@@ -150,6 +170,17 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches,
                           void* const* caches, float tau, const int32_t* cap,
                           int32_t* idx, int32_t* count, void* refreshed,
                           void* workspace, void* stream);
+
+/* One frame of a stream under a refresh period (§III-B, odd/even chunks for
+ * period 2): if frame_index % period == 0 the frame is encoded in full (every
+ * cache row and reference replaced) and reported as a step that refreshed
+ * every token: idx[v][i] = i, count[v] = N, refreshed rows = Y; otherwise it
+ * is incvit_step with the same arguments.  period >= 1, frame_index >= 0
+ * (host values).  Same buffers, errors and asynchrony as incvit_step. */
+incvit_status incvit_encode_frame(incvit_handle* h, int32_t B, const float* patches,
+                                  void* const* caches, int64_t frame_index, int32_t period,
+                                  float tau, const int32_t* cap, int32_t* idx, int32_t* count,
+                                  void* refreshed, void* workspace, void* stream);
 
 /* ----------------------------------------------------------- cache state -- */
 
@@ -230,6 +261,8 @@ typedef enum {
   INCVIT_K_FC1,       /* LN2 + MLP up projection + GELU                   */
   INCVIT_K_FC2,       /* MLP down projection (split-K partial sums)       */
   INCVIT_K_RES_LN1,   /* + bias + residual -> X^{l+1}; final LN (last)    */
+  INCVIT_K_KEY_LN,    /* key score: LayerNorm 1 of layer 0, all tokens    */
+  INCVIT_K_KEY_PROJ,  /* key score: key projection, all tokens            */
   INCVIT_K_COUNT
 } incvit_kernel_kind;
 

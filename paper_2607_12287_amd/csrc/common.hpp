@@ -32,6 +32,7 @@ struct Shape {
   int dtype;  // 0 = fp32, 1 = bf16
   int eb;     // element bytes of the storage dtype
   float eps;
+  int score;  // 0: the cosine compares embedded tokens; 1: first-layer keys
 };
 
 // Byte offsets inside one stream's cache.
@@ -94,17 +95,31 @@ struct LayerW {
 
 // ---------------------------------------------------------------- kernels --
 
+// Fixed-order fp32 product of token rows with a storage-type matrix: the patch
+// embedding (x = patches, K = P, W = W_pe, + Pos) and the key projection of
+// the key score (x = LayerNorm rows, K = D, W = W_K, pos = null).
 struct EmbedArgs {
-  const float* patches;  // [B][N][P]
+  const float* patches;  // [B][N][P] (P = K, the row length of x)
   const void* w_pe;      // [P][D] storage dtype
   const float* b_pe;     // [D]
-  const float* pos;      // [N][D]
+  const float* pos;      // [N][D], or null: nothing added after the chain
   float* t0;             // [B][N][D]
   int B, N, P, D, dtype;
   int* zero;             // counters to clear (may be null)
   int nzero;
   int* ident_idx;        // if set: idx[v][i] = i, count[v] = N
   int* ident_count;
+};
+
+// Key score, first part: LayerNorm 1 of layer 0 of every token's stored
+// layer-0 input, fixed order (one wave per token).
+struct KeyLnArgs {
+  const float* t0;     // [rows][D] embedded tokens
+  const float* ln_g;   // [D] layer-0 LayerNorm 1
+  const float* ln_b;
+  float* out;          // [rows][D]
+  int rows, D, dtype;
+  float eps;
 };
 
 struct SimArgs {
@@ -134,6 +149,7 @@ struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map
   CacheLayout cl;
   Shape sh;
   const float* t0;
+  const float* score;  // [B][N][D] score vectors: the new references of the rows
   int init_header;   // commit of a full encode: write header
   uint32_t hash;
   void* z;           // compact Z_0 [Mpad][D] (operand order)
@@ -254,6 +270,8 @@ hipError_t launch_k(void (*kernel)(A), dim3 grid, dim3 block, size_t lds, hipStr
 
 // launchers (return the launch error)
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+hipError_t launch_keyproj(const EmbedArgs& a, hipStream_t s);
+hipError_t launch_keyln(const KeyLnArgs& a, hipStream_t s);
 hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);

@@ -30,6 +30,7 @@ struct PackedLayer {
 
 struct PackedLayout {
   size_t w_pe, b_pe, pos, lnf_g, lnf_b, total;
+  size_t w_key;  // W_K of layer 0, [D][D] storage dtype (key score)
   std::vector<PackedLayer> layers;
 };
 
@@ -39,7 +40,7 @@ struct CanonLayout {  // element offsets into the canonical buffer
 };
 
 struct WsLayout {
-  size_t meta, rows, count, idx, sim, t0, z, q, o, h, g, part, total;
+  size_t meta, rows, count, idx, sim, t0, kn, key, z, q, o, h, g, part, total;
   int Mpad;
 };
 
@@ -58,6 +59,7 @@ bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::strin
   if (c->dim % c->heads) { err = "dim is not a multiple of heads"; return false; }
   if (!(c->ln_eps > 0.0f) || !std::isfinite(c->ln_eps)) { err = "ln_eps must be positive and finite"; return false; }
   if (c->dtype != INCVIT_F32 && c->dtype != INCVIT_BF16) { st = INCVIT_ERR_UNSUPPORTED; err = "dtype must be INCVIT_F32 or INCVIT_BF16"; return false; }
+  if (c->score != INCVIT_SCORE_EMBED && c->score != INCVIT_SCORE_KEY) { st = INCVIT_ERR_ARG; err = "score must be INCVIT_SCORE_EMBED or INCVIT_SCORE_KEY"; return false; }
   sh.N = (c->img_h / c->patch) * (c->img_w / c->patch);
   sh.P = c->channels * c->patch * c->patch;
   sh.D = c->dim;
@@ -71,6 +73,7 @@ bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::strin
   sh.dtype = c->dtype;
   sh.eb = c->dtype == INCVIT_BF16 ? 2 : 4;
   sh.eps = c->ln_eps;
+  sh.score = c->score;
   st = INCVIT_ERR_UNSUPPORTED;
   if (sh.D % 32) { err = "dim must be a multiple of 32"; return false; }
   if (sh.D > kMaxDim) { snprintf(buf, sizeof buf, "dim must be <= %d", kMaxDim); err = buf; return false; }
@@ -115,6 +118,7 @@ PackedLayout packed_layout(const Shape& sh) {
   }
   p.lnf_g = take(D * 4);
   p.lnf_b = take(D * 4);
+  p.w_key = take((size_t)D * D * eb);
   p.total = off;
   return p;
 }
@@ -165,7 +169,7 @@ CacheLayout cache_layout(const Shape& sh) {
 }
 
 uint32_t config_hash(const incvit_config& c) {
-  const int32_t f[10] = {c.img_h, c.img_w, c.channels, c.patch, c.dim, c.depth, c.heads, c.mlp_dim, c.dtype, 0};
+  const int32_t f[10] = {c.img_h, c.img_w, c.channels, c.patch, c.dim, c.depth, c.heads, c.mlp_dim, c.dtype, c.score};
   uint32_t h = 2166136261u;
   auto mix = [&](uint32_t x) {
     for (int i = 0; i < 4; ++i) {
@@ -173,7 +177,7 @@ uint32_t config_hash(const incvit_config& c) {
       h *= 16777619u;
     }
   };
-  for (int i = 0; i < 9; ++i) mix((uint32_t)f[i]);
+  for (int i = 0; i < 10; ++i) mix((uint32_t)f[i]);
   uint32_t e;
   memcpy(&e, &c.ln_eps, 4);
   mix(e);
@@ -234,6 +238,9 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.idx = take((size_t)M * 4);
   w.sim = take((size_t)M * 4);
   w.t0 = take((size_t)M * sh.D * 4);
+  // key score: LayerNorm rows and keys of every token (key mode only)
+  w.kn = take(sh.score ? (size_t)M * sh.D * 4 : 0);
+  w.key = take(sh.score ? (size_t)M * sh.D * 4 : 0);
   w.z = take((size_t)w.Mpad * sh.D * sh.eb);
   w.q = take((size_t)w.Mpad * sh.D * sh.eb);
   w.o = take((size_t)w.Mpad * sh.D * sh.eb);
@@ -456,6 +463,69 @@ incvit_status check_common(incvit_handle* h, int32_t B, const float* patches, vo
   return INCVIT_OK;
 }
 
+// The score vectors of every token of the call: the embedded tokens t0, or in
+// key mode their first-layer keys (LayerNorm 1 of layer 0, then W_K), both in
+// the fixed fp32 order.  Returns the buffer the cosine and the commit read.
+incvit_status score_pass(incvit_handle* h, int B, char* ws, const WsLayout& wl, const float** out, hipStream_t s) {
+  const Shape& sh = h->sh;
+  const float* t0 = reinterpret_cast<const float*>(ws + wl.t0);
+  *out = t0;
+  if (!sh.score) return INCVIT_OK;
+  float* kn = reinterpret_cast<float*>(ws + wl.kn);
+  float* key = reinterpret_cast<float*>(ws + wl.key);
+  const PackedLayer& L0 = h->pl.layers[0];
+  KeyLnArgs ka{t0, fptr(h, L0.ln1_g), fptr(h, L0.ln1_b), kn, B * sh.N, sh.D, sh.dtype, sh.eps};
+  incvit_status st = run(h, INCVIT_K_KEY_LN, s, [&] { return launch_keyln(ka, s); });
+  if (st != INCVIT_OK) return st;
+  EmbedArgs pa{kn, h->packed + h->pl.w_key, fptr(h, L0.b_qkv) + sh.D, nullptr, key,
+               B, sh.N, sh.D, sh.D, sh.dtype, nullptr, 0, nullptr, nullptr};
+  st = run(h, INCVIT_K_KEY_PROJ, s, [&] { return launch_keyproj(pa, s); });
+  if (st != INCVIT_OK) return st;
+  *out = key;
+  return INCVIT_OK;
+}
+
+// Full forward of B frames.  idx/count (device) receive the identity row map
+// (every token refreshed) when given, else the workspace's own copy does;
+// refreshed (optional) receives Y of every token.
+incvit_status full_impl(incvit_handle* h, int32_t B, const float* patches, void* const* caches, int32_t* out_idx,
+                        int32_t* out_count, void* refreshed, void* workspace, void* stream) {
+  incvit_status st = check_common(h, B, patches, workspace);
+  if (st != INCVIT_OK) return st;
+  if (reinterpret_cast<uintptr_t>(refreshed) % 16) return fail(h, INCVIT_ERR_ARG, "refreshed must be 16-byte aligned");
+  Views views;
+  if ((st = check_views(h, B, caches, views)) != INCVIT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Shape& sh = h->sh;
+  char* ws = static_cast<char*>(workspace);
+  const WsLayout wl = ws_layout(sh, B);
+  int* count = out_count ? out_count : reinterpret_cast<int*>(ws + wl.count);
+  int* idx = out_idx ? out_idx : reinterpret_cast<int*>(ws + wl.idx);
+  float* t0 = reinterpret_cast<float*>(ws + wl.t0);
+
+  EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
+               B, sh.N, sh.P, sh.D, sh.dtype, nullptr, 0, idx, count};
+  if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
+  const float* score = nullptr;
+  if ((st = score_pass(h, B, ws, wl, &score, s)) != INCVIT_OK) return st;
+  const int mmax = B * sh.N;
+  RowsArgs ra;
+  memset(&ra, 0, sizeof ra);
+  ra.rm = RowMap{count, idx, B, sh.N};
+  ra.rows = reinterpret_cast<RowInfo*>(ws + wl.rows);
+  ra.meta = reinterpret_cast<Meta*>(ws + wl.meta);
+  ra.caches = views;
+  ra.cl = h->cl;
+  ra.sh = sh;
+  ra.t0 = t0;
+  ra.score = score;
+  ra.init_header = 1;
+  ra.hash = h->hash;
+  ra.z = ws + wl.z;
+  if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
+  return run_layers(h, views, B, wl, ws, sh.N, mmax, true, refreshed, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -534,6 +604,10 @@ incvit_status incvit_pack_weights(const incvit_config* cfg, const void* canonica
   }
   conv(cn.lnf_g, pl.lnf_g, D, D);
   conv(cn.lnf_b, pl.lnf_b, D, D);
+  // W_K of layer 0 as its own [D][D] matrix (columns D..2D-1 of W_qkv) for the key score
+  if (e == hipSuccess)
+    e = hipMemcpy2DAsync(dst + pl.w_key, (size_t)D * eb, src + (cn.layers[0].w_qkv + D) * eb, (size_t)3 * D * eb,
+                         (size_t)D * eb, D, hipMemcpyDeviceToDevice, s);
   if (e != hipSuccess) return fail(nullptr, INCVIT_ERR_HIP, std::string("pack: ") + hipGetErrorString(e));
   return INCVIT_OK;
 }
@@ -584,36 +658,7 @@ size_t incvit_workspace_bytes(const incvit_handle* h, int32_t B) {
 
 incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patches, void* const* caches,
                                  void* workspace, void* stream) {
-  incvit_status st = check_common(h, B, patches, workspace);
-  if (st != INCVIT_OK) return st;
-  Views views;
-  if ((st = check_views(h, B, caches, views)) != INCVIT_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Shape& sh = h->sh;
-  char* ws = static_cast<char*>(workspace);
-  const WsLayout wl = ws_layout(sh, B);
-  int* count = reinterpret_cast<int*>(ws + wl.count);
-  int* idx = reinterpret_cast<int*>(ws + wl.idx);
-  float* t0 = reinterpret_cast<float*>(ws + wl.t0);
-
-  EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
-               B, sh.N, sh.P, sh.D, sh.dtype, nullptr, 0, idx, count};
-  if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
-  const int mmax = B * sh.N;
-  RowsArgs ra;
-  memset(&ra, 0, sizeof ra);
-  ra.rm = RowMap{count, idx, B, sh.N};
-  ra.rows = reinterpret_cast<RowInfo*>(ws + wl.rows);
-  ra.meta = reinterpret_cast<Meta*>(ws + wl.meta);
-  ra.caches = views;
-  ra.cl = h->cl;
-  ra.sh = sh;
-  ra.t0 = t0;
-  ra.init_header = 1;
-  ra.hash = h->hash;
-  ra.z = ws + wl.z;
-  if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
-  return run_layers(h, views, B, wl, ws, sh.N, mmax, true, nullptr, s);
+  return full_impl(h, B, patches, caches, nullptr, nullptr, nullptr, workspace, stream);
 }
 
 incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, void* const* caches, float tau,
@@ -646,7 +691,9 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   EmbedArgs ea{patches, h->packed + h->pl.w_pe, fptr(h, h->pl.b_pe), fptr(h, h->pl.pos), t0,
                B, sh.N, sh.P, sh.D, sh.dtype, nullptr, 0, nullptr, nullptr};
   if ((st = run(h, INCVIT_K_EMBED, s, [&] { return launch_embed(ea, s); })) != INCVIT_OK) return st;
-  SimArgs si{t0, views, h->cl.ref, sim, B, sh.N, sh.D};
+  const float* score = nullptr;
+  if ((st = score_pass(h, B, ws, wl, &score, s)) != INCVIT_OK) return st;
+  SimArgs si{score, views, h->cl.ref, sim, B, sh.N, sh.D};
   if ((st = run(h, INCVIT_K_SIM, s, [&] { return launch_sim(si, s); })) != INCVIT_OK) return st;
   sa.sim = sim;
   sa.caches = views;
@@ -668,10 +715,24 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   ra.cl = h->cl;
   ra.sh = sh;
   ra.t0 = t0;
+  ra.score = score;
   ra.z = ws + wl.z;
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
   // with the threshold disabled every stream refreshes exactly its cap
   return run_layers(h, views, B, wl, ws, max_rows, mmax, std::isinf(tau) && tau > 0, refreshed, s);
+}
+
+incvit_status incvit_encode_frame(incvit_handle* h, int32_t B, const float* patches, void* const* caches,
+                                  int64_t frame_index, int32_t period, float tau, const int32_t* cap, int32_t* idx,
+                                  int32_t* count, void* refreshed, void* workspace, void* stream) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  if (period < 1) return fail(h, INCVIT_ERR_ARG, "period must be >= 1");
+  if (frame_index < 0) return fail(h, INCVIT_ERR_ARG, "frame_index must be >= 0");
+  if (frame_index % period == 0) {
+    if (!idx || !count) return fail(h, INCVIT_ERR_ARG, "idx and count must be non-null");
+    return full_impl(h, B, patches, caches, idx, count, refreshed, workspace, stream);
+  }
+  return incvit_step(h, B, patches, caches, tau, cap, idx, count, refreshed, workspace, stream);
 }
 
 incvit_status incvit_cache_export(const incvit_handle* h, const void* cache, void* canonical_dst, void* stream) {

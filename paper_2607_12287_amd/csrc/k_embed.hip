@@ -1,14 +1,19 @@
-// Patch embedding + position, and the per-token cosine similarity against the
-// cached reference (paper §III-B, eq. 3).
+// Patch embedding + position, the first-layer key score, and the per-token
+// cosine similarity against the cached reference (paper §III-B, eq. 3).
 //
-// Selection must be bit-reproducible, so both are computed in a fixed fp32
-// order with explicitly rounded operations (no contraction):
+// Selection must be bit-reproducible, so all three are computed in a fixed
+// fp32 order with explicitly rounded operations (no contraction):
 //   T[i][d] = fma-chain over k = 0..P-1 of x_i[k] * W_pe[k][d], started at
 //             b_pe[d], then one fp32 add of Pos[i][d];
+//   key score: x = S(T[i]); mean and variance of x from 64 lane partials
+//        (lane j takes d = j, j+64, ... in increasing d: adds for the sum, fma
+//        of (x - mean)^2 for the variance) and the halving tree, each / D;
+//        rstd = 1 / sqrt(var + eps); n_d = fma((x_d - mean) * rstd, g_d, b_d);
+//        key[e] = fma-chain over d of n_d * W_K[d][e] started at b_K[e];
 //   cos: lane j of a wave sums the terms d = j, j+64, ... with fma, the 64
 //        lane partials are combined by the halving tree (offsets 32..1), then
 //        dot / max(sqrt(|a|^2) * sqrt(|b|^2), 1e-8).
-// This is fp32 vector-ALU work (P*D fma per token).
+// This is fp32 vector-ALU work (P*D fma per token, D*D more for the key).
 #include "common.hpp"
 
 namespace incvit {
@@ -36,7 +41,7 @@ __device__ __forceinline__ void unpack16(float* f, const V8<float>& v) {
 // used because the k loop stops at P) and issued two tiles ahead, so a tile's
 // data arrives while the two before it are computed.
 template <class T>
-__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
+__device__ __forceinline__ void embed_body(const EmbedArgs& a) {
   constexpr int WV = 16 / sizeof(T);  // weights per 16-byte load
   constexpr int WL = 64 * 64 / (256 * WV);  // weight loads per thread per tile
   __shared__ __align__(16) float sx[64][16];  // [k][token]
@@ -106,12 +111,12 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 
   float acc[4];
   const float bias = a.b_pe[min(d, D - 1)];
-  float posv[4];
+  float posv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     acc[r] = bias;
     const int tok = min(tok0 + 4 * w + r, N - 1);
-    posv[r] = a.pos[(size_t)tok * D + min(d, D - 1)];
+    if (a.pos) posv[r] = a.pos[(size_t)tok * D + min(d, D - 1)];
   }
   Tile t0, t1;
   fetch(t0, 0);
@@ -137,8 +142,72 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int tok = tok0 + 4 * w + r;
-      if (tok < N) a.t0[((size_t)v * N + tok) * D + d] = __fadd_rn(acc[r], posv[r]);
+      if (tok < N) a.t0[((size_t)v * N + tok) * D + d] = a.pos ? __fadd_rn(acc[r], posv[r]) : acc[r];
     }
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
+  embed_body<T>(a);
+}
+
+// The key projection of the key score: the same fixed-order product with
+// x = LayerNorm rows, K = D, W = W_K of layer 0, no position term.
+template <class T>
+__global__ __launch_bounds__(256) void keyproj_kernel(EmbedArgs a) {
+  embed_body<T>(a);
+}
+
+// Correctly rounded fp32 square root.  HIP's __fsqrt_rn is the bare hardware
+// square root (about 1 ulp) unless OCML's rounded operations are enabled;
+// __builtin_sqrtf compiles to the hardware estimate plus the fma correction
+// that rounds it correctly (the fp32 divide is correctly rounded by default).
+__device__ __forceinline__ float sqrt_rn(float x) { return __builtin_sqrtf(x); }
+
+// Sum of the 64 lane values by the halving tree; lane 0's value is the
+// result, broadcast to the wave.
+__device__ __forceinline__ float tree64(float p) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) p = __fadd_rn(p, __shfl_down(p, off, 64));
+  return __shfl(p, 0, 64);
+}
+
+// One wave per token: n = LayerNorm 1 of layer 0 on S(T0[token]), fixed order.
+template <class T>
+__global__ __launch_bounds__(256) void keyln_kernel(KeyLnArgs a) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int row = blockIdx.x * 4 + w;
+  if (row >= a.rows) return;
+  const int D = a.D;
+  const float* x = a.t0 + (size_t)row * D;
+  constexpr int kPer = kMaxDim / 64;
+  float xv[kPer], g[kPer], b[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int d = lane + 64 * j;
+    xv[j] = d < D ? Elem<T>::rnd(x[d]) : 0.0f;
+    g[j] = d < D ? a.ln_g[d] : 0.0f;
+    b[j] = d < D ? a.ln_b[d] : 0.0f;
+  }
+  float p = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j)
+    if (lane + 64 * j < D) p = __fadd_rn(p, xv[j]);
+  const float mean = __fdiv_rn(tree64(p), (float)D);
+  float q = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    xv[j] = __fsub_rn(xv[j], mean);
+    if (lane + 64 * j < D) q = __fmaf_rn(xv[j], xv[j], q);
+  }
+  const float var = __fdiv_rn(tree64(q), (float)D);
+  const float rstd = __fdiv_rn(1.0f, sqrt_rn(__fadd_rn(var, a.eps)));
+  float* out = a.out + (size_t)row * D;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int d = lane + 64 * j;
+    if (d < D) out[d] = __fmaf_rn(__fmul_rn(xv[j], rstd), g[j], b[j]);
   }
 }
 
@@ -174,7 +243,7 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
     pb = __fadd_rn(pb, __shfl_down(pb, off, 64));
   }
   if (lane == 0) {
-    const float denom = __fmul_rn(__fsqrt_rn(pa), __fsqrt_rn(pb));
+    const float denom = __fmul_rn(sqrt_rn(pa), sqrt_rn(pb));
     a.sim[gt] = __fdiv_rn(pd, fmaxf(denom, 1e-8f));
   }
 }
@@ -183,6 +252,18 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
   if (a.dtype) return launch_k(embed_kernel<uint16_t>, grid, dim3(256), 0, s, a);
   return launch_k(embed_kernel<float>, grid, dim3(256), 0, s, a);
+}
+
+hipError_t launch_keyproj(const EmbedArgs& a, hipStream_t s) {
+  dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
+  if (a.dtype) return launch_k(keyproj_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  return launch_k(keyproj_kernel<float>, grid, dim3(256), 0, s, a);
+}
+
+hipError_t launch_keyln(const KeyLnArgs& a, hipStream_t s) {
+  dim3 grid((a.rows + 3) / 4);
+  if (a.dtype) return launch_k(keyln_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  return launch_k(keyln_kernel<float>, grid, dim3(256), 0, s, a);
 }
 
 hipError_t launch_sim(const SimArgs& a, hipStream_t s) {

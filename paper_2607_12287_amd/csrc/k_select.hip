@@ -188,7 +188,8 @@ __device__ __forceinline__ void store4v(uint16_t* p, float4 v) {
   *reinterpret_cast<uint2*>(p) = make_uint2(f2bf2(v.x, v.y), f2bf2(v.z, v.w));
 }
 
-// One workgroup per compact row r: ref[tok] = T0[tok] (fp32), X0[tok] = S(T0[tok]),
+// One workgroup per compact row r: ref[tok] = score[tok] (fp32: the embedded
+// token or its first-layer key), X0[tok] = S(T0[tok]),
 // the compact Z0 row (operand order, the layer-0 input), and the row's entry in
 // the row map.  Block 0 also publishes M and the per-stream row offsets.
 // Thread t owns float4 slots t + 256 j of the row (D <= 1024 * KP).
@@ -228,6 +229,7 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
   const int tok = a.rm.idx[v * N + (r - s_off[v])];
   char* cache = a.caches.p[v];
   const float4* src = reinterpret_cast<const float4*>(a.t0 + ((size_t)v * N + tok) * D);
+  const float4* sc = reinterpret_cast<const float4*>(a.score + ((size_t)v * N + tok) * D);
   float4* ref = reinterpret_cast<float4*>(cache + a.cl.ref + (size_t)tok * D * 4);
   T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
   T* z0 = static_cast<T*>(a.z);  // operand order (frag_off)
@@ -237,7 +239,7 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
     if (q < D4) {
       const float4 t = src[q];
       const float4 zr = make_float4(Elem<T>::rnd(t.x), Elem<T>::rnd(t.y), Elem<T>::rnd(t.z), Elem<T>::rnd(t.w));
-      ref[q] = t;
+      ref[q] = sc[q];
       store4v(x0 + 4 * q, zr);
       store4v(z0 + frag_off(r, 4 * q, D / 32), zr);
     }

@@ -20,7 +20,10 @@ INCVIT_OK, INCVIT_ERR_ARG, INCVIT_ERR_SHAPE, INCVIT_ERR_UNSUPPORTED, INCVIT_ERR_
 STATUS_NAMES = {0: "INCVIT_OK", -1: "INCVIT_ERR_ARG", -2: "INCVIT_ERR_SHAPE", -3: "INCVIT_ERR_UNSUPPORTED",
                 -4: "INCVIT_ERR_STATE", -5: "INCVIT_ERR_HIP"}
 INCVIT_F32, INCVIT_BF16 = 0, 1
-KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "fc1", "fc2", "res_ln1")
+INCVIT_SCORE_EMBED, INCVIT_SCORE_KEY = 0, 1
+SCORES = {"embed": INCVIT_SCORE_EMBED, "key": INCVIT_SCORE_KEY}
+KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "fc1", "fc2", "res_ln1",
+                "key_ln", "key_proj")
 
 # Exported symbols, as declared in include/incvit.h.
 EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "incvit_pack_weights",
@@ -28,14 +31,14 @@ EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "inc
            "incvit_workspace_bytes", "incvit_full_encode", "incvit_step", "incvit_cache_export",
            "incvit_cache_import", "incvit_cache_status", "incvit_last_error", "incvit_profile_enable",
            "incvit_profile_read", "incvit_step_graph_create", "incvit_full_graph_create",
-           "incvit_graph_launch", "incvit_graph_destroy", "incvit_set_tuning")
+           "incvit_graph_launch", "incvit_graph_destroy", "incvit_set_tuning", "incvit_encode_frame")
 
 
 class incvit_config(ctypes.Structure):
     _fields_ = [("img_h", ctypes.c_int32), ("img_w", ctypes.c_int32), ("channels", ctypes.c_int32),
                 ("patch", ctypes.c_int32), ("dim", ctypes.c_int32), ("depth", ctypes.c_int32),
                 ("heads", ctypes.c_int32), ("mlp_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("ln_eps", ctypes.c_float), ("max_streams", ctypes.c_int32)]
+                ("ln_eps", ctypes.c_float), ("max_streams", ctypes.c_int32), ("score", ctypes.c_int32)]
 
 
 class incvit_tuning(ctypes.Structure):
@@ -81,6 +84,7 @@ def lib() -> ctypes.CDLL:
             "incvit_graph_launch": (I32, [P, P]),
             "incvit_graph_destroy": (None, [P]),
             "incvit_set_tuning": (I32, [P, ctypes.POINTER(incvit_tuning)]),
+            "incvit_encode_frame": (I32, [P, I32, P, P, ctypes.c_int64, I32, F32, P, P, P, P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -147,6 +151,14 @@ def incvit_step(h, B: int, patches: int, caches: Sequence[int], tau: float, cap:
                              refreshed, workspace, stream)
 
 
+def incvit_encode_frame(h, B: int, patches: int, caches: Sequence[int], frame_index: int, period: int, tau: float,
+                        cap: Sequence[int], idx: int, count: int, refreshed: int, workspace: int,
+                        stream: int = 0) -> int:
+    caps = (ctypes.c_int32 * B)(*[int(c) for c in cap])
+    return lib().incvit_encode_frame(h, B, patches, _ptr_array(caches), int(frame_index), int(period), float(tau),
+                                     caps, idx, count, refreshed, workspace, stream)
+
+
 def incvit_cache_export(h, cache: int, dst: int, stream: int = 0) -> int:
     return lib().incvit_cache_export(h, cache, dst, stream)
 
@@ -208,23 +220,26 @@ def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None, attn_qtiles: int 
 
 # --- convenience wrapper -------------------------------------------------------
 
-def make_config(shape, max_streams: int = 1) -> incvit_config:
+def make_config(shape, max_streams: int = 1, score: str = "embed") -> incvit_config:
     """Config from a model shape with attributes img_h, img_w, channels, patch,
-    dim, depth, heads, mlp_dim, dtype ('f32'/'bf16'), ln_eps."""
+    dim, depth, heads, mlp_dim, dtype ('f32'/'bf16'), ln_eps; score is 'embed'
+    or 'key' (what the cosine compares)."""
     return incvit_config(shape.img_h, shape.img_w, shape.channels, shape.patch, shape.dim, shape.depth,
                          shape.heads, shape.mlp_dim, INCVIT_BF16 if shape.dtype == "bf16" else INCVIT_F32,
-                         float(shape.ln_eps), int(max_streams))
+                         float(shape.ln_eps), int(max_streams), SCORES[score])
 
 
 class Encoder:
     """Device-resident encoder: packed weights, per-stream caches, workspace."""
 
-    def __init__(self, shape, canonical_weights, max_streams: int = 1, device: str = "cuda"):
+    def __init__(self, shape, canonical_weights, max_streams: int = 1, device: str = "cuda",
+                 score: str = "embed"):
         import torch
         self.torch = torch
         self.shape = shape
+        self.score = score
         self.device = torch.device(device)
-        self.cfg = make_config(shape, max_streams)
+        self.cfg = make_config(shape, max_streams, score)
         self.dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
         self.N = shape.n_tokens
         self.D = shape.dim
@@ -298,6 +313,25 @@ class Encoder:
         _check(incvit_step(self.h, B, patches.data_ptr(), caches, tau, cap, idx.data_ptr(), count.data_ptr(),
                            refreshed.data_ptr() if refreshed is not None else 0, self.workspace(B).data_ptr(),
                            self.stream_ptr()), self.h)
+        return idx, count, refreshed
+
+    def encode_frame(self, patches, caches: Sequence[int], frame_index: int, period: int, tau: float,
+                     cap: Sequence[int], out=None):
+        """One frame under a refresh period (full encode when frame_index % period
+        == 0, else a step); returns (idx, count, refreshed) like step."""
+        B = len(caches)
+        torch = self.torch
+        assert patches.is_cuda and patches.dtype == torch.float32 and patches.is_contiguous()
+        assert tuple(patches.shape) == (B, self.N, self.shape.patch_dim)
+        if out is None:
+            out = (torch.empty((B, self.N), dtype=torch.int32, device=self.device),
+                   torch.empty((B,), dtype=torch.int32, device=self.device),
+                   torch.empty((B, self.N, self.D), dtype=self.dtype, device=self.device))
+        idx, count, refreshed = out
+        _check(incvit_encode_frame(self.h, B, patches.data_ptr(), caches, frame_index, period, tau, cap,
+                                   idx.data_ptr(), count.data_ptr(),
+                                   refreshed.data_ptr() if refreshed is not None else 0,
+                                   self.workspace(B).data_ptr(), self.stream_ptr()), self.h)
         return idx, count, refreshed
 
     def step_graph(self, patches, caches: Sequence[int], tau: float, cap: Sequence[int], out):

@@ -3,8 +3,9 @@ same seeded inputs and compare them.
 
 Bars:
 * token indices and counts bit-exact; the fp32 reference rows (`ref`, each
-  token's embedding at its last refresh) and the layer-0 rows bit-exact, since
-  the embedding is computed in the same fixed fp32 order on both sides;
+  token's score vector -- embedding or first-layer key -- at its last refresh)
+  and the layer-0 rows bit-exact, since the embedding and the key score are
+  computed in the same fixed fp32 order on both sides;
 * per layer, teacher-forced: the oracle's layer applied to the GPU's own cached
   inputs of that layer gives the GPU's outputs (X^{l+1}, K^l, V^l, and Y)
   within max|gpu - oracle| / max|oracle| <= 2e-2 (bf16 storage) or 1e-4 (fp32);
@@ -41,10 +42,10 @@ def rel_err(a: np.ndarray, b: np.ndarray) -> float:
 class Pair:
     """The HIP encoder and the oracle on the same model and weights."""
 
-    def __init__(self, m: synth.ModelShape, w, B: int, oracle_views=None):
+    def __init__(self, m: synth.ModelShape, w, B: int, oracle_views=None, score: str = "embed"):
         self.m, self.w, self.B = m, w, B
-        self.enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=B)
-        self.model = vit.Model(m, w)
+        self.enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=B, score=score)
+        self.model = vit.Model(m, w, score=score)
         self.buf, self.caches = self.enc.new_caches(B)
         self.views = list(range(B)) if oracle_views is None else list(oracle_views)
         self.ora = {}
@@ -81,7 +82,9 @@ class Pair:
             g = self.enc.export(self.caches[v])
             U = np.arange(m.n_tokens) if U_of is None else np.asarray(U_of(v))
             assert np.array_equal(g["ref"], self.ora[v].ref), (label, v, "ref")
-            assert np.array_equal(g["X"][0][U], vit.S(g["ref"][U].astype(np.float64), dt)), (label, v, "X0")
+            assert np.array_equal(g["X"][0][U], self.ora[v].X[0][U]), (label, v, "X0")
+            if self.model.score == "embed":
+                assert np.array_equal(g["X"][0][U], vit.S(g["ref"][U].astype(np.float64), dt)), (label, v, "X0")
             if U.size == 0:
                 continue
             for l in range(m.depth):
@@ -112,3 +115,32 @@ class Pair:
             worst = max(worst, e)
             assert e <= tol, (label, v, "Y", e)
         return worst
+
+
+def workspace_arrays(enc, B: int):
+    """The per-token fp32 arrays of the last call, read from the library's
+    workspace through a mirror of its layout (256-byte aligned parts: meta,
+    row map, counts, idx, sim, T0, then in key mode the LayerNorm rows and the
+    keys).  Tests check T0 against the oracle first, which validates the mirror."""
+    N, D = enc.N, enc.D
+    M = B * N
+    mpad = (max(M, 1) + 63) // 64 * 64
+    offs, off = {}, 0
+    sizes = [("meta", 4 + 65 * 4), ("rows", mpad * 16), ("count", 64 * 4), ("idx", M * 4), ("sim", M * 4),
+             ("t0", M * D * 4)]
+    if enc.score == "key":
+        sizes += [("kn", M * D * 4), ("key", M * D * 4)]
+    for name, n in sizes:
+        offs[name] = off
+        off = (off + n + 255) // 256 * 256
+    ws = enc.workspace(B)
+    torch.cuda.synchronize()
+
+    def f32(name, shape):
+        o = offs[name]
+        return ws[o:o + int(np.prod(shape)) * 4].view(torch.float32).reshape(shape).cpu().numpy()
+
+    out = {"sim": f32("sim", (B, N)), "t0": f32("t0", (B, N, D))}
+    if enc.score == "key":
+        out["key"] = f32("key", (B, N, D))
+    return out

@@ -40,6 +40,7 @@ def test_sizes_match_canonical_layout():
     ("dtype", 7, incvit.INCVIT_ERR_UNSUPPORTED),
     ("max_streams", 0, incvit.INCVIT_ERR_UNSUPPORTED),
     ("ln_eps", float("nan"), incvit.INCVIT_ERR_SHAPE),
+    ("score", 7, incvit.INCVIT_ERR_ARG),
 ])
 def test_invalid_configs_are_rejected_before_any_device_work(field, value, status):
     cfg = incvit.make_config(synth.small_model(dtype="bf16"), 2)
