@@ -34,6 +34,15 @@ The paper's odd/even chunk schedule (a full forward on odd chunks whose keys
 become the reference, incremental encoding on even chunks) is
 ``run_schedule`` with period 2; other periods generalise it.
 
+What "all tokens are processed by the MLP layer" means (``Model.mlp``):
+"reuse" (default) reads it exactly: a reused row's MLP input is its cached
+state, so its MLP output is its cached output and only the rows U need
+computing.  "all" is the non-exact reading: every frame, every row starts from
+this frame's embedded token, reused rows add their cached attention-branch
+output (attention + output projection, per layer) to their current residual
+stream, and the MLP runs over all rows, so reused rows follow the new frame
+without their attention being recomputed (their K and V stay cached).
+
 Arithmetic: everything is float64 except the patch embedding, the key score
 and the cosine, which follow a fixed fp32 order (``pinned.c``) so that the
 selection is reproducible bit for bit. ``S(.)`` rounds to the storage precision (bf16 with
@@ -137,21 +146,25 @@ def select(sim: np.ndarray, tau: float, cap: int) -> np.ndarray:
 
 
 SCORES = ("embed", "key")
+MLPS = ("reuse", "all")
 
 
 class Model:
     """Weights of the encoder as float64 arrays (values as stored).
 
     score: "embed" (cosine of the embedded tokens) or "key" (cosine of the
-    first layer's keys, eq. 3)."""
+    first layer's keys, eq. 3); mlp: "reuse" or "all" (see the module text)."""
 
     def __init__(self, shape, weights: Dict[str, np.ndarray], dtype: Optional[str] = None,
-                 score: str = "embed"):
+                 score: str = "embed", mlp: str = "reuse"):
         if score not in SCORES:
             raise ValueError(f"score must be one of {SCORES}")
+        if mlp not in MLPS:
+            raise ValueError(f"mlp must be one of {MLPS}")
         self.shape = shape
         self.dtype = dtype or shape.dtype
         self.score = score
+        self.mlp = mlp
         self.eps = float(shape.ln_eps)
         self.w = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
         self.w32 = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in
@@ -176,16 +189,20 @@ class ViewCache:
     key, per Model.score) at its last refresh: the reference the cosine is
     taken against;
     X: [L+1][N][D] layer inputs (X[0] = embedded tokens, X[l+1] = layer l out);
-    K, V: [L][N][D] per-layer keys and values;  Y: [N][D] final output."""
+    K, V: [L][N][D] per-layer keys and values;  Y: [N][D] final output;
+    A: [L][N][D] attention-branch outputs S(O W_o + b_o) per layer (mlp "all"
+    only, else None)."""
 
     ref: np.ndarray
     X: np.ndarray
     K: np.ndarray
     V: np.ndarray
     Y: np.ndarray
+    A: Optional[np.ndarray] = None
 
     def copy(self) -> "ViewCache":
-        return ViewCache(self.ref.copy(), self.X.copy(), self.K.copy(), self.V.copy(), self.Y.copy())
+        return ViewCache(self.ref.copy(), self.X.copy(), self.K.copy(), self.V.copy(), self.Y.copy(),
+                         None if self.A is None else self.A.copy())
 
 
 @dataclasses.dataclass
@@ -246,6 +263,33 @@ def layer_rows(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray
     return S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
 
 
+def layer_all(model: Model, l: int, X: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
+              A: np.ndarray, trace: Optional[dict] = None) -> np.ndarray:
+    """Layer l in the "all" reading: attention for the rows U only (new K/V
+    rows scattered first), their attention-branch outputs S(O W_o + b_o) into
+    A; every row then adds its A row (new for U, cached for the rest) to its
+    current input and goes through the MLP.  X: [N][D] inputs of all rows;
+    returns the [N][D] outputs."""
+    m, dt = model.shape, model.dtype
+    D = m.dim
+    if U.size:
+        Z = X[U]
+        A1 = S(layer_norm(Z, model.p(l, "ln1_g"), model.p(l, "ln1_b"), model.eps), dt)
+        qkv = S(A1 @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)
+        K[U] = qkv[:, D:2 * D]
+        V[U] = qkv[:, 2 * D:]
+        O = S(attention(qkv[:, :D], K, V, m.heads), dt)
+        A[U] = S(O @ model.p(l, "w_o") + model.p(l, "b_o"), dt)
+        if trace is not None:
+            trace.setdefault("O", []).append(O)
+    Hres = S(X + A, dt)
+    if trace is not None:
+        trace.setdefault("H", []).append(Hres)
+    A2 = S(layer_norm(Hres, model.p(l, "ln2_g"), model.p(l, "ln2_b"), model.eps), dt)
+    G = S(gelu_tanh(A2 @ model.p(l, "w_1") + model.p(l, "b_1")), dt)
+    return S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
+
+
 def final_rows(model: Model, Z: np.ndarray) -> np.ndarray:
     """Final LayerNorm of the last layer's output rows."""
     return S(layer_norm(Z, model.w["lnf_g"], model.w["lnf_b"], model.eps), model.dtype)
@@ -268,18 +312,34 @@ def _encode_rows(model: Model, cache: ViewCache, U: np.ndarray, t0: np.ndarray, 
     cache.Y[U] = final_rows(model, Z)
 
 
+def _encode_all(model: Model, cache: ViewCache, U: np.ndarray, t0: np.ndarray, sv: np.ndarray,
+                trace: Optional[dict] = None) -> None:
+    """The "all" reading of one frame: rows U are refreshed (new reference,
+    new Q/K/V and attention); every row's layer-0 input is this frame's
+    embedded token and every row goes through every MLP."""
+    cache.ref[U] = sv[U]
+    X = S(t0.astype(np.float64), model.dtype)
+    cache.X[0] = X
+    for l in range(model.shape.depth):
+        X = layer_all(model, l, X, U, cache.K[l], cache.V[l], cache.A[l], trace)
+        cache.X[l + 1] = X
+    cache.Y = final_rows(model, X)
+
+
 def empty_cache(model: Model) -> ViewCache:
     m = model.shape
     N, D, L = m.n_tokens, m.dim, m.depth
     return ViewCache(ref=np.zeros((N, D), np.float32), X=np.zeros((L + 1, N, D)),
-                     K=np.zeros((L, N, D)), V=np.zeros((L, N, D)), Y=np.zeros((N, D)))
+                     K=np.zeros((L, N, D)), V=np.zeros((L, N, D)), Y=np.zeros((N, D)),
+                     A=np.zeros((L, N, D)) if model.mlp == "all" else None)
 
 
 def full_encode(model: Model, patches: np.ndarray) -> ViewCache:
     """Full forward of one frame; fills every cache row (the paper's odd chunk)."""
     cache = empty_cache(model)
     t0 = embed(model, patches)
-    _encode_rows(model, cache, np.arange(model.shape.n_tokens), t0, score_vectors(model, t0))
+    encode = _encode_all if model.mlp == "all" else _encode_rows
+    encode(model, cache, np.arange(model.shape.n_tokens), t0, score_vectors(model, t0))
     return cache
 
 
@@ -290,7 +350,9 @@ def step(model: Model, patches: np.ndarray, cache: ViewCache, tau: float, cap: i
     sv = score_vectors(model, t0)
     sim = pinned.cosine_f32(sv, cache.ref)
     U = select(sim, tau, cap)
-    if U.size:
+    if model.mlp == "all":  # every row follows the new frame, even when U is empty
+        _encode_all(model, cache, U, t0, sv, trace)
+    elif U.size:
         _encode_rows(model, cache, U, t0, sv, trace)
     return StepResult(idx=U, sim=sim, refreshed=cache.Y[U].copy(), t0=t0, sv=sv)
 
