@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0
 ALU_PEAK_TFLOPS = 78.6
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PROFILES = os.path.join(ROOT, "profiles")
-GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj"}  # epilogue template argument
+GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj", "4": "oproj"}  # epilogue template argument
 
 
 def source_hash() -> str:
@@ -55,7 +55,7 @@ def kernel_kind(name: str):
         return GEMM_KIND.get(m.group(2).split(",")[1].strip())
     if m.group(1) == "res":
         return "res_ln1"
-    return m.group(1)
+    return {"keyln": "key_ln", "keyproj": "key_proj"}.get(m.group(1), m.group(1))
 
 
 def kinds_in_order(names):
@@ -184,17 +184,35 @@ def torch_full_forward(m, w, patches, repeats: int):
     return eager_ms, "eager"
 
 
-def measure_variant(wl, frames, score: str, period: int, steps: int, warmup: int, full_repeats: int):
+def approx_vs_full(enc, caches, frame):
+    """Informational approximation error of the incremental outputs: cosine of
+    each token's Y against a full encode of the same (last) frame, mean and
+    minimum over tokens and streams."""
+    import numpy as np
+    buf, scratch = enc.new_caches(len(caches))
+    enc.full_encode(frame, scratch)
+    cos = []
+    for c, sc in zip(caches, scratch):
+        a, b = enc.export(c)["Y"], enc.export(sc)["Y"]
+        cos.append((a * b).sum(1) / np.maximum(np.linalg.norm(a, axis=1) * np.linalg.norm(b, axis=1), 1e-30))
+    cos = np.concatenate(cos)
+    return {"mean": round(float(cos.mean()), 6), "min": round(float(cos.min()), 6)}
+
+
+def measure_variant(wl, frames, score: str, period: int, steps: int, warmup: int, full_repeats: int,
+                    mlp: str = "reuse"):
     """Frames/s of the same stream with another score (embedding or first-layer
-    keys) and, for period >= 1, under a refresh period: frame t is fully
-    encoded when t % period == 0 (HIP-graph replays of the full encode), else
-    incrementally (the step graph).  Period 0 = the rolling stream (one full
-    encode of frame 0 only).  Also the per-kernel times of an eager pass."""
+    keys), another reading of the MLP over all tokens ("reuse" exact, "all")
+    and, for period >= 1, under a refresh period: frame t is fully encoded when
+    t % period == 0 (HIP-graph replays of the full encode), else incrementally
+    (the step graph).  Period 0 = the rolling stream (one full encode of frame
+    0 only).  Also the per-kernel times of an eager pass and the outputs'
+    cosine against a full encode of the last frame."""
     import torch
     from paper_2607_12287_amd import incvit, synth
     m, B = wl.model, wl.views
     dev = frames.device
-    enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B, score=score)
+    enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B, score=score, mlp=mlp)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),
@@ -233,6 +251,7 @@ def measure_variant(wl, frames, score: str, period: int, steps: int, warmup: int
     wall = time.perf_counter() - t_start
     enc.drop_graph(gstep)
     enc.drop_graph(gfull)
+    approx = approx_vs_full(enc, caches, frames[warmup + steps])
     k = counts.float().cpu().numpy()
     inc = [j for j, t in enumerate(range(warmup + 1, warmup + 1 + steps)) if not (period >= 1 and t % period == 0)]
     # per-kernel times: eager steps of the rolling stream with per-launch events
@@ -247,11 +266,12 @@ def measure_variant(wl, frames, score: str, period: int, steps: int, warmup: int
     incvit.incvit_profile_enable(enc.h, False)
     enc.close()
     full_med = statistics.median(full_ms)
-    res = {"score": score, "period": period, "frames_per_s": round(steps * B / wall, 2),
+    res = {"score": score, "mlp": mlp, "period": period, "frames_per_s": round(steps * B / wall, 2),
            "ms_per_frame": round(wall * 1e3 / steps, 5), "full_encode_ms": round(full_med, 5),
            "speedup_vs_full_encode": round(full_med / (wall * 1e3 / steps), 3),
            "rows_mean_incremental": round(float(k[inc].sum(axis=1).mean()), 2) if inc else None,
-           "kernel_us_per_launch": {kk: round(v[0] * 1e3 / v[1], 3) for kk, v in prof.items() if v[1] > 0}}
+           "kernel_us_per_launch": {kk: round(v[0] * 1e3 / v[1], 3) for kk, v in prof.items() if v[1] > 0},
+           "approx_cos_vs_full": approx}
     kp = prof.get("key_proj")
     if kp and kp[1] > 0:
         us = kp[0] * 1e3 / kp[1]
@@ -553,6 +573,7 @@ def main() -> int:
     full_med = statistics.median(full_ms)
     if gstep is not None:
         enc.drop_graph(gstep)
+    approx = approx_vs_full(enc, caches, frames[total - 1])
 
     # same frames again, eagerly, with per-kernel events on the launch stream
     buf2, caches2 = enc.new_caches(B)
@@ -585,6 +606,7 @@ def main() -> int:
         "full_encode_ms": round(full_med, 5),
         "full_encode_frames_per_s": round(B * 1e3 / full_med, 2),
         "speedup_vs_full_encode": round(full_med / step_ms, 3),
+        "approx_cos_vs_full": approx,
     }
     if not args.no_torch_full:
         tms, tmode = torch_full_forward(m, wl.weights(), frames[0], max(5, args.full_repeats // 2))
@@ -622,6 +644,9 @@ def main() -> int:
         vsteps, vwarm = min(args.steps, 200), min(args.warmup, 20)
         result["variants"] = [measure_variant(wl, frames, "key", p, vsteps, vwarm, args.full_repeats)
                               for p in (0, 2)]
+        # the non-exact reading of the MLP over all tokens (embedding score)
+        result["variants"].append(measure_variant(wl, frames, "embed", 0, vsteps, vwarm, args.full_repeats,
+                                                  mlp="all"))
 
     if not args.no_cpu_baseline:
         n_cpu = min(len(frames_np), 64)

@@ -21,6 +21,13 @@
  *     the reference, incremental encoding on even chunks) are
  *     incvit_encode_frame with period 2; between full passes every refreshed
  *     token's vector becomes its new reference;
+ *   - "all tokens are processed by the MLP layer" is read exactly by default
+ *     (a reused row's MLP input is its cached state, so only U is computed);
+ *     cfg.mlp_all = 1 selects the non-exact reading: every frame, every row
+ *     starts from this frame's embedded token, reused rows add their cached
+ *     attention-branch output S(O W_o + b_o) of each layer to their current
+ *     residual stream, and the MLP runs over all rows (their K and V stay
+ *     cached; their outputs follow the new frame);
  *   - "top rho*N lowest similarities" is generalised to: U = {i : sim_i < tau}
  *     (strict), and if |U| > cap only the cap lowest similarities are kept,
  *     equal similarities going to the lower token index.  tau = +INFINITY with
@@ -87,6 +94,8 @@ typedef struct {
   float ln_eps;        /* e.g. 1e-6 */
   int32_t max_streams; /* largest B accepted by a call */
   int32_t score;       /* incvit_score; part of the cache identity */
+  int32_t mlp_all;     /* 0: exact reuse (default); 1: every row through the MLP
+                          each frame (see above); part of the cache identity */
 } incvit_config;
 
 typedef struct incvit_handle incvit_handle;
@@ -131,12 +140,13 @@ void incvit_destroy(incvit_handle* h);
  * (magic, config hash, status word), ref [N][D] fp32 (each token's score
  * vector -- embedding or first-layer key, per cfg.score -- at its last
  * refresh), X [L+1][N][D] (layer inputs), K and V of every layer, Y [N][D]
- * (final output).  Base addresses must be 256-byte aligned. */
+ * (final output), and with mlp_all A [L][N][D] (attention-branch outputs).
+ * Base addresses must be 256-byte aligned. */
 size_t incvit_cache_bytes(const incvit_handle* h);
 
 /* Bytes of one stream's cache in the canonical (export) layout:
  * ref [N][D] fp32, then in the storage dtype X [L+1][N][D], K [L][N][D],
- * V [L][N][D], Y [N][D]. */
+ * V [L][N][D], Y [N][D], and with mlp_all A [L][N][D]. */
 size_t incvit_cache_canonical_bytes(const incvit_handle* h);
 
 /* Bytes of workspace a call with B streams needs (256-byte aligned base). */
@@ -155,7 +165,9 @@ incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patch
 /* Incremental encode of B frames (§III-B, eqs. 3-5).  For each stream v:
  * U_v is selected from this frame's patches against the cache (tau, cap[v]),
  * rows U_v are recomputed through every layer and written into the cache
- * (ref, X, K, V, Y); all other rows are left untouched.
+ * (ref, X, K, V, Y); all other rows are left untouched.  With mlp_all the
+ * rows U_v get new ref, K, V and A rows, and every row of X and Y is
+ * recomputed (also when U_v is empty); `refreshed` still receives Y[U_v].
  *   tau: threshold (not NaN; +INFINITY disables it);
  *   cap: HOST int32[B], each clamped to [0, N];
  *   idx: device int32 [B][N]; idx[v][0..count[v]) = U_v ascending;
@@ -263,6 +275,7 @@ typedef enum {
   INCVIT_K_RES_LN1,   /* + bias + residual -> X^{l+1}; final LN (last)    */
   INCVIT_K_KEY_LN,    /* key score: LayerNorm 1 of layer 0, all tokens    */
   INCVIT_K_KEY_PROJ,  /* key score: key projection, all tokens            */
+  INCVIT_K_HSUM,      /* mlp_all: H = X + cached attention branch, all rows */
   INCVIT_K_COUNT
 } incvit_kernel_kind;
 

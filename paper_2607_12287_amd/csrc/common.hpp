@@ -33,11 +33,13 @@ struct Shape {
   int eb;     // element bytes of the storage dtype
   float eps;
   int score;  // 0: the cosine compares embedded tokens; 1: first-layer keys
+  int mlp_all;  // 1: every row through the MLP each frame (cached attention branch)
 };
 
 // Byte offsets inside one stream's cache.
 struct CacheLayout {
   size_t ref, x, k, v, y, total;
+  size_t a;         // attention-branch outputs [L][N][D] (mlp_all only, else 0)
   size_t x_layer;   // N*D*eb
   size_t kv_layer;  // H*Npad*dh*eb
 };
@@ -139,6 +141,7 @@ struct SelectArgs {
   int cap[kMaxViews];
   int* idx;    // [B][N]
   int* count;  // [B]
+  int* valid;  // [B] (may be null): 1 if the stream's step runs, else 0
 };
 
 struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map
@@ -153,9 +156,17 @@ struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map
   int init_header;   // commit of a full encode: write header
   uint32_t hash;
   void* z;           // compact Z_0 [Mpad][D] (operand order)
+  // mlp_all: every row of every stream, r = v * N + tok.  X0 of all rows,
+  // the all-rows map (cache null for a stream whose step does not run), and
+  // zpos[r] = the row's compact position among the refreshed rows, or -1
+  int all_rows;
+  const int* valid;  // [B] from the selection; null: every stream runs
+  RowInfo* rows_all;
+  Meta* meta_all;
+  int* zpos;
 };
 
-enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3 };
+enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3, EPI_ATT = 4 };
 
 // Fields in the order the kernel's prologue needs them, so that its argument
 // loads go out together.
@@ -168,7 +179,8 @@ struct GemmArgs {
   const RowInfo* rows;  // row map (cache, token, stream) of each compact row
   const Meta* meta;
   const void* resid;  // RES: Z_l rows (operand order)
-  void* out;          // QKV Q [Mpad][D]; RES H (operand order); FC1 G; PART f32 [ksplit][mpad][ldo]
+  void* out;          // QKV Q [Mpad][D]; RES H (operand order); FC1 G; PART f32 [ksplit][mpad][ldo];
+                      // ATT: unused (rows go to the cache's A^l)
   int lda, kchunks, Nout, ldo;
   int ksplit;         // K is split over ksplit workgroups (PART)
   int rgroups;        // 32-row groups launched: enough for the largest M of the call
@@ -198,6 +210,23 @@ struct ResArgs {
   void* z_out;        // Z_{l+1} (operand order)
   void* refreshed;    // final: optional [B][N][D]
   int N;
+  // mlp_all (rows = all rows of the call): Z_{l+1} goes to compact row zpos[r]
+  // (skipped when -1), `refreshed` row = zpos[r] - umeta->off[view]; rows
+  // whose cache is null are skipped
+  const int* zpos;
+  const Meta* umeta;
+};
+
+// mlp_all: H = S(X^l + A^l) of every row of the call (cache rows), into the
+// compact H buffer in operand order; rows of a stream whose step does not run
+// (cache null) get zeros.
+struct HsumArgs {
+  const RowInfo* rows;  // all-rows map
+  CacheLayout cl;
+  Shape sh;
+  int layer;
+  int rows_n;           // B * N
+  void* h;
 };
 
 struct AttnArgs {
@@ -277,6 +306,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s);
+hipError_t launch_hsum(const HsumArgs& a, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, int qtiles, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s);

@@ -7,7 +7,10 @@
 //   FC1 : G = S(GELU(LN2(H) W_1 + b_1));
 //   PART: raw partial sums of A W over one share of K (the MLP down
 //         projection); a row kernel adds the bias, the residual and the
-//         next LayerNorm.
+//         next LayerNorm;
+//   ATT : the attention branch S(O W_o + b_o) alone, scattered into the
+//         cache's A^l rows (the all-rows MLP reading, whose residual is
+//         formed for every row by a row kernel).
 // Z, O, H and G are kept in MFMA operand order (frag_off).
 //
 // LayerNorm folded into the GEMM (QKV, FC1): the weights are packed as
@@ -166,7 +169,7 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
     biasv[b] = EPI == EPI_PART ? 0.0f : a.bias[(cb0 + b) * 16 + n];
     c1v[b] = LNA ? a.c1[(cb0 + b) * 16 + n] : 0.0f;
   }
-  if constexpr (EPI == EPI_QKV) rinfo = a.rows[mfirst + 16 * re + 4 * g + ie];
+  if constexpr (EPI == EPI_QKV || EPI == EPI_ATT) rinfo = a.rows[mfirst + 16 * re + 4 * g + ie];
   if constexpr (EPI == EPI_RES) load_res(mfirst);
 
   // One 32-row block.  The group's first block is a copy of its own (FIRST),
@@ -176,7 +179,7 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
     if constexpr (!decltype(first)::value) {
       load_a(m0, 0);
       if (rounds > 1) load_w(0);
-      if constexpr (EPI == EPI_QKV) rinfo = a.rows[m0 + 16 * re + 4 * g + ie];
+      if constexpr (EPI == EPI_QKV || EPI == EPI_ATT) rinfo = a.rows[m0 + 16 * re + 4 * g + ie];
       if constexpr (EPI == EPI_RES) load_res(m0);
     }
     f32x4_t acc[2][NB], accs[2], accq[2];  // accs, accq: row sums and sums of squares (LNA)
@@ -256,6 +259,11 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
         if (ok) static_cast<float*>(a.out)[((size_t)ks * a.mpad + row) * a.ldo + col] = x;
       } else if constexpr (EPI == EPI_RES) {  // H = S(Z + (O W_o + b_o))
         if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resv[b] + (x + biasv[b]));
+      } else if constexpr (EPI == EPI_ATT) {  // A^l[tok] = S(O W_o + b_o)
+        if (ok) {
+          T* arow = reinterpret_cast<T*>(rinfo.cache + a.cl.a + (size_t)a.layer * a.cl.x_layer);
+          gbl(arow)[(size_t)rinfo.tok * D + col] = Elem<T>::cv(x + biasv[b]);
+        }
       } else if constexpr (EPI == EPI_QKV) {
         x = fmaf(rstd, x, fmaf(nmr, c1v[b], biasv[b]));
         const int which = col / D, c = col - which * D;

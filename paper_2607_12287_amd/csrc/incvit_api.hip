@@ -41,6 +41,7 @@ struct CanonLayout {  // element offsets into the canonical buffer
 
 struct WsLayout {
   size_t meta, rows, count, idx, sim, t0, kn, key, z, q, o, h, g, part, total;
+  size_t valid, zpos, rows_all, meta_all;  // all-rows MLP reading
   int Mpad;
 };
 
@@ -60,6 +61,7 @@ bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::strin
   if (!(c->ln_eps > 0.0f) || !std::isfinite(c->ln_eps)) { err = "ln_eps must be positive and finite"; return false; }
   if (c->dtype != INCVIT_F32 && c->dtype != INCVIT_BF16) { st = INCVIT_ERR_UNSUPPORTED; err = "dtype must be INCVIT_F32 or INCVIT_BF16"; return false; }
   if (c->score != INCVIT_SCORE_EMBED && c->score != INCVIT_SCORE_KEY) { st = INCVIT_ERR_ARG; err = "score must be INCVIT_SCORE_EMBED or INCVIT_SCORE_KEY"; return false; }
+  if (c->mlp_all != 0 && c->mlp_all != 1) { st = INCVIT_ERR_ARG; err = "mlp_all must be 0 or 1"; return false; }
   sh.N = (c->img_h / c->patch) * (c->img_w / c->patch);
   sh.P = c->channels * c->patch * c->patch;
   sh.D = c->dim;
@@ -74,6 +76,7 @@ bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::strin
   sh.eb = c->dtype == INCVIT_BF16 ? 2 : 4;
   sh.eps = c->ln_eps;
   sh.score = c->score;
+  sh.mlp_all = c->mlp_all;
   st = INCVIT_ERR_UNSUPPORTED;
   if (sh.D % 32) { err = "dim must be a multiple of 32"; return false; }
   if (sh.D > kMaxDim) { snprintf(buf, sizeof buf, "dim must be <= %d", kMaxDim); err = buf; return false; }
@@ -164,12 +167,14 @@ CacheLayout cache_layout(const Shape& sh) {
   cl.k = take(cl.kv_layer * sh.L);
   cl.v = take(cl.kv_layer * sh.L);
   cl.y = take(cl.x_layer);
+  cl.a = sh.mlp_all ? take(cl.x_layer * sh.L) : 0;
   cl.total = off;
   return cl;
 }
 
 uint32_t config_hash(const incvit_config& c) {
-  const int32_t f[10] = {c.img_h, c.img_w, c.channels, c.patch, c.dim, c.depth, c.heads, c.mlp_dim, c.dtype, c.score};
+  const int32_t f[11] = {c.img_h, c.img_w, c.channels, c.patch, c.dim, c.depth, c.heads, c.mlp_dim, c.dtype, c.score,
+                         c.mlp_all};
   uint32_t h = 2166136261u;
   auto mix = [&](uint32_t x) {
     for (int i = 0; i < 4; ++i) {
@@ -177,7 +182,7 @@ uint32_t config_hash(const incvit_config& c) {
       h *= 16777619u;
     }
   };
-  for (int i = 0; i < 10; ++i) mix((uint32_t)f[i]);
+  for (int i = 0; i < 11; ++i) mix((uint32_t)f[i]);
   uint32_t e;
   memcpy(&e, &c.ln_eps, 4);
   mix(e);
@@ -247,6 +252,10 @@ WsLayout ws_layout(const Shape& sh, int B) {
   w.h = take((size_t)w.Mpad * sh.D * sh.eb);
   w.g = take((size_t)w.Mpad * sh.Fpad * sh.eb);
   w.part = take((size_t)gemm_geom(sh, G_FC2).ksplit * w.Mpad * sh.D * 4);
+  w.valid = take(kMaxViews * 4);
+  w.zpos = take(sh.mlp_all ? (size_t)M * 4 : 0);
+  w.rows_all = take(sh.mlp_all ? (size_t)w.Mpad * sizeof(RowInfo) : 0);
+  w.meta_all = take(sh.mlp_all ? sizeof(Meta) : 0);
   w.total = off;
   return w;
 }
@@ -333,34 +342,47 @@ incvit_status run(incvit_handle* h, int kind, hipStream_t s, F&& launch) {
 const float* fptr(const incvit_handle* h, size_t off) { return reinterpret_cast<const float*>(h->packed + off); }
 
 // Launch the per-layer kernels for the rows of the call (row map in ws).
-// Launch the per-layer kernels for the rows of the call (row map in ws).
 // refreshed: optional output of the last layer's final LayerNorm rows.
+// With mlp_all the output projection writes the attention branch of the
+// refreshed rows into the cache, and the residual and the MLP run over every
+// row of the call (the all-rows map in ws).
 incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLayout& wl, char* ws,
                          int max_rows_per_view, int mmax, bool exact_m, void* refreshed, hipStream_t s) {
   // GEMM row groups: when the call's row count M is known on the host (a full
   // encode, or a pure top-k step where M is the sum of the caps), one 32-row
   // block per workgroup (up to 8 groups); otherwise one group, which loops over
   // the row blocks (idle groups cost about a microsecond each per launch)
-  const int need = std::max(1, (mmax + 31) / 32);
-  const int rgroups = std::min(exact_m ? need : std::max(1, std::min(need, h->row_groups)), 8);
+  auto groups_for = [&](int rows, bool known) {
+    const int need = std::max(1, (rows + 31) / 32);
+    return std::min(known ? need : std::max(1, std::min(need, h->row_groups)), 8);
+  };
   const Shape& sh = h->sh;
+  const bool all = sh.mlp_all != 0;
+  const int mall = B * sh.N;
+  const int rgroups = groups_for(mmax, exact_m);
   const RowInfo* rows = reinterpret_cast<const RowInfo*>(ws + wl.rows);
   const Meta* meta = reinterpret_cast<const Meta*>(ws + wl.meta);
+  // the rows of the MLP: the refreshed rows, or with mlp_all every row
+  const RowInfo* mrows = all ? reinterpret_cast<const RowInfo*>(ws + wl.rows_all) : rows;
+  const Meta* mmeta = all ? reinterpret_cast<const Meta*>(ws + wl.meta_all) : meta;
+  const int mlp_rows = all ? mall : mmax;
+  const int mgroups = all ? groups_for(mall, true) : rgroups;
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
     auto gemm = [&](int kind, int kernel_kind) -> incvit_status {
       const GemmGeom g = gemm_geom(sh, kind);
+      const bool mlp = kind == G_FC1 || kind == G_FC2;
       GemmArgs a;
       memset(&a, 0, sizeof a);
-      a.rows = rows;
-      a.meta = meta;
+      a.rows = mlp ? mrows : rows;
+      a.meta = mlp ? mmeta : meta;
       a.cl = h->cl;
       a.sh = sh;
       a.layer = l;
       a.kchunks = g.kchunks;
       a.Nout = g.Nout;
       a.ksplit = g.ksplit;
-      a.rgroups = rgroups;
+      a.rgroups = mlp ? mgroups : rgroups;
       a.mpad = wl.Mpad;
       int epi = EPI_PART;
       switch (kind) {
@@ -371,7 +393,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           a.out = ws + wl.q; a.ldo = sh.D;
           break;
         case G_OPROJ:
-          epi = EPI_RES;
+          epi = all ? EPI_ATT : EPI_RES;
           a.A = ws + wl.o; a.lda = sh.D;
           a.W = h->packed + P.w_o; a.bias = fptr(h, P.b_o);
           a.resid = ws + wl.z;
@@ -396,8 +418,8 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       const GemmGeom g = gemm_geom(sh, G_FC2);
       ResArgs r;
       memset(&r, 0, sizeof r);
-      r.meta = meta;
-      r.rows = rows;
+      r.meta = mmeta;
+      r.rows = mrows;
       r.cl = h->cl;
       r.sh = sh;
       r.layer = l;
@@ -409,32 +431,42 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       r.bias = fptr(h, P.b_2);
       r.z_out = ws + wl.z;
       r.last = l + 1 == sh.L;
+      if (all) {
+        r.zpos = reinterpret_cast<const int*>(ws + wl.zpos);
+        r.umeta = meta;
+      }
       if (r.last) {
         r.ln_g = fptr(h, h->pl.lnf_g);
         r.ln_b = fptr(h, h->pl.lnf_b);
         r.refreshed = refreshed;
       }
-      return run(h, kernel_kind, s, [&] { return launch_res(r, mmax, s); });
+      return run(h, kernel_kind, s, [&] { return launch_res(r, mlp_rows, s); });
     };
 
     incvit_status st;
-    if ((st = gemm(G_QKV, INCVIT_K_QKV)) != INCVIT_OK) return st;
-    AttnArgs aa;
-    memset(&aa, 0, sizeof aa);
-    aa.meta = meta;
-    aa.B = B;
-    aa.caches = views;
-    aa.cl = h->cl;
-    aa.sh = sh;
-    aa.layer = l;
-    aa.q = ws + wl.q;
-    aa.o = ws + wl.o;
-    aa.qmax = wl.Mpad - 1;
-    aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
-    const int qtiles = attn_qtiles_of(h->attn_qtiles, B, sh.H, max_rows_per_view);
-    if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, qtiles, s); })) != INCVIT_OK)
-      return st;
-    if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
+    if (mmax > 0) {  // attention part: the refreshed rows only
+      if ((st = gemm(G_QKV, INCVIT_K_QKV)) != INCVIT_OK) return st;
+      AttnArgs aa;
+      memset(&aa, 0, sizeof aa);
+      aa.meta = meta;
+      aa.B = B;
+      aa.caches = views;
+      aa.cl = h->cl;
+      aa.sh = sh;
+      aa.layer = l;
+      aa.q = ws + wl.q;
+      aa.o = ws + wl.o;
+      aa.qmax = wl.Mpad - 1;
+      aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
+      const int qtiles = attn_qtiles_of(h->attn_qtiles, B, sh.H, max_rows_per_view);
+      if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, qtiles, s); })) != INCVIT_OK)
+        return st;
+      if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
+    }
+    if (all) {
+      HsumArgs ha{mrows, h->cl, sh, l, mall, ws + wl.h};
+      if ((st = run(h, INCVIT_K_HSUM, s, [&] { return launch_hsum(ha, s); })) != INCVIT_OK) return st;
+    }
     if ((st = gemm(G_FC1, INCVIT_K_FC1)) != INCVIT_OK) return st;
     if ((st = gemm(G_FC2, INCVIT_K_FC2)) != INCVIT_OK) return st;
     if ((st = rowk(INCVIT_K_RES_LN1)) != INCVIT_OK) return st;
@@ -461,6 +493,17 @@ incvit_status check_common(incvit_handle* h, int32_t B, const float* patches, vo
   if (!ws) return fail(h, INCVIT_ERR_ARG, "workspace is null");
   if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(h, INCVIT_ERR_ARG, "workspace must be 256-byte aligned");
   return INCVIT_OK;
+}
+
+// mlp_all: the commit also writes X0 of every row, the all-rows map and the
+// rows' compact positions among the refreshed rows.
+void set_all_rows(RowsArgs& ra, const Shape& sh, char* ws, const WsLayout& wl, const int* valid) {
+  if (!sh.mlp_all) return;
+  ra.all_rows = 1;
+  ra.valid = valid;
+  ra.rows_all = reinterpret_cast<RowInfo*>(ws + wl.rows_all);
+  ra.meta_all = reinterpret_cast<Meta*>(ws + wl.meta_all);
+  ra.zpos = reinterpret_cast<int*>(ws + wl.zpos);
 }
 
 // The score vectors of every token of the call: the embedded tokens t0, or in
@@ -522,6 +565,7 @@ incvit_status full_impl(incvit_handle* h, int32_t B, const float* patches, void*
   ra.init_header = 1;
   ra.hash = h->hash;
   ra.z = ws + wl.z;
+  set_all_rows(ra, sh, ws, wl, nullptr);
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
   return run_layers(h, views, B, wl, ws, sh.N, mmax, true, refreshed, s);
 }
@@ -648,7 +692,7 @@ size_t incvit_cache_canonical_bytes(const incvit_handle* h) {
   if (!h) return 0;
   const Shape& sh = h->sh;
   const size_t nd = (size_t)sh.N * sh.D;
-  return nd * 4 + ((size_t)(sh.L + 1) * nd + 2 * (size_t)sh.L * nd + nd) * sh.eb;
+  return nd * 4 + ((size_t)(sh.L + 1) * nd + 2 * (size_t)sh.L * nd + nd + (sh.mlp_all ? (size_t)sh.L * nd : 0)) * sh.eb;
 }
 
 size_t incvit_workspace_bytes(const incvit_handle* h, int32_t B) {
@@ -703,8 +747,10 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   sa.hash = h->hash;
   sa.idx = idx;
   sa.count = count;
+  sa.valid = reinterpret_cast<int*>(ws + wl.valid);
   if ((st = run(h, INCVIT_K_SELECT, s, [&] { return launch_select(sa, s); })) != INCVIT_OK) return st;
-  if (mmax == 0) return INCVIT_OK;
+  // nothing can be selected: done (with mlp_all every row still follows the frame)
+  if (mmax == 0 && !sh.mlp_all) return INCVIT_OK;
 
   RowsArgs ra;
   memset(&ra, 0, sizeof ra);
@@ -717,6 +763,7 @@ incvit_status incvit_step(incvit_handle* h, int32_t B, const float* patches, voi
   ra.t0 = t0;
   ra.score = score;
   ra.z = ws + wl.z;
+  set_all_rows(ra, sh, ws, wl, sa.valid);
   if ((st = run(h, INCVIT_K_COMMIT, s, [&] { return launch_commit(ra, mmax, s); })) != INCVIT_OK) return st;
   // with the threshold disabled every stream refreshes exactly its cap
   return run_layers(h, views, B, wl, ws, max_rows, mmax, std::isinf(tau) && tau > 0, refreshed, s);

@@ -58,14 +58,15 @@ __global__ void conv_kernel(ConvArgs a) {
 }
 
 // Canonical layout of one cache: ref [N][D] f32 | X [L+1][N][D] | K [L][N][D]
-// | V [L][N][D] | Y [N][D] (storage dtype).  Device layout differs for K
-// and V (attention operand order, k_elem / v_elem).
+// | V [L][N][D] | Y [N][D] | with mlp_all A [L][N][D] (storage dtype).  Device
+// layout differs for K and V (attention operand order, k_elem / v_elem).
 template <class T>
 __global__ void export_kernel(ExportArgs a) {
   const Shape& sh = a.sh;
   const size_t nd = (size_t)sh.N * sh.D;
   const size_t n_ref = nd, n_x = (size_t)(sh.L + 1) * nd, n_kv = (size_t)sh.L * nd;
-  const size_t total = n_ref + n_x + 2 * n_kv + nd;
+  const size_t n_a = sh.mlp_all ? (size_t)sh.L * nd : 0;
+  const size_t total = n_ref + n_x + 2 * n_kv + nd + n_a;
   char* cache = const_cast<char*>(a.cache);
   const float* cref = reinterpret_cast<const float*>(a.canon);
   const T* cT = reinterpret_cast<const T*>(a.canon + n_ref * sizeof(float));
@@ -90,8 +91,10 @@ __global__ void export_kernel(ExportArgs a) {
       const int hh = c / sh.dh, d = c % sh.dh;
       T* base = reinterpret_cast<T*>(cache + (isv ? a.cl.v : a.cl.k) + (size_t)l * a.cl.kv_layer);
       dev = base + (isv ? v_elem(sh, hh, tok, d) : k_elem(sh, hh, tok, d));
-    } else {
+    } else if (f < n_x + 2 * n_kv + nd) {
       dev = reinterpret_cast<T*>(cache + a.cl.y) + (f - n_x - 2 * n_kv);
+    } else {
+      dev = reinterpret_cast<T*>(cache + a.cl.a) + (f - n_x - 2 * n_kv - nd);
     }
     if (a.to_canonical) *can = *dev; else *dev = *can;
   }

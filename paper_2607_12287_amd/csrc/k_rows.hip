@@ -96,12 +96,16 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     v[j] = rnd4(add4(res[j], x), static_cast<T*>(nullptr));
     if (tid + 256 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
   }
+  // compact position of the next layer's input row: r itself, or with the
+  // all-rows map the row's place among the refreshed rows (-1: not one)
+  const int zr = a.zpos ? a.zpos[r] : r;
+  if (!ri.cache) return;  // uniform: a stream whose step does not run
   T* xrow = x_row<T>(ri.cache, a.cl, a.sh, a.layer + 1, ri.tok);
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     const int q = tid + 256 * j;
     if (q < D4) {
-      st4(static_cast<T*>(a.z_out) + frag_off(r, 4 * q, D / 32), 0, v[j]);
+      if (zr >= 0) st4(static_cast<T*>(a.z_out) + frag_off(zr, 4 * q, D / 32), 0, v[j]);
       st4(xrow, q, v[j]);
     }
   }
@@ -118,8 +122,11 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
   }
   const float rstd = 1.0f / sqrtf(block_sum4(sq, s_red) / (float)D + a.sh.eps);
   T* yrow = reinterpret_cast<T*>(ri.cache + a.cl.y) + (size_t)ri.tok * D;
-  T* outrow = a.refreshed ? static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + (r - a.meta->off[ri.view])) * D
-                          : nullptr;
+  T* outrow = nullptr;
+  if (a.refreshed && zr >= 0) {
+    const int j = a.zpos ? zr - a.umeta->off[ri.view] : r - a.meta->off[ri.view];
+    outrow = static_cast<T*>(a.refreshed) + ((size_t)ri.view * a.N + j) * D;
+  }
 #pragma unroll
   for (int j = 0; j < KP; ++j) {
     const int q = tid + 256 * j;
@@ -131,6 +138,38 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
       st4(yrow, q, n4);
       if (outrow) st4(outrow, q, n4);
     }
+  }
+}
+
+// mlp_all: one 256-thread workgroup per row r of the all-rows map:
+// H[r] = S(X^l[tok] + A^l[tok]) into the compact H buffer (operand order).
+template <class T, int KP>
+__global__ __launch_bounds__(256) void hsum_kernel(HsumArgs a) {
+  const int tid = threadIdx.x, r = blockIdx.x;
+  const int D = a.sh.D, D4 = D / 4;
+  const RowInfo ri = a.rows[r];
+  T* h = static_cast<T*>(a.h);
+  if (!ri.cache) {  // uniform
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      const int q = tid + 256 * j;
+      if (q < D4) st4(h + frag_off(r, 4 * q, D / 32), 0, make_float4(0.0f, 0.0f, 0.0f, 0.0f));
+    }
+    return;
+  }
+  const T* x = x_row<T>(ri.cache, a.cl, a.sh, a.layer, ri.tok);
+  const T* at = reinterpret_cast<const T*>(ri.cache + a.cl.a + (size_t)a.layer * a.cl.x_layer) + (size_t)ri.tok * D;
+  float4 xv[KP], av[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = min(tid + 256 * j, D4 - 1);
+    xv[j] = ld4s(x + 4 * q);
+    av[j] = ld4s(at + 4 * q);
+  }
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = tid + 256 * j;
+    if (q < D4) st4(h + frag_off(r, 4 * q, D / 32), 0, add4(xv[j], av[j]));
   }
 }
 
@@ -158,6 +197,15 @@ hipError_t launch_t(const ResArgs& a, dim3 grid, hipStream_t s) {
 hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s) {
   const dim3 grid(max(1, mmax));
   return a.sh.dtype ? launch_t<uint16_t>(a, grid, s) : launch_t<float>(a, grid, s);
+}
+
+hipError_t launch_hsum(const HsumArgs& a, hipStream_t s) {
+  const dim3 grid(max(1, a.rows_n));
+  if (a.sh.dtype)
+    return a.sh.D <= 1024 ? launch_k(hsum_kernel<uint16_t, 1>, grid, dim3(256), 0, s, a)
+                          : launch_k(hsum_kernel<uint16_t, 2>, grid, dim3(256), 0, s, a);
+  return a.sh.D <= 1024 ? launch_k(hsum_kernel<float, 1>, grid, dim3(256), 0, s, a)
+                        : launch_k(hsum_kernel<float, 2>, grid, dim3(256), 0, s, a);
 }
 
 }  // namespace incvit

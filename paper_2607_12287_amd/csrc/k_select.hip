@@ -79,7 +79,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
   }
   __syncthreads();
   if (!s_misc[0]) {  // never encoded, or another model: this stream is a no-op
-    if (tid == 0) a.count[v] = 0;
+    if (tid == 0) {
+      a.count[v] = 0;
+      if (a.valid) a.valid[v] = 0;
+    }
     return;
   }
   if (bad) atomicOr(&s_misc[1], 1);
@@ -89,9 +92,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectArgs a) {
     if (tid == 0) {
       hdr->status = kStatusNonFinite;
       a.count[v] = 0;
+      if (a.valid) a.valid[v] = 0;
     }
     return;
   }
+  if (tid == 0 && a.valid) a.valid[v] = 1;
   const int total = s_misc[2];
   const int cap = min(max(a.cap[v], 0), N);
 
@@ -188,6 +193,39 @@ __device__ __forceinline__ void store4v(uint16_t* p, float4 v) {
   *reinterpret_cast<uint2*>(p) = make_uint2(f2bf2(v.x, v.y), f2bf2(v.z, v.w));
 }
 
+// Row r = v * N + tok of the all-rows map (mlp_all): X0[tok] = S(T0[tok]) for
+// every token, the map entry (cache null if the stream's step does not run),
+// and zpos[r] = compact position of the token among the refreshed rows or -1
+// (binary search of the ascending index list).
+template <class T, int KP>
+__device__ void commit_all_row(const RowsArgs& a, int r, const int* s_off) {
+  const int N = a.rm.N, D = a.sh.D, D4 = D / 4;
+  const int v = r / N, tok = r - v * N;
+  const bool ok = a.init_header || !a.valid || a.valid[v];
+  char* cache = a.caches.p[v];
+  if (threadIdx.x == 0) {
+    a.rows_all[r] = RowInfo{ok ? cache : nullptr, tok, v};
+    int lo = 0, hi = a.rm.count[v];  // idx[v][lo..hi) ascending
+    const int* ix = a.rm.idx + (size_t)v * N;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (ix[mid] < tok) lo = mid + 1; else hi = mid;
+    }
+    a.zpos[r] = (lo < a.rm.count[v] && ix[lo] == tok) ? s_off[v] + lo : -1;
+  }
+  if (!ok) return;
+  const float4* src = reinterpret_cast<const float4*>(a.t0 + ((size_t)v * N + tok) * D);
+  T* x0 = x_row<T>(cache, a.cl, a.sh, 0, tok);
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const int q = threadIdx.x + 256 * j;
+    if (q < D4) {
+      const float4 t = src[q];
+      store4v(x0 + 4 * q, make_float4(Elem<T>::rnd(t.x), Elem<T>::rnd(t.y), Elem<T>::rnd(t.z), Elem<T>::rnd(t.w)));
+    }
+  }
+}
+
 // One workgroup per compact row r: ref[tok] = score[tok] (fp32: the embedded
 // token or its first-layer key), X0[tok] = S(T0[tok]),
 // the compact Z0 row (operand order, the layer-0 input), and the row's entry in
@@ -223,6 +261,13 @@ __global__ __launch_bounds__(256) void commit_kernel(RowsArgs a) {
     }
   }
   const int r = blockIdx.x;
+  if (a.all_rows) {  // uniform: this workgroup's row of the all-rows map
+    if (blockIdx.x == 0) {
+      if (tid == 0) a.meta_all->m = B * N;
+      if (tid <= B) a.meta_all->off[tid] = tid * N;
+    }
+    if (r < B * N) commit_all_row<T, KP>(a, r, s_off);
+  }
   if (r >= M) return;  // uniform per workgroup
   int v = 0;
   while (v + 1 < B && s_off[v + 1] <= r) ++v;
@@ -253,7 +298,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s) {
-  const dim3 grid(max(1, mmax));
+  const dim3 grid(max(1, a.all_rows ? max(mmax, a.rm.B * a.rm.N) : mmax));
   const bool wide = a.sh.D > 1024;
   if (a.sh.dtype)
     return wide ? launch_k(commit_kernel<uint16_t, 2>, grid, dim3(256), 0, s, a)

@@ -23,7 +23,8 @@ INCVIT_F32, INCVIT_BF16 = 0, 1
 INCVIT_SCORE_EMBED, INCVIT_SCORE_KEY = 0, 1
 SCORES = {"embed": INCVIT_SCORE_EMBED, "key": INCVIT_SCORE_KEY}
 KERNEL_KINDS = ("embed", "sim", "select", "commit", "qkv", "attn", "oproj", "fc1", "fc2", "res_ln1",
-                "key_ln", "key_proj")
+                "key_ln", "key_proj", "hsum")
+MLPS = {"reuse": 0, "all": 1}
 
 # Exported symbols, as declared in include/incvit.h.
 EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "incvit_pack_weights",
@@ -38,7 +39,8 @@ class incvit_config(ctypes.Structure):
     _fields_ = [("img_h", ctypes.c_int32), ("img_w", ctypes.c_int32), ("channels", ctypes.c_int32),
                 ("patch", ctypes.c_int32), ("dim", ctypes.c_int32), ("depth", ctypes.c_int32),
                 ("heads", ctypes.c_int32), ("mlp_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("ln_eps", ctypes.c_float), ("max_streams", ctypes.c_int32), ("score", ctypes.c_int32)]
+                ("ln_eps", ctypes.c_float), ("max_streams", ctypes.c_int32), ("score", ctypes.c_int32),
+                ("mlp_all", ctypes.c_int32)]
 
 
 class incvit_tuning(ctypes.Structure):
@@ -220,26 +222,28 @@ def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None, attn_qtiles: int 
 
 # --- convenience wrapper -------------------------------------------------------
 
-def make_config(shape, max_streams: int = 1, score: str = "embed") -> incvit_config:
+def make_config(shape, max_streams: int = 1, score: str = "embed", mlp: str = "reuse") -> incvit_config:
     """Config from a model shape with attributes img_h, img_w, channels, patch,
     dim, depth, heads, mlp_dim, dtype ('f32'/'bf16'), ln_eps; score is 'embed'
-    or 'key' (what the cosine compares)."""
+    or 'key' (what the cosine compares); mlp is 'reuse' (exact) or 'all' (every
+    row through the MLP each frame)."""
     return incvit_config(shape.img_h, shape.img_w, shape.channels, shape.patch, shape.dim, shape.depth,
                          shape.heads, shape.mlp_dim, INCVIT_BF16 if shape.dtype == "bf16" else INCVIT_F32,
-                         float(shape.ln_eps), int(max_streams), SCORES[score])
+                         float(shape.ln_eps), int(max_streams), SCORES[score], MLPS[mlp])
 
 
 class Encoder:
     """Device-resident encoder: packed weights, per-stream caches, workspace."""
 
     def __init__(self, shape, canonical_weights, max_streams: int = 1, device: str = "cuda",
-                 score: str = "embed"):
+                 score: str = "embed", mlp: str = "reuse"):
         import torch
         self.torch = torch
         self.shape = shape
         self.score = score
+        self.mlp = mlp
         self.device = torch.device(device)
-        self.cfg = make_config(shape, max_streams, score)
+        self.cfg = make_config(shape, max_streams, score, mlp)
         self.dtype = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
         self.N = shape.n_tokens
         self.D = shape.dim
@@ -358,7 +362,8 @@ class Encoder:
         incvit_graph_destroy(graph)
 
     def export(self, cache: int) -> Dict[str, np.ndarray]:
-        """Canonical copy of one cache as float64 numpy arrays: ref, X, K, V, Y."""
+        """Canonical copy of one cache as float64 numpy arrays: ref, X, K, V, Y
+        (and A with mlp 'all')."""
         torch = self.torch
         nb = incvit_cache_canonical_bytes(self.h)
         dst = torch.empty(nb, dtype=torch.uint8, device=self.device)
@@ -373,9 +378,11 @@ class Encoder:
         X = rest[o:o + (L + 1) * nd].reshape(L + 1, N, D); o += (L + 1) * nd
         K = rest[o:o + L * nd].reshape(L, N, D); o += L * nd
         V = rest[o:o + L * nd].reshape(L, N, D); o += L * nd
-        Y = rest[o:o + nd].reshape(N, D)
-        return {k: t.cpu().numpy().astype(np.float64 if k != "ref" else np.float32)
-                for k, t in (("ref", ref), ("X", X), ("K", K), ("V", V), ("Y", Y))}
+        Y = rest[o:o + nd].reshape(N, D); o += nd
+        parts = [("ref", ref), ("X", X), ("K", K), ("V", V), ("Y", Y)]
+        if self.mlp == "all":
+            parts.append(("A", rest[o:o + L * nd].reshape(L, N, D)))
+        return {k: t.cpu().numpy().astype(np.float64 if k != "ref" else np.float32) for k, t in parts}
 
     def export_raw(self, cache: int):
         nb = incvit_cache_canonical_bytes(self.h)

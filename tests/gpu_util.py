@@ -42,10 +42,11 @@ def rel_err(a: np.ndarray, b: np.ndarray) -> float:
 class Pair:
     """The HIP encoder and the oracle on the same model and weights."""
 
-    def __init__(self, m: synth.ModelShape, w, B: int, oracle_views=None, score: str = "embed"):
+    def __init__(self, m: synth.ModelShape, w, B: int, oracle_views=None, score: str = "embed",
+                 mlp: str = "reuse"):
         self.m, self.w, self.B = m, w, B
-        self.enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=B, score=score)
-        self.model = vit.Model(m, w, score=score)
+        self.enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=B, score=score, mlp=mlp)
+        self.model = vit.Model(m, w, score=score, mlp=mlp)
         self.buf, self.caches = self.enc.new_caches(B)
         self.views = list(range(B)) if oracle_views is None else list(oracle_views)
         self.ora = {}
@@ -85,6 +86,9 @@ class Pair:
             assert np.array_equal(g["X"][0][U], self.ora[v].X[0][U]), (label, v, "X0")
             if self.model.score == "embed":
                 assert np.array_equal(g["X"][0][U], vit.S(g["ref"][U].astype(np.float64), dt)), (label, v, "X0")
+            if self.model.mlp == "all":
+                worst = max(worst, self._check_layers_all(g, v, U, label))
+                continue
             if U.size == 0:
                 continue
             for l in range(m.depth):
@@ -99,6 +103,26 @@ class Pair:
             assert e <= tol, (label, v, "Y", e)
         return worst
 
+    def _check_layers_all(self, g, v, U, label):
+        """Teacher-forced parity of the all-rows MLP reading: every row of every
+        layer from the GPU's own inputs and cached K, V and attention branch."""
+        m, tol = self.m, TOL[self.m.dtype]
+        assert np.array_equal(g["X"][0], self.ora[v].X[0]), (label, v, "X0 all rows")
+        worst = 0.0
+        for l in range(m.depth):
+            K, V, A = g["K"][l].copy(), g["V"][l].copy(), g["A"][l].copy()
+            Z = vit.layer_all(self.model, l, g["X"][l], U, K, V, A)
+            pairs = [("X", g["X"][l + 1], Z)]
+            if U.size:
+                pairs += [("K", g["K"][l][U], K[U]), ("V", g["V"][l][U], V[U]), ("A", g["A"][l][U], A[U])]
+            for name, a, b in pairs:
+                e = rel_err(a, b)
+                worst = max(worst, e)
+                assert e <= tol, (label, v, "layer", l, name, e)
+        e = rel_err(g["Y"], vit.final_rows(self.model, g["X"][m.depth]))
+        assert e <= tol, (label, v, "Y", e)
+        return max(worst, e)
+
     def check_caches(self, label=""):
         tol = FREE_TOL[self.m.dtype]
         worst = 0.0
@@ -106,7 +130,10 @@ class Pair:
             g = self.enc.export(self.caches[v])
             o = self.ora[v]
             assert np.array_equal(g["ref"], o.ref), (label, v, "ref")
-            for name, depth in (("X", self.m.depth + 1), ("K", self.m.depth), ("V", self.m.depth)):
+            names = [("X", self.m.depth + 1), ("K", self.m.depth), ("V", self.m.depth)]
+            if self.model.mlp == "all":
+                names.append(("A", self.m.depth))
+            for name, depth in names:
                 for l in range(depth):
                     e = rel_err(g[name][l], getattr(o, name)[l])
                     worst = max(worst, e)
