@@ -23,6 +23,11 @@ __device__ __forceinline__ void load16(V8<uint16_t>& v, const uint16_t* p) { v.l
 __device__ __forceinline__ void load16(V8<float>& v, const float* p) {
   v.a = __builtin_bit_cast(float4, *(const INCVIT_GLOBAL f32x4_t*)p);
 }
+// the same 16 bytes through a buffer resource (lane offset voff, uniform soff)
+__device__ __forceinline__ void bload16(V8<uint16_t>& v, Rsrc r, uint32_t voff, uint32_t soff) { v.bload(r, voff, soff); }
+__device__ __forceinline__ void bload16(V8<float>& v, Rsrc r, uint32_t voff, uint32_t soff) {
+  v.a = bload16f(r, voff, soff);
+}
 __device__ __forceinline__ void unpack16(float* f, const V8<uint16_t>& v) {
   const uint32_t q[4] = {v.v.x, v.v.y, v.v.z, v.v.w};
 #pragma unroll
@@ -36,16 +41,18 @@ __device__ __forceinline__ void unpack16(float* f, const V8<float>& v) {
 }
 
 // Workgroup: 16 tokens x 64 columns; wave w computes tokens 4w..4w+3 of the
-// tile, lane = column.  k is staged through LDS in tiles of 64.  Every global
-// load is unconditional (clamped addresses; values past P are loaded but never
-// used because the k loop stops at P) and issued two tiles ahead, so a tile's
-// data arrives while the two before it are computed.
-template <class T>
+// tile, lane = column.  k is staged through LDS in tiles of 64, double
+// buffered, with one barrier per tile.  A tile's global loads go out two
+// tiles of compute ahead into one of three register slots (the loop body is unrolled over
+// the slots, so no register copy waits on a load in flight); every load is
+// unconditional (clamped addresses; values past P are loaded but never used
+// because the k loop stops at P).
+template <class T, int NT>
 __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
   constexpr int WV = 16 / sizeof(T);  // weights per 16-byte load
   constexpr int WL = 64 * 64 / (256 * WV);  // weight loads per thread per tile
-  __shared__ __align__(16) float sx[64][16];  // [k][token]
-  __shared__ __align__(16) float sw[64][64];  // [k][column]
+  __shared__ __align__(16) float sx[2][64][16];  // [buffer][k][token]
+  __shared__ __align__(16) float sw[2][64][64];  // [buffer][k][column]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   // Workgroups are dealt to the 8 XCDs round robin by linear launch index, and
   // each XCD has its own L2.  Renumber them XCD-major (a bijection) and take
@@ -70,9 +77,24 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
   }
 
   const int d = c0 + lane;
-  const float* xp = a.patches + (size_t)v * N * P;
-  const T* wp = static_cast<const T*>(a.w_pe);
-  // this thread's share of a tile: 4 patch values (token e/64, k e%64) and WL
+  // Operands through buffer loads: every lane offset below is fixed for the
+  // whole kernel and the tile's k position is a wave-uniform offset, so a
+  // fetch needs no address registers.  Reads past the buffer return zero; reads
+  // past a row's end (k >= P) are never used because the k loop stops at P.
+  const Rsrc rx = make_rsrc(a.patches + (size_t)v * N * P, (uint32_t)((size_t)N * P * 4));
+  const Rsrc rw = make_rsrc(a.w_pe, (uint32_t)((size_t)P * D * sizeof(T)));
+  uint32_t xoff[4], woff[WL > 0 ? WL : 1];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = tid + 256 * j;
+    xoff[j] = (uint32_t)((min(tok0 + (e & 15), N - 1) * P + (e >> 4)) * 4);
+  }
+#pragma unroll
+  for (int j = 0; j < WL; ++j) {
+    const int e = tid + 256 * j;
+    woff[j] = (uint32_t)(((e / (64 / WV)) * D + min(c0 + (e % (64 / WV)) * WV, D - WV)) * sizeof(T));
+  }
+  // this thread's share of a tile: 4 patch values (token e%16, k e/16) and WL
   // 16-byte runs of weights (row k, WV consecutive columns)
   struct Tile {
     float x[4];
@@ -80,24 +102,16 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
   };
   auto fetch = [&](Tile& t, int kt) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = tid + 256 * j;
-      const int tok = min(tok0 + (e >> 6), N - 1), k = min(kt + (e & 63), P - 1);
-      t.x[j] = xp[(size_t)tok * P + k];
-    }
+    for (int j = 0; j < 4; ++j)
+      t.x[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rx, xoff[j], (uint32_t)kt * 4, 0));
 #pragma unroll
-    for (int j = 0; j < WL; ++j) {
-      const int e = tid + 256 * j;                 // run index in the tile
-      const int k = min(kt + e / (64 / WV), P - 1);
-      const int col = min(c0 + (e % (64 / WV)) * WV, D - WV);
-      load16(t.wv[j], wp + (size_t)k * D + col);
-    }
+    for (int j = 0; j < WL; ++j) bload16(t.wv[j], rw, woff[j], (uint32_t)(kt * D * sizeof(T)));
   };
-  auto stage = [&](const Tile& t) {
+  auto stage = [&](const Tile& t, int b) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int e = tid + 256 * j;
-      sx[e & 63][e >> 6] = t.x[j];
+      sx[b][e >> 4][e & 15] = t.x[j];
     }
 #pragma unroll
     for (int j = 0; j < WL; ++j) {
@@ -105,7 +119,7 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
       float f[WV];
       unpack16(f, t.wv[j]);
 #pragma unroll
-      for (int q = 0; q < WV; ++q) sw[e / (64 / WV)][(e % (64 / WV)) * WV + q] = f[q];
+      for (int q = 0; q < WV; ++q) sw[b][e / (64 / WV)][(e % (64 / WV)) * WV + q] = f[q];
     }
   };
 
@@ -118,25 +132,63 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
     const int tok = min(tok0 + 4 * w + r, N - 1);
     if (a.pos) posv[r] = a.pos[(size_t)tok * D + min(d, D - 1)];
   }
-  Tile t0, t1;
-  fetch(t0, 0);
-  fetch(t1, 64);
-  for (int kt = 0; kt < P; kt += 64) {
-    stage(t0);
-    __syncthreads();
-    t0 = t1;
-    fetch(t1, kt + 128);  // two tiles ahead (clamped past the end)
-    const int kmax = min(64, P - kt);
+  auto compute = [&](int b, int kmax) {
 #pragma unroll 8
     for (int kk = 0; kk < kmax; ++kk) {
-      const float wv = sw[kk][lane];
-      const float4 xv = *reinterpret_cast<const float4*>(&sx[kk][4 * w]);
+      const float wv = sw[b][kk][lane];
+      const float4 xv = *reinterpret_cast<const float4*>(&sx[b][kk][4 * w]);
       acc[0] = __fmaf_rn(xv.x, wv, acc[0]);
       acc[1] = __fmaf_rn(xv.y, wv, acc[1]);
       acc[2] = __fmaf_rn(xv.z, wv, acc[2]);
       acc[3] = __fmaf_rn(xv.w, wv, acc[3]);
     }
-    __syncthreads();
+  };
+  Tile tl[3];
+  fetch(tl[0], 0);
+  fetch(tl[1], 64);
+  fetch(tl[2], 128);
+  stage(tl[0], 0);
+  __syncthreads();
+  if constexpr (NT > 0) {
+    // NT = ceil(P / 64) tiles, unrolled: every slot and buffer index is a
+    // constant, so each wait covers exactly the loads of the tile it stages
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      if (it + 1 < NT) {
+#pragma unroll
+        for (int kk = 0; kk < 64; ++kk) {  // a full tile
+          const float wv = sw[it & 1][kk][lane];
+          const float4 xv = *reinterpret_cast<const float4*>(&sx[it & 1][kk][4 * w]);
+          acc[0] = __fmaf_rn(xv.x, wv, acc[0]);
+          acc[1] = __fmaf_rn(xv.y, wv, acc[1]);
+          acc[2] = __fmaf_rn(xv.z, wv, acc[2]);
+          acc[3] = __fmaf_rn(xv.w, wv, acc[3]);
+        }
+        stage(tl[(it + 1) % 3], (it + 1) & 1);
+        if (it + 3 < NT) fetch(tl[it % 3], 64 * (it + 3));
+        __syncthreads();
+      } else {
+        compute(it & 1, P - 64 * it);
+      }
+    }
+  } else {
+    const int nt = (P + 63) / 64;
+    for (int i0 = 0; i0 < nt; i0 += 3) {
+#pragma unroll
+      for (int s3 = 0; s3 < 3; ++s3) {
+        const int it = i0 + s3;
+        if (it < nt) {  // uniform
+          // tile it is in LDS buffer it & 1; tile it + 1 waits in slot (s3 + 1) % 3
+          // and is staged after the compute; slot s3 (tile it, already staged)
+          // then takes tile it + 3, whose loads have two tiles of compute to land
+          const int b = it & 1;
+          compute(b, min(64, P - 64 * it));
+          if (it + 1 < nt) stage(tl[(s3 + 1) % 3], b ^ 1);
+          fetch(tl[s3], 64 * (it + 3));
+          __syncthreads();
+        }
+      }
+    }
   }
   if (d < D) {
 #pragma unroll
@@ -147,16 +199,16 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
   }
 }
 
-template <class T>
+template <class T, int NT>
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
-  embed_body<T>(a);
+  embed_body<T, NT>(a);
 }
 
 // The key projection of the key score: the same fixed-order product with
 // x = LayerNorm rows, K = D, W = W_K of layer 0, no position term.
-template <class T>
+template <class T, int NT>
 __global__ __launch_bounds__(256) void keyproj_kernel(EmbedArgs a) {
-  embed_body<T>(a);
+  embed_body<T, NT>(a);
 }
 
 // Correctly rounded fp32 square root.  HIP's __fsqrt_rn is the bare hardware
@@ -248,16 +300,36 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
   }
 }
 
+// Tile counts of the shapes in use are compiled unrolled (patch 14 and 16 with
+// 3 channels: P = 588, 768; D = 192, 1024, 1152); other lengths run the loop.
+template <class T, template <class, int> class Launch>
+hipError_t launch_nt(const EmbedArgs& a, dim3 grid, hipStream_t s) {
+  switch ((a.P + 63) / 64) {
+    case 3: return Launch<T, 3>::go(a, grid, s);
+    case 10: return Launch<T, 10>::go(a, grid, s);
+    case 12: return Launch<T, 12>::go(a, grid, s);
+    case 16: return Launch<T, 16>::go(a, grid, s);
+    case 18: return Launch<T, 18>::go(a, grid, s);
+    default: return Launch<T, 0>::go(a, grid, s);
+  }
+}
+template <class T, int NT>
+struct EmbedLaunch {
+  static hipError_t go(const EmbedArgs& a, dim3 g, hipStream_t s) { return launch_k(embed_kernel<T, NT>, g, dim3(256), 0, s, a); }
+};
+template <class T, int NT>
+struct KeyLaunch {
+  static hipError_t go(const EmbedArgs& a, dim3 g, hipStream_t s) { return launch_k(keyproj_kernel<T, NT>, g, dim3(256), 0, s, a); }
+};
+
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
-  if (a.dtype) return launch_k(embed_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  return launch_k(embed_kernel<float>, grid, dim3(256), 0, s, a);
+  return a.dtype ? launch_nt<uint16_t, EmbedLaunch>(a, grid, s) : launch_nt<float, EmbedLaunch>(a, grid, s);
 }
 
 hipError_t launch_keyproj(const EmbedArgs& a, hipStream_t s) {
   dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
-  if (a.dtype) return launch_k(keyproj_kernel<uint16_t>, grid, dim3(256), 0, s, a);
-  return launch_k(keyproj_kernel<float>, grid, dim3(256), 0, s, a);
+  return a.dtype ? launch_nt<uint16_t, KeyLaunch>(a, grid, s) : launch_nt<float, KeyLaunch>(a, grid, s);
 }
 
 hipError_t launch_keyln(const KeyLnArgs& a, hipStream_t s) {
