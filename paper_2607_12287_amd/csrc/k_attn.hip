@@ -98,7 +98,12 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, n = lane & 15;
-  const int h = blockIdx.y, v = blockIdx.z;
+  // launch order: heads, then streams, then query groups, so the query
+  // groups that are likely to have rows (the first of every head and stream)
+  // are dispatched before all groups that will find none; the query groups of
+  // one head and stream are H * B launch positions apart, which keeps them on
+  // one XCD whenever H * B is a multiple of 8
+  const int h = blockIdx.x, v = blockIdx.y, qg = blockIdx.z;
   const int N = a.sh.N, dh = a.sh.dh, D = a.sh.D;
   const int nkb = (N + 31) / 32;  // = Npad / 32
   const T* kbase = reinterpret_cast<const T*>(a.caches.p[v] + a.cl.k + (size_t)a.layer * a.cl.kv_layer) +
@@ -122,10 +127,10 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(AttnArgs a) {
   // The first query groups of a stream are the likely active ones: they load
   // before reading the offsets.  The other groups read them first and leave
   // without loading when they have no rows.
-  const bool spec = (int)blockIdx.x < a.nspec;
+  const bool spec = qg < a.nspec;
   if (spec && kb0 < kb1) load_group(kb0);
 
-  const int q0 = blockIdx.x * QT * 16;
+  const int q0 = qg * QT * 16;
   // Q fragments: dims past d_h read in-bounds data of the same row and are
   // not zeroed, because the K fragments are zero there (no select on Q, so no
   // wait right after its loads)
@@ -304,8 +309,8 @@ hipError_t launch_attn(const AttnArgs& a0, int max_rows_per_view, int qtiles, hi
   AttnArgs a = a0;
   if (!a.sh.dtype) qtiles = 1;
   const int qrows = 16 * qtiles;
-  dim3 grid((max_rows_per_view + qrows - 1) / qrows, a.sh.H, a.B);
-  if (grid.x == 0) return hipSuccess;
+  dim3 grid(a.sh.H, a.B, (max_rows_per_view + qrows - 1) / qrows);
+  if (grid.z == 0) return hipSuccess;
   a.nspec = qtiles == 1 ? 2 : 1;
   if (!a.sh.dtype) launch_dh<float, 1>(a, grid, s);  // fp32 operands: one tile (registers)
   else if (qtiles == 1) launch_dh<uint16_t, 1>(a, grid, s);
