@@ -283,6 +283,33 @@ def measure_variant(wl, frames, score: str, period: int, steps: int, warmup: int
     return res
 
 
+def measure_flow(S: int, n: int, reps: int = 200):
+    """The two-anchor flow update on S samples of n values (action chunks of
+    horizon 50 x 32 dimensions by default): time per launch from HIP events
+    over `reps` launches on the current stream, and its algorithmic bytes
+    (x_0, v_0, v_7, b read, x_T written, fp32)."""
+    import torch
+    from paper_2607_12287_amd import incvit
+    g = torch.Generator(device="cuda").manual_seed(7)
+    x0, v0, v7, b = (torch.randn(S, n, device="cuda", generator=g) for _ in range(4))
+    al, be = (torch.randn(S, device="cuda", generator=g) for _ in range(2))
+    out = torch.empty_like(x0)
+    for _ in range(10):
+        incvit.flow_two_anchor(x0, v0, v7, al, be, b, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        incvit.flow_two_anchor(x0, v0, v7, al, be, b, out=out)
+    e1.record()
+    e1.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    nbytes = 5 * S * n * 4 + 2 * S * 4
+    return {"samples": S, "values_per_sample": n, "us_per_launch": round(us, 3),
+            "bytes_per_launch": nbytes, "achieved_gbs": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "note": "launch-bound at this size; back-to-back launches include the launch gap"}
+
+
 def cpu_baseline(wl, frames, seconds: float):
     """The oracle as it is, on this host: full encode of frame 0, then steps of
     the same stream until about `seconds` of step time have been spent."""
@@ -647,6 +674,9 @@ def main() -> int:
         # the non-exact reading of the MLP over all tokens (embedding score)
         result["variants"].append(measure_variant(wl, frames, "embed", 0, vsteps, vwarm, args.full_repeats,
                                                   mlp="all"))
+
+    if not args.no_variants:
+        result["flow_two_anchor"] = measure_flow(64, 50 * 32)
 
     if not args.no_cpu_baseline:
         n_cpu = min(len(frames_np), 64)

@@ -213,6 +213,23 @@ incvit_status incvit_cache_status(const incvit_handle* h, const void* cache, voi
  * h is NULL).  Valid until the next call on h. */
 const char* incvit_last_error(const incvit_handle* h);
 
+/* ----------------------------------------------------------- action side -- */
+
+/* The compressed 2-step flow update of the action expert (§III-C): with the
+ * solver's step velocities modelled by two anchors (the first, v_0, and a
+ * mid-trajectory one, v_7), the Euler sum reduces to, for each of S samples,
+ *   x_T[s] = x_0[s] + alpha[s] v_0[s] + beta[s] v_7[s] + b[s],
+ * elementwise over the n values of a sample (an action chunk: horizon x action
+ * dimensions).  The coefficients come from the caller (the paper predicts them
+ * with a trained adaptor from v_0).  All device fp32: x0, v0, v7, b, xT [S][n];
+ * alpha, beta [S]; xT may alias x0, no other overlap.  Evaluated as
+ * fma(beta, v7, fma(alpha, v0, x0)) + b.  S >= 1, n >= 1, pointers non-null,
+ * else INCVIT_ERR_ARG before anything is enqueued (text: incvit_last_error(NULL)).
+ * Asynchronous on `stream`. */
+incvit_status incvit_flow_two_anchor(int32_t S, int64_t n, const float* x0, const float* v0,
+                                     const float* v7, const float* alpha, const float* beta,
+                                     const float* b, float* xT, void* stream);
+
 /* ------------------------------------------------------------ HIP graphs -- */
 
 typedef struct incvit_graph incvit_graph;

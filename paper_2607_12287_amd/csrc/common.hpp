@@ -270,6 +270,19 @@ struct ConvArgs {  // storage dtype vector -> fp32 (with zero padding)
   int dtype;
 };
 
+// The two-anchor flow update: x_T[s] = x_0[s] + alpha[s] v_0[s] + beta[s] v_7[s] + b[s].
+struct FlowArgs {
+  const float* x0;
+  const float* v0;
+  const float* v7;
+  const float* alpha;  // [S]
+  const float* beta;   // [S]
+  const float* b;
+  float* xT;           // [S][n]; may alias x0
+  int S;
+  long n;
+};
+
 struct ExportArgs {
   const char* cache;
   char* canon;
@@ -312,6 +325,7 @@ hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);
 hipError_t launch_export(const ExportArgs& a, hipStream_t s);
+hipError_t launch_flow(const FlowArgs& a, hipStream_t s);
 
 }  // namespace incvit
 

@@ -782,6 +782,16 @@ incvit_status incvit_encode_frame(incvit_handle* h, int32_t B, const float* patc
   return incvit_step(h, B, patches, caches, tau, cap, idx, count, refreshed, workspace, stream);
 }
 
+incvit_status incvit_flow_two_anchor(int32_t S, int64_t n, const float* x0, const float* v0, const float* v7,
+                                     const float* alpha, const float* beta, const float* b, float* xT, void* stream) {
+  if (S < 1 || n < 1) return fail(nullptr, INCVIT_ERR_ARG, "S and n must be >= 1");
+  if (!x0 || !v0 || !v7 || !alpha || !beta || !b || !xT) return fail(nullptr, INCVIT_ERR_ARG, "null buffer");
+  FlowArgs a{x0, v0, v7, alpha, beta, b, xT, S, (long)n};
+  const hipError_t e = launch_flow(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(nullptr, INCVIT_ERR_HIP, std::string("flow: ") + hipGetErrorString(e));
+  return INCVIT_OK;
+}
+
 incvit_status incvit_cache_export(const incvit_handle* h, const void* cache, void* canonical_dst, void* stream) {
   if (!h || !cache || !canonical_dst) return fail(const_cast<incvit_handle*>(h), INCVIT_ERR_ARG, "null argument");
   ExportArgs a{static_cast<const char*>(cache), static_cast<char*>(canonical_dst), h->cl, h->sh, 1, h->hash};

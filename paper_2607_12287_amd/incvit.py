@@ -32,7 +32,8 @@ EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "inc
            "incvit_workspace_bytes", "incvit_full_encode", "incvit_step", "incvit_cache_export",
            "incvit_cache_import", "incvit_cache_status", "incvit_last_error", "incvit_profile_enable",
            "incvit_profile_read", "incvit_step_graph_create", "incvit_full_graph_create",
-           "incvit_graph_launch", "incvit_graph_destroy", "incvit_set_tuning", "incvit_encode_frame")
+           "incvit_graph_launch", "incvit_graph_destroy", "incvit_set_tuning", "incvit_encode_frame",
+           "incvit_flow_two_anchor")
 
 
 class incvit_config(ctypes.Structure):
@@ -87,6 +88,7 @@ def lib() -> ctypes.CDLL:
             "incvit_graph_destroy": (None, [P]),
             "incvit_set_tuning": (I32, [P, ctypes.POINTER(incvit_tuning)]),
             "incvit_encode_frame": (I32, [P, I32, P, P, ctypes.c_int64, I32, F32, P, P, P, P, P, P]),
+            "incvit_flow_two_anchor": (I32, [I32, ctypes.c_int64, P, P, P, P, P, P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -159,6 +161,28 @@ def incvit_encode_frame(h, B: int, patches: int, caches: Sequence[int], frame_in
     caps = (ctypes.c_int32 * B)(*[int(c) for c in cap])
     return lib().incvit_encode_frame(h, B, patches, _ptr_array(caches), int(frame_index), int(period), float(tau),
                                      caps, idx, count, refreshed, workspace, stream)
+
+
+def incvit_flow_two_anchor(S: int, n: int, x0: int, v0: int, v7: int, alpha: int, beta: int, b: int, xT: int,
+                           stream: int = 0) -> int:
+    return lib().incvit_flow_two_anchor(int(S), int(n), x0, v0, v7, alpha, beta, b, xT, stream)
+
+
+def flow_two_anchor(x0, v0, v7, alpha, beta, b, out=None):
+    """x_T = x_0 + alpha v_0 + beta v_7 + b per sample on device fp32 tensors
+    ([S][...] and [S]); returns out (a new tensor unless given)."""
+    import torch
+    S = x0.shape[0]
+    n = x0.numel() // S
+    for t in (x0, v0, v7, b):
+        assert t.is_cuda and t.dtype == torch.float32 and t.is_contiguous() and t.numel() == S * n
+    assert alpha.numel() == S and beta.numel() == S and alpha.is_contiguous() and beta.is_contiguous()
+    if out is None:
+        out = torch.empty_like(x0)
+    _check(incvit_flow_two_anchor(S, n, x0.data_ptr(), v0.data_ptr(), v7.data_ptr(), alpha.data_ptr(),
+                                  beta.data_ptr(), b.data_ptr(), out.data_ptr(),
+                                  torch.cuda.current_stream(x0.device).cuda_stream))
+    return out
 
 
 def incvit_cache_export(h, cache: int, dst: int, stream: int = 0) -> int:
