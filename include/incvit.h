@@ -263,6 +263,8 @@ void incvit_graph_destroy(incvit_graph* g);
  * projection, 2 = MLP up, 3 = MLP down): 1 or 2 (2 only takes effect when the
  * block count is even); 0 = automatic.
  * attn_qtiles: 16-query tiles per attention workgroup: 1 or 2; 0 = automatic.
+ * attn_waves: waves per attention workgroup, splitting the stream's keys: 2, 4
+ * or 8; 0 = automatic (about two 32-key blocks per wave).
  * row_groups: 32-row groups per GEMM launch in steps with a finite threshold
  * (1..8; 0 = 1): a caller that expects about R refreshed rows per call can set
  * ceil(R / 32).  Full encodes and pure top-k steps (tau = +inf), whose row
@@ -272,6 +274,7 @@ typedef struct {
   int32_t cols[4];
   int32_t attn_qtiles;
   int32_t row_groups;
+  int32_t attn_waves;
 } incvit_tuning;
 
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);

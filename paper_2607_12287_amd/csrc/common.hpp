@@ -320,7 +320,7 @@ hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s);
 hipError_t launch_hsum(const HsumArgs& a, hipStream_t s);
-hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, int qtiles, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, int qtiles, int waves, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs& a, hipStream_t s);

@@ -281,6 +281,7 @@ struct incvit_handle {
   int64_t prof_n[INCVIT_K_COUNT] = {};
   int cols[4] = {0, 0, 0, 0};  // 0 = automatic
   int attn_qtiles = 0;         // 0 = automatic
+  int attn_waves = 0;          // 0 = automatic
   int row_groups = 1;          // GEMM row groups of threshold steps
 };
 
@@ -459,7 +460,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       aa.qmax = wl.Mpad - 1;
       aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
       const int qtiles = attn_qtiles_of(h->attn_qtiles, B, sh.H, max_rows_per_view);
-      if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, qtiles, s); })) != INCVIT_OK)
+      if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, qtiles, h->attn_waves, s); })) != INCVIT_OK)
         return st;
       if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
     }
@@ -862,9 +863,12 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   if (q < 0 || q > 2) return fail(h, INCVIT_ERR_ARG, "attn_qtiles must be 0, 1 or 2");
   const int rg = t ? t->row_groups : 0;
   if (rg < 0 || rg > 8) return fail(h, INCVIT_ERR_ARG, "row_groups must be in [0, 8]");
+  const int aw = t ? t->attn_waves : 0;
+  if (aw != 0 && aw != 2 && aw != 4 && aw != 8) return fail(h, INCVIT_ERR_ARG, "attn_waves must be 0, 2, 4 or 8");
   for (int k = 0; k < 4; ++k) h->cols[k] = t ? t->cols[k] : 0;
   h->attn_qtiles = q;
   h->row_groups = rg > 0 ? rg : 1;
+  h->attn_waves = aw;
   return INCVIT_OK;
 }
 

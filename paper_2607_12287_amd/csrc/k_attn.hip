@@ -78,21 +78,19 @@ __device__ __forceinline__ void mask_v(V8<float>& v, int first_key, int N) {
 }
 
 // One workgroup: QT query tiles (16 queries each) of one head of one stream.
-// Its KW = 8 waves split the stream's key blocks into contiguous runs (one
-// 32-key block per wave at N = 256), so the K/V of a head are pulled through
-// the CU by eight waves at once and each wave's chain of dependent MFMA and
-// softmax steps is short; every wave processes all QT query tiles against
-// its keys.  Key/value loads do not depend on the row offsets, so the first
+// Its KW waves split the stream's key blocks into contiguous runs (about two
+// 32-key blocks per wave: 4 waves at N = 256, 8 at N = 1024), so the K/V of a
+// head are pulled through the CU by several waves at once and each wave's
+// chain of dependent MFMA and softmax steps stays short, while the exchange
+// of the waves' partial results stays small; every wave processes all QT
+// query tiles against its keys.  Key/value loads do not depend on the row offsets, so the first
 // `a.nspec` query groups issue their first key blocks before the offsets are
 // read; the first stream's rows always start at 0, so its query loads are
 // issued early too.  The waves' (max, sum, O) are exchanged through LDS once
 // and combined in wave order, each wave finishing a share of the output
 // tiles.
-constexpr int kAttnWaves = 8;
-
-template <class T, int NDC, int NDT, int GB, int QT>
-__global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(AttnArgs a) {
-  constexpr int KW = kAttnWaves;
+template <class T, int NDC, int NDT, int GB, int QT, int KW>
+__global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
   extern __shared__ __align__(16) char attn_smem[];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -270,51 +268,57 @@ __global__ __launch_bounds__(kAttnWaves * 64) void attn_kernel(AttnArgs a) {
   }
 }
 
-template <int NDT, int QT>
+template <int NDT, int QT, int KW>
 constexpr int attn_lds_bytes() {
-  return kAttnWaves * QT * 16 * 4 * 2 + kAttnWaves * QT * NDT * 64 * 16;  // m and l, then O
+  return KW * QT * 16 * 4 * 2 + KW * QT * NDT * 64 * 16;  // m and l, then O
 }
 
-template <class T, int NDC, int NDT, int GB, int QT>
+template <class T, int NDC, int NDT, int GB, int QT, int KW>
 static void launch_g(const AttnArgs& a, dim3 grid, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, GB, QT>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, attn_lds_bytes<NDT, QT>()) == hipSuccess;
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, GB, QT, KW>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               attn_lds_bytes<NDT, QT, KW>()) == hipSuccess;
   }
-  (void)launch_k((attn_kernel<T, NDC, NDT, GB, QT>), grid, dim3(kAttnWaves * 64), (size_t)attn_lds_bytes<NDT, QT>(),
+  (void)launch_k((attn_kernel<T, NDC, NDT, GB, QT, KW>), grid, dim3(KW * 64), (size_t)attn_lds_bytes<NDT, QT, KW>(),
                  s, a);
 }
 
 template <class T, int NDC, int NDT, int QT>
-static void launch_t(const AttnArgs& a, dim3 grid, hipStream_t s) {
+static void launch_t(const AttnArgs& a, int kw, dim3 grid, hipStream_t s) {
   // two key blocks in flight per wave where the registers allow
   constexpr int kGB = NDT <= (sizeof(T) == 2 ? 6 : 4) ? 2 : 1;
-  launch_g<T, NDC, NDT, kGB, QT>(a, grid, s);
+  if (kw == 2) launch_g<T, NDC, NDT, kGB, QT, 2>(a, grid, s);
+  else if (kw == 4) launch_g<T, NDC, NDT, kGB, QT, 4>(a, grid, s);
+  else launch_g<T, NDC, NDT, kGB, QT, 8>(a, grid, s);
 }
 
 template <class T, int QT>
-static void launch_dh(const AttnArgs& a, dim3 grid, hipStream_t s) {
+static void launch_dh(const AttnArgs& a, int kw, dim3 grid, hipStream_t s) {
   const int dh = a.sh.dh;
-  if (dh <= 32) launch_t<T, 1, 2, QT>(a, grid, s);
-  else if (dh <= 64) launch_t<T, 2, 4, QT>(a, grid, s);
-  else if (dh <= 96) launch_t<T, 3, 6, QT>(a, grid, s);
-  else launch_t<T, 4, 8, QT>(a, grid, s);
+  if (dh <= 32) launch_t<T, 1, 2, QT>(a, kw, grid, s);
+  else if (dh <= 64) launch_t<T, 2, 4, QT>(a, kw, grid, s);
+  else if (dh <= 96) launch_t<T, 3, 6, QT>(a, kw, grid, s);
+  else launch_t<T, 4, 8, QT>(a, kw, grid, s);
 }
 
 // qtiles: 16-query tiles per workgroup (1 or 2).  One tile per workgroup
 // doubles the workgroups (and the K/V reads) for short per-stream row counts;
-// two halve the K/V traffic when there are many rows.
-hipError_t launch_attn(const AttnArgs& a0, int max_rows_per_view, int qtiles, hipStream_t s) {
+// two halve the K/V traffic when there are many rows.  waves: 2, 4 or 8 per
+// workgroup; 0 = about two key blocks per wave.
+hipError_t launch_attn(const AttnArgs& a0, int max_rows_per_view, int qtiles, int waves, hipStream_t s) {
   AttnArgs a = a0;
   if (!a.sh.dtype) qtiles = 1;
   const int qrows = 16 * qtiles;
   dim3 grid(a.sh.H, a.B, (max_rows_per_view + qrows - 1) / qrows);
   if (grid.z == 0) return hipSuccess;
   a.nspec = qtiles == 1 ? 2 : 1;
-  if (!a.sh.dtype) launch_dh<float, 1>(a, grid, s);  // fp32 operands: one tile (registers)
-  else if (qtiles == 1) launch_dh<uint16_t, 1>(a, grid, s);
-  else launch_dh<uint16_t, 2>(a, grid, s);
+  const int nkb = a.sh.Npad / 32;
+  const int kw = waves > 0 ? waves : nkb >= 16 ? 8 : 4;
+  if (!a.sh.dtype) launch_dh<float, 1>(a, kw, grid, s);  // fp32 operands: one tile (registers)
+  else if (qtiles == 1) launch_dh<uint16_t, 1>(a, kw, grid, s);
+  else launch_dh<uint16_t, 2>(a, kw, grid, s);
   return hipGetLastError();
 }
 

@@ -45,7 +45,8 @@ class incvit_config(ctypes.Structure):
 
 
 class incvit_tuning(ctypes.Structure):
-    _fields_ = [("cols", ctypes.c_int32 * 4), ("attn_qtiles", ctypes.c_int32), ("row_groups", ctypes.c_int32)]
+    _fields_ = [("cols", ctypes.c_int32 * 4), ("attn_qtiles", ctypes.c_int32), ("row_groups", ctypes.c_int32),
+                ("attn_waves", ctypes.c_int32)]
 
 
 class IncvitError(RuntimeError):
@@ -236,11 +237,12 @@ def incvit_graph_destroy(g) -> None:
     lib().incvit_graph_destroy(g)
 
 
-def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None, attn_qtiles: int = 0, row_groups: int = 0) -> int:
-    if cols is None and not attn_qtiles and not row_groups:
+def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None, attn_qtiles: int = 0, row_groups: int = 0,
+                      attn_waves: int = 0) -> int:
+    if cols is None and not attn_qtiles and not row_groups and not attn_waves:
         return lib().incvit_set_tuning(h, None)
     t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in (cols or (0, 0, 0, 0))]), int(attn_qtiles),
-                      int(row_groups))
+                      int(row_groups), int(attn_waves))
     return lib().incvit_set_tuning(h, ctypes.byref(t))
 
 

@@ -236,4 +236,5 @@ def test_argument_errors_are_reported_before_launch():
     assert L.incvit_set_tuning(enc.h, [3, 0, 0, 0]) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, [0, 0, -1, 0]) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, [1, 2, 0, 2]) == L.INCVIT_OK
+    assert L.incvit_set_tuning(enc.h, attn_waves=3) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, None) == L.INCVIT_OK

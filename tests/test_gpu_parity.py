@@ -84,3 +84,25 @@ def test_so400m_448_top_k(rho):
 
 def test_vitl_eight_streams_sampled():
     _workload_run("vitl_x8", 2, oracle_views=[0, 5])
+
+
+@pytest.mark.parametrize("waves", [2, 4, 8])
+@pytest.mark.parametrize("qtiles", [1, 2])
+def test_attention_tunings(waves, qtiles):
+    """Every attention workgroup shape (waves splitting the keys, query tiles
+    per workgroup) meets the parity bar: they differ only in the order of the
+    fp32 partial sums."""
+    from paper_2607_12287_amd import incvit
+    m = synth.small_model(dim=288, depth=2, heads=4, mlp=300, img=64, patch=4, dtype="bf16")
+    w = synth.make_weights(m, 951)
+    say(f"[attn waves={waves} qtiles={qtiles}] N={m.n_tokens} dh={m.head_dim}")
+    its = [synth.RefillRectStream(m, 960 + v, v, 21, 30).frames(3) for v in range(2)]
+    frames = [np.stack([synth.patchify(next(it), m.patch) for it in its]) for _ in range(3)]
+    p = Pair(m, w, 2)
+    incvit._check(incvit.incvit_set_tuning(p.enc.h, attn_qtiles=qtiles, attn_waves=waves), p.enc.h)
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    for t in (1, 2):
+        idx, count, refreshed, res = p.step(frames[t], 0.98, [m.n_tokens, 40])
+        p.check_step(idx, count, refreshed, res, f"step {t}")
+        p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
