@@ -511,6 +511,8 @@ def main() -> int:
     ap.add_argument("--attn-qtiles", type=int, default=0, help="16-query tiles per attention workgroup (0 = automatic)")
     ap.add_argument("--row-groups", type=int, default=0, help="GEMM row groups of threshold steps (0 = 1)")
     ap.add_argument("--attn-waves", type=int, default=0, help="waves per attention workgroup (0 = automatic)")
+    ap.add_argument("--fc2-mode", type=int, default=0, help="MLP down projection: 1 split-K + row kernel, "
+                                                            "2 unsplit with the residual in the epilogue (0 = default)")
     args = ap.parse_args()
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace)
@@ -542,10 +544,10 @@ def main() -> int:
     torch.cuda.set_device(dev)
     frames = torch.from_numpy(np.stack(frames_np)).to(dev)  # [T][B][N][P], resident in HBM
     enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
-    if args.cols or args.attn_qtiles or args.row_groups or args.attn_waves:
+    if args.cols or args.attn_qtiles or args.row_groups or args.attn_waves or args.fc2_mode:
         cols = [int(x) for x in args.cols.split(",")] if args.cols else None
-        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles, args.row_groups, args.attn_waves),
-                      enc.h)
+        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles, args.row_groups, args.attn_waves,
+                                               args.fc2_mode), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),

@@ -265,6 +265,11 @@ void incvit_graph_destroy(incvit_graph* g);
  * attn_qtiles: 16-query tiles per attention workgroup: 1 or 2; 0 = automatic.
  * attn_waves: waves per attention workgroup, splitting the stream's keys: 2, 4
  * or 8; 0 = automatic (about two 32-key blocks per wave).
+ * fc2_mode: the MLP down projection of every layer but the last: 1 = K split
+ * over workgroups, partial sums finished by a row kernel; 2 = whole K per
+ * workgroup with the residual and the cache write in its epilogue; 0 = 2 when
+ * the call's row count is known on the host (full encodes, pure top-k steps)
+ * and at least 192, else 1.
  * row_groups: 32-row groups per GEMM launch in steps with a finite threshold
  * (1..8; 0 = 1): a caller that expects about R refreshed rows per call can set
  * ceil(R / 32).  Full encodes and pure top-k steps (tau = +inf), whose row
@@ -275,6 +280,7 @@ typedef struct {
   int32_t attn_qtiles;
   int32_t row_groups;
   int32_t attn_waves;
+  int32_t fc2_mode;
 } incvit_tuning;
 
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);

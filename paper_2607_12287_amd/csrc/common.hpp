@@ -166,7 +166,7 @@ struct RowsArgs {  // commit: ref/X0/Z0 of the refreshed rows, row map
   int* zpos;
 };
 
-enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3, EPI_ATT = 4 };
+enum Epi { EPI_QKV = 0, EPI_FC1 = 1, EPI_PART = 2, EPI_RES = 3, EPI_ATT = 4, EPI_DOWN = 5 };
 
 // Fields in the order the kernel's prologue needs them, so that its argument
 // loads go out together.
@@ -178,9 +178,10 @@ struct GemmArgs {
                       // then holds beta^T W + b (see FoldArgs)
   const RowInfo* rows;  // row map (cache, token, stream) of each compact row
   const Meta* meta;
-  const void* resid;  // RES: Z_l rows (operand order)
+  const void* resid;  // RES: Z_l rows, DOWN: H rows (operand order)
   void* out;          // QKV Q [Mpad][D]; RES H (operand order); FC1 G; PART f32 [ksplit][mpad][ldo];
-                      // ATT: unused (rows go to the cache's A^l)
+                      // ATT: unused (rows go to the cache's A^l); DOWN: Z_{l+1} (operand
+                      // order), also written to the cache's X^{l+1}
   int lda, kchunks, Nout, ldo;
   int ksplit;         // K is split over ksplit workgroups (PART)
   int rgroups;        // 32-row groups launched: enough for the largest M of the call

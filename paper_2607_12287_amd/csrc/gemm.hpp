@@ -10,7 +10,10 @@
 //         next LayerNorm;
 //   ATT : the attention branch S(O W_o + b_o) alone, scattered into the
 //         cache's A^l rows (the all-rows MLP reading, whose residual is
-//         formed for every row by a row kernel).
+//         formed for every row by a row kernel);
+//   DOWN: the MLP down projection over the whole K with its residual,
+//         Z_{l+1} = S(H + (G W_2 + b_2)) into the compact Z and the cache's
+//         X^{l+1} (one kernel instead of split-K partials and a row kernel).
 // Z, O, H and G are kept in MFMA operand order (frag_off).
 //
 // LayerNorm folded into the GEMM (QKV, FC1): the weights are packed as
@@ -58,6 +61,14 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   return 0.5f * x * (1.0f + tanhf(u));
 }
 
+template <int EPI>
+__host__ __device__ constexpr bool has_resid() {
+  return EPI == EPI_RES || EPI == EPI_DOWN;
+}
+template <int EPI>
+__host__ __device__ constexpr bool has_rows() {
+  return EPI == EPI_QKV || EPI == EPI_ATT || EPI == EPI_DOWN;
+}
 template <int EPI>
 __host__ __device__ constexpr bool ln_on_load() {
   return EPI == EPI_QKV || EPI == EPI_FC1;
@@ -166,11 +177,11 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   load_w(0);
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    biasv[b] = EPI == EPI_PART ? 0.0f : a.bias[(cb0 + b) * 16 + n];
+    biasv[b] = EPI == EPI_PART ? 0.0f : a.bias[(cb0 + b) * 16 + n];  // DOWN: b_2
     c1v[b] = LNA ? a.c1[(cb0 + b) * 16 + n] : 0.0f;
   }
-  if constexpr (EPI == EPI_QKV || EPI == EPI_ATT) rinfo = a.rows[mfirst + 16 * re + 4 * g + ie];
-  if constexpr (EPI == EPI_RES) load_res(mfirst);
+  if constexpr (has_rows<EPI>()) rinfo = a.rows[mfirst + 16 * re + 4 * g + ie];
+  if constexpr (has_resid<EPI>()) load_res(mfirst);
 
   // One 32-row block.  The group's first block is a copy of its own (FIRST),
   // so its waits count exactly the loads issued above instead of the fewer a
@@ -179,8 +190,8 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
     if constexpr (!decltype(first)::value) {
       load_a(m0, 0);
       if (rounds > 1) load_w(0);
-      if constexpr (EPI == EPI_QKV || EPI == EPI_ATT) rinfo = a.rows[m0 + 16 * re + 4 * g + ie];
-      if constexpr (EPI == EPI_RES) load_res(m0);
+      if constexpr (has_rows<EPI>()) rinfo = a.rows[m0 + 16 * re + 4 * g + ie];
+      if constexpr (has_resid<EPI>()) load_res(m0);
     }
     f32x4_t acc[2][NB], accs[2], accq[2];  // accs, accq: row sums and sums of squares (LNA)
 #pragma unroll
@@ -259,6 +270,12 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
         if (ok) static_cast<float*>(a.out)[((size_t)ks * a.mpad + row) * a.ldo + col] = x;
       } else if constexpr (EPI == EPI_RES) {  // H = S(Z + (O W_o + b_o))
         if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resv[b] + (x + biasv[b]));
+      } else if constexpr (EPI == EPI_DOWN) {  // Z_{l+1} = S(H + (G W_2 + b_2))
+        if (ok) {
+          const T z = Elem<T>::cv(resv[b] + (x + biasv[b]));
+          static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = z;
+          gbl(x_row<T>(rinfo.cache, a.cl, a.sh, a.layer + 1, rinfo.tok))[col] = z;
+        }
       } else if constexpr (EPI == EPI_ATT) {  // A^l[tok] = S(O W_o + b_o)
         if (ok) {
           T* arow = reinterpret_cast<T*>(rinfo.cache + a.cl.a + (size_t)a.layer * a.cl.x_layer);

@@ -282,6 +282,7 @@ struct incvit_handle {
   int cols[4] = {0, 0, 0, 0};  // 0 = automatic
   int attn_qtiles = 0;         // 0 = automatic
   int attn_waves = 0;          // 0 = automatic
+  int fc2_mode = 0;            // 1: split-K + row kernel, 2: unsplit with the residual in the epilogue, 0: by M
   int row_groups = 1;          // GEMM row groups of threshold steps
 };
 
@@ -370,8 +371,18 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
   const int mgroups = all ? groups_for(mall, true) : rgroups;
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
+    // the MLP down projection of every layer but the last (whose row kernel
+    // also applies the final LayerNorm) can run unsplit with the residual and
+    // the cache write in its epilogue instead of split-K partials + row kernel:
+    // slower for a few dozen rows (the whole K of 16 columns per workgroup
+    // against a third of it), faster once M is in the hundreds (the partial
+    // sums of every row no longer go through memory), so by default only when
+    // M is known on the host and at least 192
+    const bool down = !all && l + 1 < sh.L &&
+                      (h->fc2_mode == 2 || (h->fc2_mode == 0 && exact_m && mmax >= 192));
     auto gemm = [&](int kind, int kernel_kind) -> incvit_status {
-      const GemmGeom g = gemm_geom(sh, kind);
+      GemmGeom g = gemm_geom(sh, kind);
+      if (kind == G_FC2 && down) g.ksplit = 1;
       const bool mlp = kind == G_FC1 || kind == G_FC2;
       GemmArgs a;
       memset(&a, 0, sizeof a);
@@ -410,6 +421,12 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           a.A = ws + wl.g; a.lda = sh.Fpad;
           a.W = h->packed + P.w_2;
           a.out = ws + wl.part; a.ldo = sh.D;
+          if (down) {
+            epi = EPI_DOWN;
+            a.bias = fptr(h, P.b_2);
+            a.resid = ws + wl.h;
+            a.out = ws + wl.z;
+          }
           break;
       }
       const int cols = cols_of(h->cols, g, kind);
@@ -470,7 +487,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
     }
     if ((st = gemm(G_FC1, INCVIT_K_FC1)) != INCVIT_OK) return st;
     if ((st = gemm(G_FC2, INCVIT_K_FC2)) != INCVIT_OK) return st;
-    if ((st = rowk(INCVIT_K_RES_LN1)) != INCVIT_OK) return st;
+    if (!down && (st = rowk(INCVIT_K_RES_LN1)) != INCVIT_OK) return st;
   }
   return INCVIT_OK;
 }
@@ -865,10 +882,13 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   if (rg < 0 || rg > 8) return fail(h, INCVIT_ERR_ARG, "row_groups must be in [0, 8]");
   const int aw = t ? t->attn_waves : 0;
   if (aw != 0 && aw != 2 && aw != 4 && aw != 8) return fail(h, INCVIT_ERR_ARG, "attn_waves must be 0, 2, 4 or 8");
+  const int fm = t ? t->fc2_mode : 0;
+  if (fm < 0 || fm > 2) return fail(h, INCVIT_ERR_ARG, "fc2_mode must be 0, 1 or 2");
   for (int k = 0; k < 4; ++k) h->cols[k] = t ? t->cols[k] : 0;
   h->attn_qtiles = q;
   h->row_groups = rg > 0 ? rg : 1;
   h->attn_waves = aw;
+  h->fc2_mode = fm;
   return INCVIT_OK;
 }
 

@@ -9,6 +9,7 @@ hipError_t launch_gemm_fc1(int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_part(int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_res(int cols, const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_att(int cols, const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_down(int cols, const GemmArgs& a, hipStream_t s);
 
 hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s) {
   switch (epi) {
@@ -16,6 +17,7 @@ hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s) {
     case EPI_FC1: return launch_gemm_fc1(cols, a, s);
     case EPI_RES: return launch_gemm_res(cols, a, s);
     case EPI_ATT: return launch_gemm_att(cols, a, s);
+    case EPI_DOWN: return launch_gemm_down(cols, a, s);
     default: return launch_gemm_part(cols, a, s);
   }
 }

@@ -106,3 +106,44 @@ def test_attention_tunings(waves, qtiles):
         idx, count, refreshed, res = p.step(frames[t], 0.98, [m.n_tokens, 40])
         p.check_step(idx, count, refreshed, res, f"step {t}")
         p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_down_projection_modes(mode, dtype):
+    """Both forms of the MLP down projection (K split with a row kernel; whole
+    K with the residual and the cache write in the epilogue, on every layer but
+    the last) meet the parity bar, in full encodes and steps."""
+    from paper_2607_12287_amd import incvit
+    m = synth.small_model(dim=256, depth=3, heads=4, mlp=520, img=40, patch=4, dtype=dtype)
+    w = synth.make_weights(m, 971)
+    say(f"[fc2 mode {mode} {dtype}] N={m.n_tokens} F={m.mlp_dim}")
+    its = [synth.RefillRectStream(m, 980 + v, v, 15, 19).frames(3) for v in range(2)]
+    frames = [np.stack([synth.patchify(next(it), m.patch) for it in its]) for _ in range(3)]
+    p = Pair(m, w, 2)
+    incvit._check(incvit.incvit_set_tuning(p.enc.h, fc2_mode=mode), p.enc.h)
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    p.check_caches("full")
+    for t in (1, 2):
+        idx, count, refreshed, res = p.step(frames[t], [0.98, np.inf][t - 1], [m.n_tokens, 30])
+        p.check_step(idx, count, refreshed, res, f"step {t}")
+        p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
+        p.check_caches(f"step {t}")
+
+
+def test_down_projection_fused_so400m():
+    from paper_2607_12287_amd import incvit
+    wl = synth.workload("so400m")
+    say("[fc2 mode 2 so400m]")
+    p = Pair(wl.model, wl.weights(), 1)
+    incvit._check(incvit.incvit_set_tuning(p.enc.h, fc2_mode=2), p.enc.h)
+    frames = list(wl.patch_frames(3))
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    for t in (1, 2):
+        idx, count, refreshed, res = p.step(frames[t], wl.tau, wl.caps)
+        p.check_step(idx, count, refreshed, res, f"step {t}")
+        tf = p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
+        worst = p.check_caches(f"step {t}")
+        say(f"  step {t}: count={count.tolist()} per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
