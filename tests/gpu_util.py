@@ -48,7 +48,8 @@ class Pair:
         self.enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=B, score=score, mlp=mlp)
         self.model = vit.Model(m, w, score=score, mlp=mlp)
         self.buf, self.caches = self.enc.new_caches(B)
-        self.views = list(range(B)) if oracle_views is None else list(oracle_views)
+        # each sampled stream once (the oracle steps every listed stream's cache)
+        self.views = list(range(B)) if oracle_views is None else sorted(set(oracle_views))
         self.ora = {}
 
     def full_encode(self, batch: np.ndarray):
