@@ -235,13 +235,17 @@ __global__ __launch_bounds__(256) void keyln_kernel(KeyLnArgs a) {
   const float* x = a.t0 + (size_t)row * D;
   constexpr int kPer = kMaxDim / 64;
   float xv[kPer], g[kPer], b[kPer];
+  // unconditional loads (clamped index), all issued before any is used; the
+  // values past D are never used
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
-    const int d = lane + 64 * j;
-    xv[j] = d < D ? Elem<T>::rnd(x[d]) : 0.0f;
-    g[j] = d < D ? a.ln_g[d] : 0.0f;
-    b[j] = d < D ? a.ln_b[d] : 0.0f;
+    const int d = min(lane + 64 * j, D - 1);
+    xv[j] = x[d];
+    g[j] = a.ln_g[d];
+    b[j] = a.ln_b[d];
   }
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) xv[j] = Elem<T>::rnd(xv[j]);
   float p = 0.0f;
 #pragma unroll
   for (int j = 0; j < kPer; ++j)
@@ -273,15 +277,17 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
   const float* y = reinterpret_cast<const float*>(a.caches.p[v] + a.ref_off) + (size_t)tok * a.D;
   constexpr int kPer = kMaxDim / 64;
   float xv[kPer], yv[kPer];
+  // unconditional loads (clamped index), all issued before any is used; the
+  // values past D are never used
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
-    const int d = lane + 64 * j;
-    xv[j] = d < a.D ? x[d] : 0.0f;
-    yv[j] = d < a.D ? y[d] : 0.0f;
+    const int d = min(lane + 64 * j, a.D - 1);
+    xv[j] = x[d];
+    yv[j] = y[d];
   }
   float pd = 0.0f, pa = 0.0f, pb = 0.0f;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {  // d = lane + 64 j in increasing d; zero pads add nothing
+  for (int j = 0; j < kPer; ++j) {  // d = lane + 64 j in increasing d; entries past D are skipped
     if (lane + 64 * j < a.D) {
       pd = __fmaf_rn(xv[j], yv[j], pd);
       pa = __fmaf_rn(xv[j], xv[j], pa);
