@@ -310,6 +310,70 @@ def measure_flow(S: int, n: int, reps: int = 200):
             "note": "launch-bound at this size; back-to-back launches include the launch gap"}
 
 
+def rho_sweep(steps: int, full_repeats: int) -> dict:
+    """The 448x448 So400m configuration (N = 1024) under top-k refresh at every
+    ratio of the sweep: graph-replayed steps over the ratio's own moving-blob
+    stream against graph-replayed full encodes of the same model, and the
+    break-even ratio where the step costs as much as the full encode (linear
+    interpolation between the two measured ratios around it)."""
+    import numpy as np
+    import torch
+    from paper_2607_12287_amd import incvit, synth
+    dev = torch.device("cuda:0")
+    enc = None
+    rows = []
+    for rho in synth.RHO_SWEEP:
+        wl = synth.workload("so400m_448", rho=rho)
+        m = wl.model
+        if enc is None:  # the weights do not depend on the ratio
+            enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=1)
+        frames = torch.from_numpy(np.stack(list(wl.patch_frames(steps + 1)))).to(dev)
+        buf, caches = enc.new_caches(1)
+        out = (torch.empty((1, m.n_tokens), dtype=torch.int32, device=dev),
+               torch.empty((1,), dtype=torch.int32, device=dev),
+               torch.empty((1, m.n_tokens, m.dim), dtype=enc.dtype, device=dev))
+        inp = torch.empty_like(frames[0])
+        inp.copy_(frames[0])
+        gfull = enc.full_graph(inp, caches)
+        full_ms = []
+        for i in range(full_repeats + 3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            enc.launch(gfull)
+            e1.record()
+            e1.synchronize()
+            if i >= 3:
+                full_ms.append(e0.elapsed_time(e1))
+        gstep = enc.step_graph(inp, caches, wl.tau, wl.caps, out)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for t in range(1, 4):  # warm-up
+            inp.copy_(frames[t])
+            enc.launch(gstep)
+        torch.cuda.synchronize()
+        e0.record()
+        for t in range(1, steps + 1):
+            inp.copy_(frames[t])
+            enc.launch(gstep)
+        e1.record()
+        e1.synchronize()
+        step_ms = e0.elapsed_time(e1) / steps
+        enc.drop_graph(gstep)
+        enc.drop_graph(gfull)
+        full = statistics.median(full_ms)
+        rows.append({"rho": rho, "rows": wl.caps[0], "step_ms": round(step_ms, 5), "full_encode_ms": round(full, 5),
+                     "speedup": round(full / step_ms, 3)})
+        del buf, caches, frames
+    enc.close()
+    even = None
+    for a, b in zip(rows, rows[1:]):
+        if a["speedup"] >= 1.0 >= b["speedup"] and a["speedup"] != b["speedup"]:
+            f = (a["speedup"] - 1.0) / (a["speedup"] - b["speedup"])
+            even = round(a["rho"] + f * (b["rho"] - a["rho"]), 4)
+            break
+    return {"workload": "so400m_448: 448x448 p14 N=1024 D=1152 L=27, top-k refresh, graph replay, "
+                        f"{steps} steps per ratio", "sweep": rows, "break_even_rho": even}
+
+
 def cpu_baseline(wl, frames, seconds: float):
     """The oracle as it is, on this host: full encode of frame 0, then steps of
     the same stream until about `seconds` of step time have been spent."""
@@ -502,6 +566,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-torch-full", action="store_true", help="skip the torch full forward (context)")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel events")
+    ap.add_argument("--rho-sweep", action="store_true",
+                    help="only the refresh-ratio sweep of the 448x448 configuration and its break-even ratio")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the key-score and odd/even-schedule measurements")
     ap.add_argument("--eager", dest="graph", action="store_false",
@@ -530,6 +596,9 @@ def main() -> int:
         return 2
     if args.copy_pass:
         return copy_pass(args.copy_pass)
+    if args.rho_sweep:
+        print(json.dumps(rho_sweep(min(args.steps, 30), args.full_repeats)), flush=True)
+        return 0
 
     import numpy as np
     import torch
