@@ -19,6 +19,7 @@ import csv
 import glob
 import hashlib
 import json
+import math
 import os
 import re
 import statistics
@@ -575,7 +576,8 @@ def main() -> int:
     ap.add_argument("--cols", default=None, help="column blocks per GEMM workgroup: four comma-separated values "
                                                  "(QKV, O-proj, fc1, fc2; 0 = automatic)")
     ap.add_argument("--attn-qtiles", type=int, default=0, help="16-query tiles per attention workgroup (0 = automatic)")
-    ap.add_argument("--row-groups", type=int, default=0, help="GEMM row groups of threshold steps (0 = 1)")
+    ap.add_argument("--row-groups", type=int, default=0,
+                    help="GEMM row groups of threshold steps (0 = ceil(mean rows / 32) of 8 calibration steps)")
     ap.add_argument("--attn-waves", type=int, default=0, help="waves per attention workgroup (0 = automatic)")
     ap.add_argument("--fc2-mode", type=int, default=0, help="MLP down projection: 1 split-K + row kernel, "
                                                             "2 unsplit with the residual in the epilogue (0 = default)")
@@ -613,9 +615,21 @@ def main() -> int:
     torch.cuda.set_device(dev)
     frames = torch.from_numpy(np.stack(frames_np)).to(dev)  # [T][B][N][P], resident in HBM
     enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
-    if args.cols or args.attn_qtiles or args.row_groups or args.attn_waves or args.fc2_mode:
+    row_groups = args.row_groups
+    if row_groups == 0 and math.isfinite(wl.tau):
+        # a caller that knows how many rows its streams refresh sets the GEMM
+        # row groups of threshold steps (the library cannot know M on the
+        # host): eight eager steps on scratch caches give the mean rows
+        cbuf, ccaches = enc.new_caches(B)
+        enc.full_encode(frames[0], ccaches)
+        seen = []
+        for t in range(1, min(9, total)):
+            seen.append(int(enc.step(frames[t], ccaches, wl.tau, wl.caps)[1].sum()))
+        row_groups = max(1, min(8, math.ceil(statistics.mean(seen) / 32)))
+        del cbuf, ccaches
+    if args.cols or args.attn_qtiles or row_groups > 1 or args.attn_waves or args.fc2_mode:
         cols = [int(x) for x in args.cols.split(",")] if args.cols else None
-        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles, args.row_groups, args.attn_waves,
+        incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles, row_groups, args.attn_waves,
                                                args.fc2_mode), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
@@ -700,7 +714,7 @@ def main() -> int:
                                f"L={m.depth} h={m.heads} F={m.mlp_dim}, {B} stream(s), tau={wl.tau}, "
                                f"caps={wl.caps[:1]}{'...' if B > 1 else ''}",
                    "views": B, "tokens": m.n_tokens, "refresh_mean": round(mean_rows / (B * m.n_tokens), 4),
-                   "rows_mean": round(mean_rows, 2)},
+                   "rows_mean": round(mean_rows, 2), "gemm_row_groups": row_groups},
         "device_ms_per_step": round(dev_ms / args.steps, 5),
         "launch": "hip-graph" if args.graph else "eager",
         "full_encode_ms": round(full_med, 5),
