@@ -16,10 +16,11 @@ from tests.gpu_util import TOL, Pair, rel_err, say
 pytestmark = pytest.mark.gpu
 
 
-def _setup(dtype="bf16", B=2, dim=256, heads=4, mlp=200, img=40, patch=4, frames=4, seed=5):
+def _setup(dtype="bf16", B=2, dim=256, heads=4, mlp=200, img=40, patch=4, frames=4, seed=5, score="embed",
+           mlp_mode="reuse"):
     m = synth.small_model(dim=dim, depth=2, heads=heads, mlp=mlp, img=img, patch=patch, dtype=dtype)
     w = synth.make_weights(m, seed)
-    enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=max(B, 2))
+    enc = incvit.Encoder(m, synth.flatten_weights(m, w), max_streams=max(B, 2), score=score, mlp=mlp_mode)
     streams = [synth.RefillRectStream(m, seed + 10 + v, v, 2 * patch + 5, 3 * patch) for v in range(B)]
     its = [s.frames(frames) for s in streams]
     fr = [torch.from_numpy(np.stack([synth.patchify(next(it), patch) for it in its])).cuda() for _ in range(frames)]
@@ -31,8 +32,14 @@ def _raw(enc, caches):
     return [enc.export_raw(c).clone() for c in caches]
 
 
-def test_step_graph_replays_match_eager_steps():
-    m, w, enc, fr = _setup()
+MODES = [("embed", "reuse", 1), ("key", "reuse", 1), ("embed", "all", 1), ("key", "all", 1), ("embed", "reuse", 3)]
+
+
+@pytest.mark.parametrize("score,mlp_mode,row_groups", MODES)
+def test_step_graph_replays_match_eager_steps(score, mlp_mode, row_groups):
+    m, w, enc, fr = _setup(score=score, mlp_mode=mlp_mode)
+    if row_groups > 1:
+        incvit._check(incvit.incvit_set_tuning(enc.h, row_groups=row_groups), enc.h)
     B = 2
     caps = [m.n_tokens, 9]
     bufa, ca = enc.new_caches(B)
@@ -62,8 +69,9 @@ def test_step_graph_replays_match_eager_steps():
         enc.drop_graph(g)
 
 
-def test_full_graph_matches_eager():
-    m, w, enc, fr = _setup(B=1)
+@pytest.mark.parametrize("score,mlp_mode", [("embed", "reuse"), ("key", "all")])
+def test_full_graph_matches_eager(score, mlp_mode):
+    m, w, enc, fr = _setup(B=1, score=score, mlp_mode=mlp_mode)
     bufa, ca = enc.new_caches(1)
     bufb, cb = enc.new_caches(1)
     inp = fr[1].clone()
