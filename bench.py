@@ -110,6 +110,15 @@ def kernel_bytes(m, M: float, kind: str):
     return None
 
 
+def gemm_flops(m, M: float, kind: str):
+    """Algorithmic FLOP of one launch of a gathered GEMM over M rows (2 per
+    multiply-add, the output columns the model has; the LayerNorm statistics
+    the matrix cores form beside the products are not counted)."""
+    D, F = m.dim, m.mlp_dim
+    return {"qkv": 2 * M * D * 3 * D, "oproj": 2 * M * D * D, "fc1": 2 * M * D * F,
+            "fc2": 2 * M * F * D}.get(kind)
+
+
 def torch_full_forward(m, w, patches, repeats: int):
     """Context for the full-encode baseline: the same model's full forward over
     every token written with plain torch ops (hipBLASLt GEMMs in the storage
@@ -511,6 +520,37 @@ def summarize_pmc(fetch_dir: str, write_dir: str, copy_fetch_dir: str, copy_writ
     print("\n".join(lines))
 
 
+def summarize_mfma(directory: str, drive_log: str, out: str, command: str) -> None:
+    """Matrix-core use per kernel kind from one rocprofv3 --pmc pass of the
+    derived counters MfmaUtil (MFMA-busy cycles over active cycles x SIMDs, %)
+    and MfmaFlopsBF16 (bf16 MFMA operations x 512), averaged over the last n
+    dispatches of each kind (the incremental steps of the driver's run)."""
+    b = _bench_json(drive_log)
+    vals = {}
+    for name in ("MfmaUtil", "MfmaFlopsBF16"):
+        disp = _pmc_per_dispatch(directory, name)
+        by_kind = {}
+        for (_, n, v), k in zip(disp, kinds_in_order([n for _, n, _ in disp])):
+            if k:
+                by_kind.setdefault(k, []).append(v)
+        for k, n in b["kernel_launches"].items():
+            got = by_kind.get(k, [])[-n:]
+            if got:
+                vals.setdefault(k, {})[name] = statistics.mean(got)
+    lines = [f"# matrix-core use per launch from rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 ({b['config']['workload']})",
+             f"# command: {command}",
+             f"# mean rows/step {b['config']['rows_mean']}; per kind: mean over the last n dispatches (the incremental "
+             "steps); mfma_util_pct = MFMA-busy cycles / (active cycles x SIMDs); mfma_flop = bf16 MFMA operations "
+             "x 512 per launch (includes the LayerNorm statistics products and the padded rows of a 32-row block)",
+             f"source_hash {source_hash()}",
+             f"{'kind':8s} {'mfma_util_pct':>14s} {'mfma_flop':>14s}"]
+    for k, v in vals.items():
+        lines.append(f"{k:8s} {v.get('MfmaUtil', float('nan')):14.3f} {v.get('MfmaFlopsBF16', float('nan')):14.0f}")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def dump_workload(name: str, rho: float, directory: str, frames: int) -> int:
     """Write a workload for the native driver (CPU only): config.txt,
     weights.bin (canonical, storage dtype) and frames.bin ([frames][views][N][P] f32)."""
@@ -555,6 +595,7 @@ def main() -> int:
     ap.add_argument("--dump-workload", metavar="DIR", help="write the workload for the native driver and exit (CPU)")
     ap.add_argument("--summarize-trace", nargs=5, metavar=("TRACE_DIR", "TRACED_BENCH_LOG", "PLAIN_BENCH_LOG", "OUT",
                                                            "COMMAND"))
+    ap.add_argument("--summarize-mfma", nargs=4, metavar=("PMC_DIR", "DRIVE_LOG", "OUT", "COMMAND"))
     ap.add_argument("--summarize-pmc", nargs=8, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
                                                          "COPY_WRITE_DIR", "BENCH_LOG", "COPY_LOG", "OUT", "COMMANDS"))
     ap.add_argument("--steps", type=int, default=500)
@@ -587,6 +628,9 @@ def main() -> int:
         return 0
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
+        return 0
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma)
         return 0
     if args.dump_workload:
         return dump_workload(args.workload, args.rho, args.dump_workload, args.steps + 1)
@@ -747,6 +791,16 @@ def main() -> int:
             "traffic": stored_traffic(wl.name, dom), "avg_launch_us": round(avg_us, 3),
             "bytes_per_launch": nbytes,
         }
+        # the gathered GEMMs against the dense bf16 (fp32 for fp32 models) matrix-core peak
+        peak = 2500.0 if m.dtype == "bf16" else 157.3
+        gm = {}
+        for k in ("qkv", "oproj", "fc1", "fc2"):
+            if k in kinds:
+                us = kinds[k][0] * 1e3 / kinds[k][1]
+                tf = gemm_flops(m, mean_rows, k) / (us * 1e-6) / 1e12
+                gm[k] = {"tflops": round(tf, 2), "frac": round(tf / peak, 4), "us": round(us, 3)}
+        result["gemm_mfma"] = {"peak_tflops": peak, "rows": round(mean_rows, 2), "kernels": gm,
+                               "note": "weight-streaming below ~315 rows: the HBM roofline binds, not MFMA"}
         result["kernel_launches"] = {k: int(v[1]) for k, v in kinds.items()}
         result["kernel_us_per_launch"] = {k: round(v[0] * 1e3 / v[1], 3) for k, v in kinds.items()}
         result["kernel_ms_per_step"] = {k: round(v[0] / args.steps, 5) for k, v in kinds.items()}
