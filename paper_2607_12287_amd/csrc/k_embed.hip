@@ -40,19 +40,30 @@ __device__ __forceinline__ void unpack16(float* f, const V8<float>& v) {
   f[0] = v.a.x; f[1] = v.a.y; f[2] = v.a.z; f[3] = v.a.w;
 }
 
-// Workgroup: 16 tokens x 64 columns; wave w computes tokens 4w..4w+3 of the
-// tile, lane = column.  k is staged through LDS in tiles of 64, double
-// buffered, with one barrier per tile.  A tile's global loads go out two
-// tiles of compute ahead into one of three register slots (the loop body is unrolled over
-// the slots, so no register copy waits on a load in flight); every load is
-// unconditional (clamped addresses; values past P are loaded but never used
-// because the k loop stops at P).
-template <class T, int NT>
+// Workgroup: 4*TM tokens x 64*TN columns; wave w computes tokens
+// TM*w..TM*w+TM-1 of the tile and lane l one column (TN = 1: column l) or two
+// adjacent ones (TN = 2, bf16 weights: columns 2l, 2l+1, kept in LDS as one
+// packed pair), so a k step reads TM + 1 values from LDS for TM*TN fma.  k is
+// staged through LDS in tiles of 64, double buffered, with one barrier per
+// tile.  A tile's global loads go out two tiles of compute ahead into one of
+// three register slots (the loop body is unrolled over the slots, so no
+// register copy waits on a load in flight); every load is unconditional
+// (clamped addresses; values past P are loaded but never used because the k
+// loop stops at P).  The patch tiles sit first in LDS and every buffer stays
+// below 64 KB, so each LDS read is a base register plus an immediate offset.
+template <class T, int NT, int TM, int TN>
 __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
+  static_assert(TN == 1 || (TN == 2 && sizeof(T) == 2), "two columns per lane need bf16 weights");
+  constexpr int TT = 4 * TM, TC = 64 * TN;  // tile tokens, tile columns
   constexpr int WV = 16 / sizeof(T);  // weights per 16-byte load
-  constexpr int WL = 64 * 64 / (256 * WV);  // weight loads per thread per tile
-  __shared__ __align__(16) float sx[2][64][16];  // [buffer][k][token]
-  __shared__ __align__(16) float sw[2][64][64];  // [buffer][k][column]
+  constexpr int WL = 64 * TC / (256 * WV);  // weight loads per thread per tile
+  constexpr int XL = 64 * TT / 256;  // patch loads per thread per tile (= TM)
+  constexpr int XB = 64 * TT;  // floats per patch buffer
+  constexpr int WB = 64 * 64;  // 32-bit words per weight buffer (one per lane and k)
+  __shared__ __align__(16) float smem[2 * XB + 2 * WB];
+  float* const sx = smem;                                            // [buffer][k][token]
+  float* const swf = smem + 2 * XB;                                  // TN = 1: [buffer][k][column]
+  uint32_t* const swp = reinterpret_cast<uint32_t*>(smem + 2 * XB);  // TN = 2: [buffer][k][lane] pairs
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   // Workgroups are dealt to the 8 XCDs round robin by linear launch index, and
   // each XCD has its own L2.  Renumber them XCD-major (a bijection) and take
@@ -65,7 +76,7 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
   const int x = i % 8, q = total / 8, rem = total % 8;
   const int pos = x * q + min(x, rem) + i / 8;
   const int v = pos / (ncb * ntg), cb = (pos / ntg) % ncb, tg = pos % ntg;
-  const int tok0 = tg * 16, c0 = cb * 64;
+  const int tok0 = tg * TT, c0 = cb * TC;
   const int N = a.N, P = a.P, D = a.D;
 
   if (tg == 0 && cb == 0) {
@@ -76,72 +87,98 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
     }
   }
 
-  const int d = c0 + lane;
   // Operands through buffer loads: every lane offset below is fixed for the
   // whole kernel and the tile's k position is a wave-uniform offset, so a
   // fetch needs no address registers.  Reads past the buffer return zero; reads
   // past a row's end (k >= P) are never used because the k loop stops at P.
   const Rsrc rx = make_rsrc(a.patches + (size_t)v * N * P, (uint32_t)((size_t)N * P * 4));
   const Rsrc rw = make_rsrc(a.w_pe, (uint32_t)((size_t)P * D * sizeof(T)));
-  uint32_t xoff[4], woff[WL > 0 ? WL : 1];
+  uint32_t xoff[XL], woff[WL];
+  // patch element e of a tile: token e / 64, k e % 64 (a wave reads 64
+  // consecutive k of one token's row)
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < XL; ++j) {
     const int e = tid + 256 * j;
-    xoff[j] = (uint32_t)((min(tok0 + (e & 15), N - 1) * P + (e >> 4)) * 4);
+    xoff[j] = (uint32_t)((min(tok0 + (e >> 6), N - 1) * P + (e & 63)) * 4);
   }
+  // weight run e of a tile: row k = e / (TC / WV), WV columns from (e % (TC / WV)) * WV
 #pragma unroll
   for (int j = 0; j < WL; ++j) {
     const int e = tid + 256 * j;
-    woff[j] = (uint32_t)(((e / (64 / WV)) * D + min(c0 + (e % (64 / WV)) * WV, D - WV)) * sizeof(T));
+    woff[j] = (uint32_t)(((e / (TC / WV)) * D + min(c0 + (e % (TC / WV)) * WV, D - WV)) * sizeof(T));
   }
-  // this thread's share of a tile: 4 patch values (token e%16, k e/16) and WL
-  // 16-byte runs of weights (row k, WV consecutive columns)
   struct Tile {
-    float x[4];
-    V8<T> wv[WL > 0 ? WL : 1];
+    float x[XL];
+    V8<T> wv[WL];
   };
   auto fetch = [&](Tile& t, int kt) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < XL; ++j)
       t.x[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rx, xoff[j], (uint32_t)kt * 4, 0));
 #pragma unroll
     for (int j = 0; j < WL; ++j) bload16(t.wv[j], rw, woff[j], (uint32_t)(kt * D * sizeof(T)));
   };
   auto stage = [&](const Tile& t, int b) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < XL; ++j) {
       const int e = tid + 256 * j;
-      sx[b][e >> 4][e & 15] = t.x[j];
+      sx[b * XB + (e & 63) * TT + (e >> 6)] = t.x[j];
     }
 #pragma unroll
     for (int j = 0; j < WL; ++j) {
       const int e = tid + 256 * j;
-      float f[WV];
-      unpack16(f, t.wv[j]);
+      const int k = e / (TC / WV), c = (e % (TC / WV)) * WV;
+      if constexpr (TN == 2) {
+        // 8 bf16 columns = 4 packed pairs, stored as they came
+        *reinterpret_cast<uint4*>(&swp[b * WB + k * 64 + c / 2]) = __builtin_bit_cast(uint4, t.wv[j]);
+      } else {
+        float f[WV];
+        unpack16(f, t.wv[j]);
 #pragma unroll
-      for (int q = 0; q < WV; ++q) sw[b][e / (64 / WV)][(e % (64 / WV)) * WV + q] = f[q];
+        for (int q = 0; q < WV; ++q) swf[b * WB + k * 64 + c + q] = f[q];
+      }
     }
   };
 
-  float acc[4];
-  const float bias = a.b_pe[min(d, D - 1)];
-  float posv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  // the lane's columns: TN = 1: c0 + lane; TN = 2: c0 + 2 lane and the next
+  const int dl = c0 + (TN == 2 ? 2 * lane : lane);
+  float acc[TM][TN], posv[TM][TN];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    acc[r] = bias;
-    const int tok = min(tok0 + 4 * w + r, N - 1);
-    if (a.pos) posv[r] = a.pos[(size_t)tok * D + min(d, D - 1)];
+  for (int n = 0; n < TN; ++n) {
+    const int d = min(dl + n, D - 1);
+    const float bias = a.b_pe[d];
+#pragma unroll
+    for (int r = 0; r < TM; ++r) {
+      acc[r][n] = bias;
+      const int tok = min(tok0 + TM * w + r, N - 1);
+      posv[r][n] = a.pos ? a.pos[(size_t)tok * D + d] : 0.0f;
+    }
   }
+  // one k step: TM patch values (the same for the whole wave) and TN weights
+  auto kstep = [&](int b, int kk) {
+    float wv[TN], xv[TM];
+    if constexpr (TN == 2) {
+      const uint32_t pr = swp[b * WB + kk * 64 + lane];
+      wv[0] = __uint_as_float(pr << 16);
+      wv[1] = __uint_as_float(pr & 0xffff0000u);
+    } else {
+      wv[0] = swf[b * WB + kk * 64 + lane];
+    }
+    if constexpr (TM == 4) {
+      const float4 x4 = *reinterpret_cast<const float4*>(&sx[b * XB + kk * TT + 4 * w]);
+      xv[0] = x4.x; xv[1] = x4.y; xv[2] = x4.z; xv[3] = x4.w;
+    } else {
+#pragma unroll
+      for (int r = 0; r < TM; ++r) xv[r] = sx[b * XB + kk * TT + TM * w + r];
+    }
+#pragma unroll
+    for (int r = 0; r < TM; ++r)
+#pragma unroll
+      for (int n = 0; n < TN; ++n) acc[r][n] = __fmaf_rn(xv[r], wv[n], acc[r][n]);
+  };
   auto compute = [&](int b, int kmax) {
 #pragma unroll 8
-    for (int kk = 0; kk < kmax; ++kk) {
-      const float wv = sw[b][kk][lane];
-      const float4 xv = *reinterpret_cast<const float4*>(&sx[b][kk][4 * w]);
-      acc[0] = __fmaf_rn(xv.x, wv, acc[0]);
-      acc[1] = __fmaf_rn(xv.y, wv, acc[1]);
-      acc[2] = __fmaf_rn(xv.z, wv, acc[2]);
-      acc[3] = __fmaf_rn(xv.w, wv, acc[3]);
-    }
+    for (int kk = 0; kk < kmax; ++kk) kstep(b, kk);
   };
   Tile tl[3];
   fetch(tl[0], 0);
@@ -156,14 +193,7 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
     for (int it = 0; it < NT; ++it) {
       if (it + 1 < NT) {
 #pragma unroll
-        for (int kk = 0; kk < 64; ++kk) {  // a full tile
-          const float wv = sw[it & 1][kk][lane];
-          const float4 xv = *reinterpret_cast<const float4*>(&sx[it & 1][kk][4 * w]);
-          acc[0] = __fmaf_rn(xv.x, wv, acc[0]);
-          acc[1] = __fmaf_rn(xv.y, wv, acc[1]);
-          acc[2] = __fmaf_rn(xv.z, wv, acc[2]);
-          acc[3] = __fmaf_rn(xv.w, wv, acc[3]);
-        }
+        for (int kk = 0; kk < 64; ++kk) kstep(it & 1, kk);  // a full tile
         stage(tl[(it + 1) % 3], (it + 1) & 1);
         if (it + 3 < NT) fetch(tl[it % 3], 64 * (it + 3));
         __syncthreads();
@@ -190,25 +220,29 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
       }
     }
   }
-  if (d < D) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int tok = tok0 + 4 * w + r;
-      if (tok < N) a.t0[((size_t)v * N + tok) * D + d] = a.pos ? __fadd_rn(acc[r], posv[r]) : acc[r];
+  for (int n = 0; n < TN; ++n) {
+    const int d = dl + n;
+    if (d < D) {
+#pragma unroll
+      for (int r = 0; r < TM; ++r) {
+        const int tok = tok0 + TM * w + r;
+        if (tok < N) a.t0[((size_t)v * N + tok) * D + d] = a.pos ? __fadd_rn(acc[r][n], posv[r][n]) : acc[r][n];
+      }
     }
   }
 }
 
-template <class T, int NT>
+template <class T, int NT, int TM, int TN>
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
-  embed_body<T, NT>(a);
+  embed_body<T, NT, TM, TN>(a);
 }
 
 // The key projection of the key score: the same fixed-order product with
 // x = LayerNorm rows, K = D, W = W_K of layer 0, no position term.
-template <class T, int NT>
+template <class T, int NT, int TM, int TN>
 __global__ __launch_bounds__(256) void keyproj_kernel(EmbedArgs a) {
-  embed_body<T, NT>(a);
+  embed_body<T, NT, TM, TN>(a);
 }
 
 // Correctly rounded fp32 square root.  HIP's __fsqrt_rn is the bare hardware
@@ -308,34 +342,78 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
 
 // Tile counts of the shapes in use are compiled unrolled (patch 14 and 16 with
 // 3 channels: P = 588, 768; D = 192, 1024, 1152); other lengths run the loop.
-template <class T, template <class, int> class Launch>
+template <class T, int TM, int TN, template <class, int, int, int> class Launch>
 hipError_t launch_nt(const EmbedArgs& a, dim3 grid, hipStream_t s) {
   switch ((a.P + 63) / 64) {
-    case 3: return Launch<T, 3>::go(a, grid, s);
-    case 10: return Launch<T, 10>::go(a, grid, s);
-    case 12: return Launch<T, 12>::go(a, grid, s);
-    case 16: return Launch<T, 16>::go(a, grid, s);
-    case 18: return Launch<T, 18>::go(a, grid, s);
-    default: return Launch<T, 0>::go(a, grid, s);
+    case 3: return Launch<T, 3, TM, TN>::go(a, grid, s);
+    case 10: return Launch<T, 10, TM, TN>::go(a, grid, s);
+    case 12: return Launch<T, 12, TM, TN>::go(a, grid, s);
+    case 16: return Launch<T, 16, TM, TN>::go(a, grid, s);
+    case 18: return Launch<T, 18, TM, TN>::go(a, grid, s);
+    default: return Launch<T, 0, TM, TN>::go(a, grid, s);
   }
 }
-template <class T, int NT>
+template <class T, int NT, int TM, int TN>
 struct EmbedLaunch {
-  static hipError_t go(const EmbedArgs& a, dim3 g, hipStream_t s) { return launch_k(embed_kernel<T, NT>, g, dim3(256), 0, s, a); }
+  static hipError_t go(const EmbedArgs& a, dim3 g, hipStream_t s) {
+    return launch_k(embed_kernel<T, NT, TM, TN>, g, dim3(256), 0, s, a);
+  }
 };
-template <class T, int NT>
+template <class T, int NT, int TM, int TN>
 struct KeyLaunch {
-  static hipError_t go(const EmbedArgs& a, dim3 g, hipStream_t s) { return launch_k(keyproj_kernel<T, NT>, g, dim3(256), 0, s, a); }
+  static hipError_t go(const EmbedArgs& a, dim3 g, hipStream_t s) {
+    return launch_k(keyproj_kernel<T, NT, TM, TN>, g, dim3(256), 0, s, a);
+  }
 };
 
+// Register tile of the fixed-order product, TM tokens x TN columns per lane,
+// chosen per shape.  Per k step a CU's LDS returns 4 waves x 64 lanes x
+// (TM + 1) words at 128 bytes per clock, 8 (TM + 1) clocks, while each SIMD
+// spends 4 clocks per wave64 instruction on TM TN fma (and two more to unpack a
+// bf16 pair); the workgroups run in ceil(count / 256) rounds of one per CU.
+// The tile with the fewest estimated clocks wins (the first listed on a tie).
+struct Tiling {
+  int tm, tn;
+};
+constexpr Tiling kTilings[] = {{4, 1}, {3, 2}, {4, 2}};
+
+// fp32 weights take one column per lane only
+inline int pick_tiling(const EmbedArgs& a) {
+  int best = 0;
+  long best_cost = -1;
+  for (int t = 0; t < (a.dtype ? (int)(sizeof(kTilings) / sizeof(kTilings[0])) : 1); ++t) {
+    const int tm = kTilings[t].tm, tn = kTilings[t].tn;
+    const long wgs = (long)((a.N + 4 * tm - 1) / (4 * tm)) * ((a.D + 64 * tn - 1) / (64 * tn)) * a.B;
+    const long step = std::max(8 * (tm + 1), 4 * (tm * tn + (tn == 2 ? 2 : 0)));
+    const long cost = (wgs + 255) / 256 * step;
+    if (best_cost < 0 || cost < best_cost) {
+      best = t;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+template <class T, template <class, int, int, int> class Launch>
+hipError_t launch_tiled(const EmbedArgs& a, hipStream_t s) {
+  const int t = pick_tiling(a);
+  const int tm = kTilings[t].tm, tn = kTilings[t].tn;
+  const dim3 grid((a.N + 4 * tm - 1) / (4 * tm), (a.D + 64 * tn - 1) / (64 * tn), a.B);
+  // two columns per lane run the tile loop: unrolled over 16 or more tiles
+  // the compiler's hoisting exceeds the register file and spills
+  if constexpr (sizeof(T) == 2) {
+    if (t == 1) return Launch<T, 0, 3, 2>::go(a, grid, s);
+    if (t == 2) return Launch<T, 0, 4, 2>::go(a, grid, s);
+  }
+  return launch_nt<T, 4, 1, Launch>(a, grid, s);
+}
+
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
-  dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
-  return a.dtype ? launch_nt<uint16_t, EmbedLaunch>(a, grid, s) : launch_nt<float, EmbedLaunch>(a, grid, s);
+  return a.dtype ? launch_tiled<uint16_t, EmbedLaunch>(a, s) : launch_tiled<float, EmbedLaunch>(a, s);
 }
 
 hipError_t launch_keyproj(const EmbedArgs& a, hipStream_t s) {
-  dim3 grid((a.N + 15) / 16, (a.D + 63) / 64, a.B);
-  return a.dtype ? launch_nt<uint16_t, KeyLaunch>(a, grid, s) : launch_nt<float, KeyLaunch>(a, grid, s);
+  return a.dtype ? launch_tiled<uint16_t, KeyLaunch>(a, s) : launch_tiled<float, KeyLaunch>(a, s);
 }
 
 hipError_t launch_keyln(const KeyLnArgs& a, hipStream_t s) {
