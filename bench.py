@@ -32,7 +32,7 @@ HBM_PEAK_GBS = 8000.0
 ALU_PEAK_TFLOPS = 78.6
 ROOT = os.path.dirname(os.path.abspath(__file__))
 PROFILES = os.path.join(ROOT, "profiles")
-GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj", "4": "oproj"}  # epilogue template argument
+GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj", "4": "oproj", "5": "fc2"}  # epilogue template argument
 
 
 def source_hash() -> str:

@@ -1,0 +1,72 @@
+"""Host-side logic of bench.py (no GPU): trace-name parsing, the stored-counter
+gate, the algorithmic byte and FLOP counts against hand-counted So400m figures,
+and the refusal of more than one GPU."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from paper_2607_12287_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("name,kind", [
+    ("void incvit::gemm_kernel<unsigned short, 0, 1, 5>(incvit::GemmArgs)", "qkv"),
+    ("void incvit::gemm_kernel<unsigned short, 1, 2, 5>(incvit::GemmArgs)", "fc1"),
+    ("void incvit::gemm_kernel<unsigned short, 2, 1, 6>(incvit::GemmArgs)", "fc2"),
+    ("void incvit::gemm_kernel<unsigned short, 3, 1, 5>(incvit::GemmArgs)", "oproj"),
+    ("void incvit::gemm_kernel<unsigned short, 4, 1, 5>(incvit::GemmArgs)", "oproj"),
+    ("void incvit::gemm_kernel<unsigned short, 5, 2, 8>(incvit::GemmArgs)", "fc2"),
+    ("void incvit::gemm_kernel<float, 0, 1, 2>(incvit::GemmArgs)", "qkv"),
+    ("void incvit::res_kernel<unsigned short, 3, 2>(incvit::ResArgs)", "res_ln1"),
+    ("void incvit::embed_kernel<unsigned short, 0, 3, 2>(incvit::EmbedArgs)", "embed"),
+    ("void incvit::keyproj_kernel<unsigned short, 0, 3, 2>(incvit::EmbedArgs)", "key_proj"),
+    ("void incvit::keyln_kernel<unsigned short>(incvit::KeyLnArgs)", "key_ln"),
+    ("incvit::sim_kernel(incvit::SimArgs)", "sim"),
+    ("incvit::select_kernel(incvit::SelectArgs)", "select"),
+    ("void incvit::attn_kernel<unsigned short, 3, 6, 2, 1, 4>(incvit::AttnArgs)", "attn"),
+    ("__amd_rocclr_copyBuffer", None),
+    ("void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<unsigned char>>", None),
+])
+def test_kernel_kind(name, kind):
+    assert bench.kernel_kind(name) == kind
+
+
+def test_so400m_bytes_and_flops():
+    # hand-counted for So400m (D 1152, F 4304, bf16) at 23 refreshed rows
+    m = synth.workload("so400m").model
+    assert (m.dim, m.mlp_dim, m.dtype) == (1152, 4304, "bf16")
+    assert bench.ksplit(m) == 3  # 72 column blocks: 256 // 72 = 3 splits of the 135 K chunks
+    M = 23
+    weights = {"qkv": 1152 * 3456 * 2, "oproj": 1152 * 1152 * 2, "fc1": 1152 * 4304 * 2, "fc2": 4304 * 1152 * 2}
+    rows_in = {"qkv": M * 1152 * 2, "oproj": M * 1152 * 2, "fc1": M * 1152 * 2, "fc2": M * 4304 * 2}
+    rows_out = {"qkv": M * 3456 * 2, "oproj": 2 * M * 1152 * 2, "fc1": M * 4304 * 2, "fc2": 3 * M * 1152 * 4}
+    for kind in weights:
+        assert bench.kernel_bytes(m, M, kind) == weights[kind] + rows_in[kind] + rows_out[kind], kind
+        assert bench.gemm_flops(m, M, kind) == 2 * M * weights[kind] // 2, kind
+    # the whole step's weights: 27 layers of 30.45 MB
+    per_layer = sum(weights.values())
+    assert abs(27 * per_layer / 1e6 - 822) < 1
+    assert bench.kernel_bytes(m, M, "embed") is None
+
+
+def test_stored_traffic_gate(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    f = tmp_path / "step_hbm_traffic_so400m.txt"
+    assert bench.stored_traffic("so400m", "fc1") is None  # no file
+    f.write_text(f"source_hash {bench.source_hash()}\ntraffic_bytes_per_launch fc1 10900000\n")
+    assert bench.stored_traffic("so400m", "fc1") == 10900000.0
+    assert bench.stored_traffic("so400m", "qkv") is None
+    f.write_text("source_hash 0000000000000000\ntraffic_bytes_per_launch fc1 10900000\n")
+    assert bench.stored_traffic("so400m", "fc1") is None  # kernels changed since
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
