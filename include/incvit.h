@@ -85,8 +85,12 @@ typedef enum { INCVIT_SCORE_EMBED = 0, INCVIT_SCORE_KEY = 1 } incvit_score;
  * patch features, D = dim, L = depth, h = heads, d_h = D/h, F = mlp_dim.
  * Supported: img_h, img_w multiples of patch; D % 32 == 0; D % h == 0;
  * d_h % 8 == 0 and d_h <= 128; N <= 4096; D <= 2048; F >= 1;
- * 1 <= max_streams <= 64.  dtype is the storage type of weights, caches and
- * activations (GEMMs accumulate in fp32; LayerNorm, softmax, GELU in fp32). */
+ * 1 <= max_streams <= 64; and every buffer one kernel addresses below 4 GiB:
+ * N*P*4 bytes (one stream's patches), P*D*e (W_pe), max(3D, F)*max(D, F)*e (a
+ * packed GEMM matrix) and max_streams*N*max(D, F)*e (the widest compact GEMM
+ * operand), e = 2 (bf16) or 4 (f32); otherwise INCVIT_ERR_UNSUPPORTED.
+ * dtype is the storage type of weights, caches and activations (GEMMs
+ * accumulate in fp32; LayerNorm, softmax, GELU in fp32). */
 typedef struct {
   int32_t img_h, img_w, channels, patch;
   int32_t dim, depth, heads, mlp_dim;
@@ -156,8 +160,9 @@ size_t incvit_workspace_bytes(const incvit_handle* h, int32_t B);
 
 /* Full forward of B frames (the paper's full pass on odd chunks, §III-B):
  * patches [B][N][P] fp32 (frame pixels, token-major, features (c, dy, dx));
- * caches: host array of B device pointers, one cache per stream; every cache
- * row is (re)written and the cache header is initialised for this model.
+ * caches: host array of B device pointers, one cache per stream (B distinct
+ * buffers that do not overlap, else INCVIT_ERR_ARG); every cache row is
+ * (re)written and the cache header is initialised for this model.
  * workspace: incvit_workspace_bytes(h, B) bytes, device. */
 incvit_status incvit_full_encode(incvit_handle* h, int32_t B, const float* patches,
                                  void* const* caches, void* workspace, void* stream);

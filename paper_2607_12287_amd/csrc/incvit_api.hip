@@ -1,6 +1,7 @@
 // C ABI of the incremental ViT encoder: validation, buffer layouts and the
 // launch sequence of one encode call.  The host only enqueues; it never waits
 // for the device inside incvit_full_encode / incvit_step.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -83,6 +84,21 @@ bool make_shape(const incvit_config* c, Shape& sh, incvit_status& st, std::strin
   if (sh.dh % 8 || sh.dh > kMaxHeadDim) { err = "head dim must be a multiple of 8 and <= 128"; return false; }
   if (sh.N > kMaxTokens) { snprintf(buf, sizeof buf, "at most %d tokens", kMaxTokens); err = buf; return false; }
   if (c->max_streams < 1 || c->max_streams > kMaxViews) { snprintf(buf, sizeof buf, "max_streams must be in [1, %d]", kMaxViews); err = buf; return false; }
+  // Kernels address each buffer through 32-bit offsets (buffer resources and
+  // 32-bit index products), so the largest buffer one launch can touch must
+  // stay below 4 GiB: a stream's patches, W_pe, a packed GEMM matrix, and the
+  // compact GEMM operands of the largest call (every token of max_streams
+  // streams, the MLP hidden rows being the widest).
+  {
+    const size_t lim = 0xffffffffu;
+    const size_t mpad = (size_t)round_up(c->max_streams * sh.N, kGemmRows);
+    const size_t kmax = (size_t)std::max(sh.D, sh.Fpad);
+    const size_t wide = (size_t)round_up(std::max(3 * sh.D, sh.Fpad), 32);
+    const size_t sizes[] = {(size_t)sh.N * sh.P * 4, (size_t)sh.P * sh.D * sh.eb, mpad * kmax * sh.eb,
+                            wide * kmax * sh.eb};
+    for (size_t b : sizes)
+      if (b > lim) { err = "a buffer that one kernel addresses would exceed 4 GiB (fewer streams, tokens, channels or a smaller MLP)"; return false; }
+  }
   st = INCVIT_OK;
   return true;
 }
@@ -511,6 +527,12 @@ incvit_status check_views(incvit_handle* h, int32_t B, void* const* caches, View
     if (reinterpret_cast<uintptr_t>(caches[v]) % kAlign) return fail(h, INCVIT_ERR_ARG, "cache pointers must be 256-byte aligned");
     views.p[v] = static_cast<char*>(caches[v]);
   }
+  // each stream's step writes its whole cache: two streams sharing bytes would race
+  std::vector<uintptr_t> base(B);
+  for (int v = 0; v < B; ++v) base[v] = reinterpret_cast<uintptr_t>(caches[v]);
+  std::sort(base.begin(), base.end());
+  for (int v = 1; v < B; ++v)
+    if (base[v] - base[v - 1] < h->cl.total) return fail(h, INCVIT_ERR_ARG, "caches of one call must not overlap");
   return INCVIT_OK;
 }
 

@@ -1,6 +1,5 @@
 """The C-ABI library loads and exports every symbol include/incvit.h declares;
 host-only queries (no GPU) validate configs and report sizes."""
-import ctypes
 import os
 import re
 
@@ -49,6 +48,41 @@ def test_invalid_configs_are_rejected_before_any_device_work(field, value, statu
     assert incvit.incvit_last_error(None) != ""
     # packing with an invalid config fails synchronously with the right code
     assert incvit.incvit_pack_weights(cfg, 256, 256, 0) == status
+
+
+@pytest.mark.parametrize("fields", [
+    # 64 streams of 4096 tokens with a 16384-wide fp32 MLP: the hidden rows alone are 16 GiB
+    dict(img_h=256, img_w=256, patch=4, dim=2048, heads=16, mlp_dim=16384, dtype=0, max_streams=64),
+    # 1000 channels of 64x64 patches: one stream's patches are 64 MiB but W_pe is 32 GiB
+    dict(img_h=256, img_w=256, channels=1000, patch=64, dim=2048, heads=16, mlp_dim=64, dtype=0, max_streams=1),
+])
+def test_buffers_beyond_32_bit_offsets_are_rejected(fields):
+    cfg = incvit.make_config(synth.small_model(dtype="bf16"), 2)
+    for k, v in fields.items():
+        setattr(cfg, k, v)
+    assert incvit.incvit_canonical_weights_bytes(cfg) == 0
+    assert "4 GiB" in incvit.incvit_last_error(None)
+    assert incvit.incvit_pack_weights(cfg, 256, 256, 0) == incvit.INCVIT_ERR_UNSUPPORTED
+    # the same shapes with one stream and a narrow MLP are accepted
+    if fields.get("channels", 3) == 3:
+        cfg.max_streams, cfg.mlp_dim = 1, 512
+        assert incvit.incvit_canonical_weights_bytes(cfg) > 0
+
+
+def test_overlapping_caches_are_rejected_before_any_device_work():
+    # a handle needs no device memory of its own; every pointer below is only
+    # checked on the host (the call fails before anything is enqueued)
+    cfg = incvit.make_config(synth.small_model(dtype="bf16"), 4)
+    st, h = incvit.incvit_create(cfg, 1 << 20)
+    assert st == incvit.INCVIT_OK
+    try:
+        cb = incvit.incvit_cache_bytes(h)
+        base, ws, patches = 1 << 32, 1 << 30, 1 << 31
+        for ptrs in ([base, base], [base, base + cb - 256], [base + cb // 512 * 256, base]):
+            assert incvit.incvit_full_encode(h, len(ptrs), patches, ptrs, ws) == incvit.INCVIT_ERR_ARG
+            assert "overlap" in incvit.incvit_last_error(h)
+    finally:
+        incvit.lib().incvit_destroy(h)
 
 
 def test_null_arguments_are_rejected():
