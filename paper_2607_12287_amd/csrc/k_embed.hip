@@ -155,28 +155,60 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
     }
   }
   // one k step: TM patch values (the same for the whole wave) and TN weights
-  auto kstep = [&](int b, int kk) {
-    float wv[TN], xv[TM];
-    if constexpr (TN == 2) {
-      const uint32_t pr = swp[b * WB + kk * 64 + lane];
-      wv[0] = __uint_as_float(pr << 16);
-      wv[1] = __uint_as_float(pr & 0xffff0000u);
-    } else {
-      wv[0] = swf[b * WB + kk * 64 + lane];
-    }
+  // (TN = 2: one packed bf16 pair), read from LDS, then the TM * TN fma
+  struct Ops {
+    float x[TM];
+    uint32_t w;
+  };
+  auto read_ops = [&](Ops& o, int b, int kk) {
+    if constexpr (TN == 2) o.w = swp[b * WB + kk * 64 + lane];
+    else o.w = __float_as_uint(swf[b * WB + kk * 64 + lane]);
     if constexpr (TM == 4) {
       const float4 x4 = *reinterpret_cast<const float4*>(&sx[b * XB + kk * TT + 4 * w]);
-      xv[0] = x4.x; xv[1] = x4.y; xv[2] = x4.z; xv[3] = x4.w;
+      o.x[0] = x4.x; o.x[1] = x4.y; o.x[2] = x4.z; o.x[3] = x4.w;
     } else {
 #pragma unroll
-      for (int r = 0; r < TM; ++r) xv[r] = sx[b * XB + kk * TT + TM * w + r];
+      for (int r = 0; r < TM; ++r) o.x[r] = sx[b * XB + kk * TT + TM * w + r];
+    }
+  };
+  auto fma_ops = [&](const Ops& o) {
+    float wv[TN];
+    if constexpr (TN == 2) {
+      wv[0] = __uint_as_float(o.w << 16);
+      wv[1] = __uint_as_float(o.w & 0xffff0000u);
+    } else {
+      wv[0] = __uint_as_float(o.w);
     }
 #pragma unroll
     for (int r = 0; r < TM; ++r)
 #pragma unroll
-      for (int n = 0; n < TN; ++n) acc[r][n] = __fmaf_rn(xv[r], wv[n], acc[r][n]);
+      for (int n = 0; n < TN; ++n) acc[r][n] = __fmaf_rn(o.x[r], wv[n], acc[r][n]);
+  };
+  auto kstep = [&](int b, int kk) {
+    Ops o;
+    read_ops(o, b, kk);
+    fma_ops(o);
+  };
+  // A full tile of 64 k steps with each step's LDS reads issued PD steps
+  // ahead of its fma: with one wave per SIMD nothing else hides the LDS
+  // latency (the fma order is unchanged).
+  constexpr int PD = 4;
+  auto full_tile = [&](int b) {
+    Ops o[PD];
+#pragma unroll
+    for (int p = 0; p < PD; ++p) read_ops(o[p], b, p);
+#pragma unroll
+    for (int kk = 0; kk < 64; ++kk) {
+      const Ops cur = o[kk % PD];
+      if (kk + PD < 64) read_ops(o[kk % PD], b, kk + PD);
+      fma_ops(cur);
+    }
   };
   auto compute = [&](int b, int kmax) {
+    if (kmax == 64) {  // uniform
+      full_tile(b);
+      return;
+    }
 #pragma unroll 8
     for (int kk = 0; kk < kmax; ++kk) kstep(b, kk);
   };
@@ -192,8 +224,7 @@ __device__ __forceinline__ void embed_body(const EmbedArgs& a) {
 #pragma unroll
     for (int it = 0; it < NT; ++it) {
       if (it + 1 < NT) {
-#pragma unroll
-        for (int kk = 0; kk < 64; ++kk) kstep(it & 1, kk);  // a full tile
+        full_tile(it & 1);
         stage(tl[(it + 1) % 3], (it + 1) & 1);
         if (it + 3 < NT) fetch(tl[it % 3], 64 * (it + 3));
         __syncthreads();
@@ -399,11 +430,21 @@ hipError_t launch_tiled(const EmbedArgs& a, hipStream_t s) {
   const int t = pick_tiling(a);
   const int tm = kTilings[t].tm, tn = kTilings[t].tn;
   const dim3 grid((a.N + 4 * tm - 1) / (4 * tm), (a.D + 64 * tn - 1) / (64 * tn), a.B);
-  // two columns per lane run the tile loop: unrolled over 16 or more tiles
-  // the compiler's hoisting exceeds the register file and spills
+  // two columns per lane: the patch lengths in use (10 and 12 tiles) run
+  // unrolled, longer rows the tile loop (unrolled over 16 or more tiles the
+  // compiler's hoisting exceeds the register file and spills)
   if constexpr (sizeof(T) == 2) {
-    if (t == 1) return Launch<T, 0, 3, 2>::go(a, grid, s);
-    if (t == 2) return Launch<T, 0, 4, 2>::go(a, grid, s);
+    const int nt = (a.P + 63) / 64;
+    if (t == 1) {
+      if (nt == 10) return Launch<T, 10, 3, 2>::go(a, grid, s);
+      if (nt == 12) return Launch<T, 12, 3, 2>::go(a, grid, s);
+      return Launch<T, 0, 3, 2>::go(a, grid, s);
+    }
+    if (t == 2) {
+      if (nt == 10) return Launch<T, 10, 4, 2>::go(a, grid, s);
+      if (nt == 12) return Launch<T, 12, 4, 2>::go(a, grid, s);
+      return Launch<T, 0, 4, 2>::go(a, grid, s);
+    }
   }
   return launch_nt<T, 4, 1, Launch>(a, grid, s);
 }
