@@ -147,3 +147,35 @@ def test_down_projection_fused_so400m():
         tf = p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
         worst = p.check_caches(f"step {t}")
         say(f"  step {t}: count={count.tolist()} per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
+
+
+@pytest.mark.parametrize("case", ["3x2", "4x2"])
+@pytest.mark.parametrize("score", ["embed", "key"])
+def test_patch16_register_tiles(case, score):
+    """Patch 16 (P = 768, 12 LDS tiles of k) through each register tile of the
+    fixed-order product that has an unrolled 12-tile form: one stream of 64
+    tokens takes 3 tokens x 2 columns per thread, 8 streams of 256 tokens at
+    D = 768 take 4 x 2 (fewer workgroup rounds); with the key score at
+    D = 768 the key projection (K = 768, 12 tiles) takes the same tile, at
+    D = 128 the tile loop.  Selection is checked bit-exactly, so the product
+    must keep its fma order."""
+    if case == "3x2":
+        m = synth.small_model(dim=128, depth=1, heads=2, mlp=160, img=128, patch=16, dtype="bf16")
+        B, views = 2, None
+    else:
+        m = synth.small_model(dim=768, depth=1, heads=8, mlp=256, img=256, patch=16, dtype="bf16")
+        B, views = 8, [0, 7]
+    assert m.patch_dim == 768
+    w = synth.make_weights(m, 1501)
+    say(f"[patch 16 {case} {score}] N={m.n_tokens} D={m.dim} B={B}")
+    its = [synth.RefillRectStream(m, 1510 + v, v, 37, 45).frames(3) for v in range(B)]
+    frames = [np.stack([synth.patchify(next(it), m.patch) for it in its]) for _ in range(3)]
+    p = Pair(m, w, B, oracle_views=views, score=score)
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    for t, (tau, cap) in enumerate([(0.98, m.n_tokens), (np.inf, 9)], start=1):
+        idx, count, refreshed, res = p.step(frames[t], tau, [cap] * B)
+        say(f"  step {t}: count={count.tolist()}")
+        assert count.sum() > 0 if t == 1 else (count == 9).all()
+        p.check_step(idx, count, refreshed, res, f"step {t}")
+        p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
