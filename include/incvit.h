@@ -265,12 +265,15 @@ void incvit_graph_destroy(incvit_graph* g);
 /* Performance knobs; every setting gives a deterministic result, and the
  * settings differ only in the order of fp32 partial sums.
  * cols[k]: 16-column blocks per workgroup of GEMM k (0 = QKV, 1 = output
- * projection, 2 = MLP up, 3 = MLP down): 1 or 2 (2 only takes effect when the
- * block count is even); 0 = automatic: when the call's row count is not known
- * on the host (threshold steps) one block, two for outputs of more than 256
- * blocks; when it is known (full encodes, top-k steps) two for the output
- * projection and the MLP down projection, and for the MLP up projection from
- * 1536 rows.
+ * projection, 2 = MLP up, 3 = MLP down): 1, 2 or 4 (a count takes effect only
+ * when it divides the output's block count; 4 only for bf16 models, fp32 ones
+ * take 2); 0 = automatic: with one row group (threshold steps without
+ * row_groups) one block, two for outputs of more than 256 blocks; with
+ * several (full encodes, pure top-k steps, or row_groups > 1) four for QKV and
+ * for the MLP down projection when it runs unsplit (fc2_mode), unless the call
+ * has more than 1024 rows known on the host, two for the
+ * output projection and the K-split down projection, and for the MLP up
+ * projection from 1536 rows.
  * attn_qtiles: 16-query tiles per attention workgroup: 1 or 2; 0 = automatic.
  * attn_waves: waves per attention workgroup, splitting the stream's keys: 2, 4
  * or 8; 0 = automatic (about two 32-key blocks per wave).

@@ -308,13 +308,19 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
 
 template <class T, int EPI, int NB, int CPW>
 hipError_t launch_gemm_cfg(const GemmArgs& a, hipStream_t s) {
+  constexpr int lds = gemm_lds_bytes<EPI, NB>();
+  if constexpr (lds > 65536) {  // four column blocks: the partial tiles exceed the default 64 KB
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<T, EPI, NB, CPW>),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (attr != hipSuccess) return attr;
+  }
   return launch_k(gemm_kernel<T, EPI, NB, CPW>, dim3(a.Nout / 16 / NB, a.ksplit, a.rgroups),
-                  dim3(gemm_waves<EPI>() * 64), (size_t)gemm_lds_bytes<EPI, NB>(), s, a);
+                  dim3(gemm_waves<EPI>() * 64), (size_t)lds, s, a);
 }
 
 // Chunks per wave: the smallest instantiated count that covers this
 // workgroup's share of K in one round (the last wave may own fewer); longer
-// shares run in rounds of the largest.
+// shares run in rounds of the largest (8, or 6 for four column blocks).
 template <class T, int EPI, int NB>
 hipError_t launch_gemm_nb(int cpw, const GemmArgs& a, hipStream_t s) {
   if (cpw <= 1) return launch_gemm_cfg<T, EPI, NB, 1>(a, s);
@@ -322,19 +328,29 @@ hipError_t launch_gemm_nb(int cpw, const GemmArgs& a, hipStream_t s) {
   if (cpw <= 3) return launch_gemm_cfg<T, EPI, NB, 3>(a, s);
   if (cpw <= 4) return launch_gemm_cfg<T, EPI, NB, 4>(a, s);
   if (cpw <= 5) return launch_gemm_cfg<T, EPI, NB, 5>(a, s);
-  if (cpw <= 6) return launch_gemm_cfg<T, EPI, NB, 6>(a, s);
-  return launch_gemm_cfg<T, EPI, NB, 8>(a, s);
+  // four column blocks hold at most 6 chunks per wave in registers (8 spill)
+  if (cpw <= 6 || NB == 4) return launch_gemm_cfg<T, EPI, NB, 6>(a, s);
+  if constexpr (NB != 4) return launch_gemm_cfg<T, EPI, NB, 8>(a, s);
+  return hipErrorInvalidValue;
 }
 
+// cols: 16-column blocks per workgroup, 1, 2 or 4 (4: bf16 only, fp32 takes
+// 2: its operands would not fit the registers); a count that does not divide
+// the output's blocks falls back to fewer.
 template <int EPI>
 hipError_t launch_gemm_epi(int cols, const GemmArgs& a, hipStream_t s) {
-  const bool two = cols == 2 && (a.Nout / 16) % 2 == 0;
+  const int nb = a.Nout / 16;
+  int c = cols >= 4 && nb % 4 == 0 ? 4 : cols >= 2 && nb % 2 == 0 ? 2 : 1;
+  if (c == 4 && !a.sh.dtype) c = nb % 2 == 0 ? 2 : 1;
   const int kper = (a.kchunks + a.ksplit - 1) / a.ksplit;
   const int cpw = std::min((kper + gemm_waves<EPI>() - 1) / gemm_waves<EPI>(), 8);
   // the folded LayerNorm needs the whole K range in one workgroup
   if (ln_on_load<EPI>() && a.ksplit != 1) return hipErrorInvalidValue;
-  if (a.sh.dtype) return two ? launch_gemm_nb<uint16_t, EPI, 2>(cpw, a, s) : launch_gemm_nb<uint16_t, EPI, 1>(cpw, a, s);
-  return two ? launch_gemm_nb<float, EPI, 2>(cpw, a, s) : launch_gemm_nb<float, EPI, 1>(cpw, a, s);
+  if (a.sh.dtype) {
+    if (c == 4) return launch_gemm_nb<uint16_t, EPI, 4>(cpw, a, s);
+    return c == 2 ? launch_gemm_nb<uint16_t, EPI, 2>(cpw, a, s) : launch_gemm_nb<uint16_t, EPI, 1>(cpw, a, s);
+  }
+  return c == 2 ? launch_gemm_nb<float, EPI, 2>(cpw, a, s) : launch_gemm_nb<float, EPI, 1>(cpw, a, s);
 }
 
 }  // namespace incvit

@@ -238,10 +238,19 @@ GemmGeom gemm_geom(const Shape& sh, int kind) {
 // the output projection and the MLP down projection (and the MLP up
 // projection from 1536 rows) halve the A reads: measured on MI355X, e.g. the
 // 8-stream full encode 5.75 -> 4.70 ms, the 448x448 top-k step 1.58 -> 1.47 ms.
-int cols_of(const int* tuned, const GemmGeom& g, int kind, int rgroups, int rows) {
+int cols_of(const int* tuned, const GemmGeom& g, int kind, int rgroups, int rows, bool exact) {
   const int t = tuned ? tuned[kind] : 0;
   if (t > 0) return t;
   if (rgroups > 1) {
+    // four blocks (bf16; fewer where they do not divide) for QKV and for the
+    // unsplit MLP down projection: 448x448 top-k at 102 / 256 / 1024 rows,
+    // QKV 11.2 -> 8.9, 17.3 -> 15.3, 41.9 -> 33.1 us; down projection at 256
+    // and 1024 rows 18.5 -> 15.7, 65.1 -> 45.5 us; the output projection, fc1
+    // and the K-split down projection were slower with four.  Not beyond 1024
+    // known rows, where each row group loops over many row blocks and a
+    // quarter of the workgroups leaves CUs idle (8 streams' full encode
+    // 4.7 -> 5.2 ms).
+    if ((kind == G_QKV || (kind == G_FC2 && g.ksplit == 1)) && (!exact || rows <= 1024)) return 4;
     if (kind == G_OPROJ || kind == G_FC2) return g.nblocks % 2 == 0 ? 2 : 1;
     if (kind == G_FC1) return rows >= 1536 || g.nblocks > 256 * rgroups ? 2 : 1;
     return 1;
@@ -456,7 +465,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           }
           break;
       }
-      const int cols = cols_of(h->cols, g, kind, a.rgroups, mlp ? mlp_rows : mmax);
+      const int cols = cols_of(h->cols, g, kind, a.rgroups, mlp ? mlp_rows : mmax, exact_m || (mlp && all));
       return run(h, kernel_kind, s, [&] { return launch_gemm(epi, cols, a, s); });
     };
     auto rowk = [&](int kernel_kind) -> incvit_status {
@@ -907,7 +916,7 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
   for (int k = 0; k < 4; ++k) {
     const int c = t ? t->cols[k] : 0;
-    if (c < 0 || c > 2) return fail(h, INCVIT_ERR_ARG, "cols must be 0, 1 or 2");
+    if (c < 0 || c > 4 || c == 3) return fail(h, INCVIT_ERR_ARG, "cols must be 0, 1, 2 or 4");
   }
   const int q = t ? t->attn_qtiles : 0;
   if (q < 0 || q > 2) return fail(h, INCVIT_ERR_ARG, "attn_qtiles must be 0, 1 or 2");

@@ -243,6 +243,8 @@ def test_argument_errors_are_reported_before_launch():
     assert L.incvit_full_encode(enc.h, 2, fr[0].data_ptr(), [c[0] + 8, c[1]], ws) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, [3, 0, 0, 0]) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, [0, 0, -1, 0]) == L.INCVIT_ERR_ARG
+    assert L.incvit_set_tuning(enc.h, [0, 0, 0, 5]) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, [1, 2, 0, 2]) == L.INCVIT_OK
+    assert L.incvit_set_tuning(enc.h, [4, 4, 4, 4]) == L.INCVIT_OK
     assert L.incvit_set_tuning(enc.h, attn_waves=3) == L.INCVIT_ERR_ARG
     assert L.incvit_set_tuning(enc.h, None) == L.INCVIT_OK

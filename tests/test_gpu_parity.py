@@ -179,3 +179,30 @@ def test_patch16_register_tiles(case, score):
         assert count.sum() > 0 if t == 1 else (count == 9).all()
         p.check_step(idx, count, refreshed, res, f"step {t}")
         p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+@pytest.mark.parametrize("cols", [(4, 4, 4, 4), (1, 2, 1, 2)])
+def test_gemm_column_blocks(cols, mode):
+    """GEMM workgroups of one, two and four 16-column blocks (every epilogue:
+    QKV with the folded LayerNorm and the K/V scatter, output projection with
+    the residual, MLP up with GELU, MLP down as K-split partial sums or whole
+    K with the residual) in full encodes (8 row groups) and steps: the column
+    count changes which workgroup computes a column, never its sum order."""
+    from paper_2607_12287_amd import incvit
+    m = synth.small_model(dim=256, depth=2, heads=4, mlp=512, img=64, patch=4, dtype="bf16")
+    w = synth.make_weights(m, 1601)
+    say(f"[gemm cols={cols} fc2 mode {mode}] N={m.n_tokens} D={m.dim} F={m.mlp_dim}")
+    its = [synth.RefillRectStream(m, 1610 + v, v, 23, 29).frames(3) for v in range(2)]
+    frames = [np.stack([synth.patchify(next(it), m.patch) for it in its]) for _ in range(3)]
+    p = Pair(m, w, 2)
+    incvit._check(incvit.incvit_set_tuning(p.enc.h, cols=cols, fc2_mode=mode), p.enc.h)
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    p.check_caches("full")
+    for t, (tau, caps) in enumerate([(0.98, [m.n_tokens, 50]), (np.inf, [200, 37])], start=1):
+        idx, count, refreshed, res = p.step(frames[t], tau, caps)
+        say(f"  step {t}: count={count.tolist()}")
+        p.check_step(idx, count, refreshed, res, f"step {t}")
+        p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
+        p.check_caches(f"step {t}")
