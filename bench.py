@@ -636,8 +636,8 @@ def main() -> int:
         return dump_workload(args.workload, args.rho, args.dump_workload, args.steps + 1)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the encoder's state is per stream and this build runs "
-              "single-GPU only (streams would shard across GPUs with no exchange); use --gpus 1.",
+        print("bench.py measures one GPU: the encoder's state is per stream and the library runs "
+              "on one GPU only (streams would shard across GPUs with no exchange); use --gpus 1.",
               file=sys.stderr)
         return 2
     if args.copy_pass:

@@ -22,7 +22,7 @@ The model is a pre-LN ViT (the paper's vision encoder is a SigLIP/ViT, §III-A):
 no CLS token, learned positions added after the patch embedding, biased
 linear layers, LayerNorm with biased variance, tanh-form GELU, softmax
 attention scaled by 1/sqrt(d_h), and a final LayerNorm.  These details are not
-in the paper; they are the readings this build takes.
+in the paper; they are the readings taken here.
 
 What the cosine compares (``Model.score``): "embed" scores the layer-1 input
 token (patch embedding + position) against its value at the token's last

@@ -249,8 +249,12 @@ int cols_of(const int* tuned, const GemmGeom& g, int kind, int rgroups, int rows
     // and the K-split down projection were slower with four.  Not beyond 1024
     // known rows, where each row group loops over many row blocks and a
     // quarter of the workgroups leaves CUs idle (8 streams' full encode
-    // 4.7 -> 5.2 ms).
-    if ((kind == G_QKV || (kind == G_FC2 && g.ksplit == 1)) && (!exact || rows <= 1024)) return 4;
+    // 4.7 -> 5.2 ms), and for QKV only while the workgroups still cover the
+    // CUs (448x448 top-k at 51 rows, 2 row groups, 108 workgroups: the step
+    // 1.21 -> 1.26 ms).
+    const bool few = !exact || rows <= 1024;
+    if (kind == G_QKV && few && g.nblocks / 4 * rgroups >= 192) return 4;
+    if (kind == G_FC2 && g.ksplit == 1 && few) return 4;
     if (kind == G_OPROJ || kind == G_FC2) return g.nblocks % 2 == 0 ? 2 : 1;
     if (kind == G_FC1) return rows >= 1536 || g.nblocks > 256 * rgroups ? 2 : 1;
     return 1;
