@@ -551,6 +551,37 @@ def summarize_mfma(directory: str, drive_log: str, out: str, command: str) -> No
     print("\n".join(lines))
 
 
+def summarize_counters(directory: str, drive_log: str, out: str, command: str) -> None:
+    """Every counter of one rocprofv3 --pmc pass, per kernel kind: the mean per
+    dispatch over the last n dispatches of each kind (the incremental steps of
+    the driver's run).  SQ counters are summed over the chip's shader engines
+    (cycles are counted per SIMD or per wave as the counter defines)."""
+    b = _bench_json(drive_log)
+    names = sorted({r["Counter_Name"] for r in _csv_rows(directory, "counter_collection.csv")})
+    vals = {}
+    for name in names:
+        disp = _pmc_per_dispatch(directory, name)
+        by_kind = {}
+        for (_, n, v), k in zip(disp, kinds_in_order([n for _, n, _ in disp])):
+            if k:
+                by_kind.setdefault(k, []).append(v)
+        for k, n in b["kernel_launches"].items():
+            got = by_kind.get(k, [])[-n:]
+            if got:
+                vals.setdefault(k, {})[name] = statistics.mean(got)
+    lines = [f"# rocprofv3 --pmc {' '.join(names)} per launch ({b['config']['workload']})",
+             f"# command: {command}",
+             f"# mean rows/step {b['config']['rows_mean']}; per kind: mean per dispatch over the last n dispatches "
+             "(the incremental steps)",
+             f"source_hash {source_hash()}",
+             f"{'kind':8s} " + " ".join(f"{n:>20s}" for n in names)]
+    for k, v in vals.items():
+        lines.append(f"{k:8s} " + " ".join(f"{v.get(n, float('nan')):20.0f}" for n in names))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def dump_workload(name: str, rho: float, directory: str, frames: int) -> int:
     """Write a workload for the native driver (CPU only): config.txt,
     weights.bin (canonical, storage dtype) and frames.bin ([frames][views][N][P] f32)."""
@@ -596,6 +627,7 @@ def main() -> int:
     ap.add_argument("--summarize-trace", nargs=5, metavar=("TRACE_DIR", "TRACED_BENCH_LOG", "PLAIN_BENCH_LOG", "OUT",
                                                            "COMMAND"))
     ap.add_argument("--summarize-mfma", nargs=4, metavar=("PMC_DIR", "DRIVE_LOG", "OUT", "COMMAND"))
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("PMC_DIR", "DRIVE_LOG", "OUT", "COMMAND"))
     ap.add_argument("--summarize-pmc", nargs=8, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
                                                          "COPY_WRITE_DIR", "BENCH_LOG", "COPY_LOG", "OUT", "COMMANDS"))
     ap.add_argument("--steps", type=int, default=500)
@@ -631,6 +663,9 @@ def main() -> int:
         return 0
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma)
+        return 0
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
         return 0
     if args.dump_workload:
         return dump_workload(args.workload, args.rho, args.dump_workload, args.steps + 1)

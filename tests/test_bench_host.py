@@ -70,3 +70,27 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_counter_summary(tmp_path):
+    # two kinds, the last n dispatches of each kind are averaged (n from the run's launch counts)
+    d = tmp_path / "pmc"
+    d.mkdir()
+    rows = ["Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value"]
+    names = ["incvit::sim_kernel(incvit::SimArgs)", "void incvit::gemm_kernel<unsigned short, 1, 2, 5>(incvit::GemmArgs)"]
+    vals = {0: [1.0, 10.0], 1: [3.0, 30.0], 2: [5.0, 50.0]}  # dispatch round -> (sim, fc1) values
+    i = 0
+    for rnd in range(3):
+        for k, name in enumerate(names):
+            for se in range(2):  # per shader engine: summed per dispatch
+                rows.append(f'{i},"{name}",SQ_INSTS_VALU,{vals[rnd][k] / 2}')
+            i += 1
+    (d / "run_counter_collection.csv").write_text("\n".join(rows) + "\n")
+    log = tmp_path / "drive.log"
+    log.write_text('{"config": {"workload": "w", "rows_mean": 1.0}, "kernel_launches": {"sim": 2, "fc1": 1}}\n')
+    out = tmp_path / "out.txt"
+    bench.summarize_counters(str(d), str(log), str(out), "cmd")
+    lines = {ln.split()[0]: ln.split()[1:] for ln in out.read_text().splitlines() if not ln.startswith("#")}
+    assert float(lines["sim"][0]) == 4.0    # mean of rounds 1, 2
+    assert float(lines["fc1"][0]) == 50.0   # the last round only
+    assert lines["source_hash"] == [bench.source_hash()]
