@@ -285,7 +285,11 @@ void incvit_graph_destroy(incvit_graph* g);
  * row_groups: 32-row groups per GEMM launch in steps with a finite threshold
  * (1..8; 0 = 1): a caller that expects about R refreshed rows per call can set
  * ceil(R / 32).  Full encodes and pure top-k steps (tau = +inf), whose row
- * count is known, choose it themselves.
+ * count is known, choose it themselves.  With at most 6 groups each GEMM keeps
+ * only as many as its workgroups fill the chip once (QKV in four-block
+ * workgroups: one per CU; MLP up projection: two per CU; K-split MLP down
+ * projection: one per CU; output projection: all), the rest looping over the
+ * row blocks.
  * A NULL pointer restores the defaults. */
 typedef struct {
   int32_t cols[4];

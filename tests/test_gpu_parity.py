@@ -46,12 +46,15 @@ def test_small_models_stream(name):
         p.check_caches(f"{name} step {t}")
 
 
-def _workload_run(name, steps, oracle_views=None, rho=0.10):
+def _workload_run(name, steps, oracle_views=None, rho=0.10, row_groups=0):
     wl = synth.workload(name, rho=rho)
     m = wl.model
-    say(f"[{name}] rho={rho} views={wl.views} steps={steps}")
+    say(f"[{name}] rho={rho} views={wl.views} steps={steps} row_groups={row_groups}")
     w = wl.weights()
     p = Pair(m, w, wl.views, oracle_views)
+    if row_groups:
+        from paper_2607_12287_amd import incvit
+        incvit._check(incvit.incvit_set_tuning(p.enc.h, row_groups=row_groups), p.enc.h)
     frames = list(wl.patch_frames(steps + 1))
     p.full_encode(frames[0])
     tf = p.check_layers(None, f"{name} full")
@@ -73,8 +76,11 @@ def test_so400m_workload():
     _workload_run("so400m", 3)
 
 
-def test_so400m_three_views():
-    _workload_run("so400m_x3", 2)
+@pytest.mark.parametrize("row_groups", [0, 4])
+def test_so400m_three_views(row_groups):
+    """row_groups 4: the threshold steps' GEMM row groups that a caller expecting
+    about a hundred rows sets (each GEMM then takes its own share of them)."""
+    _workload_run("so400m_x3", 2, row_groups=row_groups)
 
 
 @pytest.mark.parametrize("rho", [0.02, 0.10, 1.0])
@@ -82,8 +88,9 @@ def test_so400m_448_top_k(rho):
     _workload_run("so400m_448", 1, rho=rho)
 
 
-def test_vitl_eight_streams_sampled():
-    _workload_run("vitl_x8", 2, oracle_views=[0, 5])
+@pytest.mark.parametrize("row_groups", [0, 6])
+def test_vitl_eight_streams_sampled(row_groups):
+    _workload_run("vitl_x8", 2, oracle_views=[0, 5], row_groups=row_groups)
 
 
 @pytest.mark.parametrize("waves", [2, 4, 8])
