@@ -188,8 +188,10 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   // later block reloads (the weights stay in registers).
   auto row_block = [&](const int m0, auto first) {
     if constexpr (!decltype(first)::value) {
-      load_a(m0, 0);
-      if (rounds > 1) load_w(0);
+      if (rounds > 1) {  // with one round the A fragments were loaded ahead (below)
+        load_a(m0, 0);
+        load_w(0);
+      }
       if constexpr (has_rows<EPI>()) rinfo = a.rows[m0 + 16 * re + 4 * g + ie];
       if constexpr (has_resid<EPI>()) load_res(m0);
     }
@@ -224,6 +226,10 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
         }
       }
     }
+    // One round: the weights stay in registers and the A fragments are free
+    // once the products are issued, so the group's next row block loads its A
+    // now, behind this block's reduction and epilogue (uniform branch).
+    if (rounds == 1 && m0 + mstep < M) load_a(m0 + mstep, 0);
 
     // ---- sum the waves' partial tiles in wave order
 #pragma unroll
