@@ -36,25 +36,30 @@ constexpr int kMaxDT = kMaxHeadDim / 16;  // 16-wide d tiles
 // K/V operands of one 32-key block come straight from the cache, which stores
 // them in operand order (k_elem / v_elem): every load is one contiguous
 // kilobyte.  Dims past d_h are zeroed in the K operand (the matching Q values
-// are in-bounds data of the same row); keys past N are masked in the scores
-// and zeroed in the V operand (their cache entries are never written).
+// are in-bounds data of the same row); the lanes that hold them read the
+// position of lane group 0 instead (lines the wave fetches anyway), so a
+// padded chunk moves a quarter of its bytes.  Keys past N are masked in the
+// scores and zeroed in the V operand (their cache entries are never written).
 template <class T, int NDC>
 __device__ __forceinline__ void load_kblock(V8<T> (&kop)[2][NDC], const T* kbase, int kb, int dh, int g, int lane) {
-  const T* blk = kbase + (size_t)kb * 2 * NDC * kChunkElems + lane * 8;
+  const T* blk = kbase + (size_t)kb * 2 * NDC * kChunkElems;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int c = 0; c < NDC; ++c) {
-      kop[t][c].load(blk + (t * NDC + c) * kChunkElems);
-      if (32 * c + 8 * g >= dh) kop[t][c].zero();
+      const bool pad = 32 * c + 8 * g >= dh;
+      kop[t][c].load(blk + (t * NDC + c) * kChunkElems + (pad ? lane & 15 : lane) * 8);
+      if (pad) kop[t][c].zero();
     }
 }
 
-template <class T, int NDT>
-__device__ __forceinline__ void load_vblock(V8<T> (&vop)[NDT], const T* vbase, int kb, int lane) {
+// V: the block stores NDT 16-dim tiles; only the first NDTU (those holding
+// dims below d_h) are loaded and multiplied
+template <class T, int NDT, int NDTU>
+__device__ __forceinline__ void load_vblock(V8<T> (&vop)[NDTU], const T* vbase, int kb, int lane) {
   const T* blk = vbase + (size_t)kb * NDT * kChunkElems + lane * 8;
 #pragma unroll
-  for (int t = 0; t < NDT; ++t) vop[t].load(blk + t * kChunkElems);
+  for (int t = 0; t < NDTU; ++t) vop[t].load(blk + t * kChunkElems);
 }
 
 // zero the V operand entries of keys >= N (lane group g holds keys 8g..8g+7)
@@ -89,7 +94,7 @@ __device__ __forceinline__ void mask_v(V8<float>& v, int first_key, int N) {
 // issued early too.  The waves' (max, sum, O) are exchanged through LDS once
 // and combined in wave order, each wave finishing a share of the output
 // tiles.
-template <class T, int NDC, int NDT, int GB, int QT, int KW>
+template <class T, int NDC, int NDT, int NDTU, int GB, int QT, int KW>
 __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
   extern __shared__ __align__(16) char attn_smem[];
 
@@ -113,13 +118,13 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
   // the stream's row offsets: scalar loads, issued first, waited for last
   const int off_v = a.meta->off[v], off_next = a.meta->off[v + 1];
   const int kb0 = w * nkb / KW, kb1 = (w + 1) * nkb / KW;  // this wave's key blocks (may be none)
-  V8<T> kop[GB][2][NDC], vop[GB][NDT];
+  V8<T> kop[GB][2][NDC], vop[GB][NDTU];
   auto load_group = [&](int kb) {
 #pragma unroll
     for (int b = 0; b < GB; ++b) {
       const int k = min(kb + b, nkb - 1);
       load_kblock<T, NDC>(kop[b], kbase, k, dh, g, lane);
-      load_vblock<T, NDT>(vop[b], vbase, k, lane);
+      load_vblock<T, NDT, NDTU>(vop[b], vbase, k, lane);
     }
   };
   // The first query groups of a stream are the likely active ones: they load
@@ -154,13 +159,13 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
   if (!spec || v != 0) load_q(rowbase, kv);
 
   float m_run[QT], l_run[QT];
-  f32x4_t o[QT][NDT];
+  f32x4_t o[QT][NDTU];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     m_run[qt] = -INFINITY;
     l_run[qt] = 0.0f;
 #pragma unroll
-    for (int t = 0; t < NDT; ++t) o[qt][t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int t = 0; t < NDTU; ++t) o[qt][t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
   }
 
   for (int kb = kb0; kb < kb1; kb += GB) {
@@ -171,7 +176,7 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
         const int key0 = (kb + b) * 32;
         if (key0 + 32 > N) {  // the stream's last, partial block (uniform)
 #pragma unroll
-          for (int t = 0; t < NDT; ++t) mask_v(vop[b][t], key0 + 8 * g, N);
+          for (int t = 0; t < NDTU; ++t) mask_v(vop[b][t], key0 + 8 * g, N);
         }
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
@@ -211,7 +216,7 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
           V8<T> pop;
           pack_p(pop, p);
 #pragma unroll
-          for (int t = 0; t < NDT; ++t) {
+          for (int t = 0; t < NDTU; ++t) {
             o[qt][t] *= alpha;
             mma(o[qt][t], vop[b][t], pop);
           }
@@ -231,7 +236,7 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
   // partials, in wave order, for its share of the output tiles and stores them
   float* s_m = reinterpret_cast<float*>(attn_smem);               // [KW][QT][16]
   float* s_l = s_m + KW * QT * 16;                                 // [KW][QT][16]
-  f32x4_t* s_o = reinterpret_cast<f32x4_t*>(s_l + KW * QT * 16);   // [KW][QT][NDT][64]
+  f32x4_t* s_o = reinterpret_cast<f32x4_t*>(s_l + KW * QT * 16);   // [KW][QT][NDTU][64]
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     if (g == 0) {
@@ -239,11 +244,11 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
       s_l[(w * QT + qt) * 16 + n] = l_run[qt];
     }
 #pragma unroll
-    for (int t = 0; t < NDT; ++t) s_o[((w * QT + qt) * NDT + t) * 64 + lane] = o[qt][t];
+    for (int t = 0; t < NDTU; ++t) s_o[((w * QT + qt) * NDTU + t) * 64 + lane] = o[qt][t];
   }
   __syncthreads();
-  for (int it = w; it < QT * NDT; it += KW) {
-    const int qt = it / NDT, t = it % NDT;
+  for (int it = w; it < QT * NDTU; it += KW) {
+    const int qt = it / NDTU, t = it % NDTU;
     const int qrow = q0 + 16 * qt + n;
     const int d0 = 16 * t + 4 * g;
     float mm = -INFINITY;
@@ -256,7 +261,7 @@ __global__ __launch_bounds__(KW * 64) void attn_kernel(AttnArgs a) {
       const float mw = s_m[(ww * QT + qt) * 16 + n];
       const float f = mw == -INFINITY ? 0.0f : exp2f(mw - mm);
       lsum += f * s_l[(ww * QT + qt) * 16 + n];
-      acc += s_o[((ww * QT + qt) * NDT + t) * 64 + lane] * f;
+      acc += s_o[((ww * QT + qt) * NDTU + t) * 64 + lane] * f;
     }
     if (qrow < kv && d0 < dh) {
       const float inv = 1.0f / lsum;
@@ -273,34 +278,37 @@ constexpr int attn_lds_bytes() {
   return KW * QT * 16 * 4 * 2 + KW * QT * NDT * 64 * 16;  // m and l, then O
 }
 
-template <class T, int NDC, int NDT, int GB, int QT, int KW>
+template <class T, int NDC, int NDT, int NDTU, int GB, int QT, int KW>
 static void launch_g(const AttnArgs& a, dim3 grid, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, GB, QT, KW>),
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, NDC, NDT, NDTU, GB, QT, KW>),
                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                               attn_lds_bytes<NDT, QT, KW>()) == hipSuccess;
+                               attn_lds_bytes<NDTU, QT, KW>()) == hipSuccess;
   }
-  (void)launch_k((attn_kernel<T, NDC, NDT, GB, QT, KW>), grid, dim3(KW * 64), (size_t)attn_lds_bytes<NDT, QT, KW>(),
-                 s, a);
+  (void)launch_k((attn_kernel<T, NDC, NDT, NDTU, GB, QT, KW>), grid, dim3(KW * 64),
+                 (size_t)attn_lds_bytes<NDTU, QT, KW>(), s, a);
 }
 
-template <class T, int NDC, int NDT, int QT>
+template <class T, int NDC, int NDT, int NDTU, int QT>
 static void launch_t(const AttnArgs& a, int kw, dim3 grid, hipStream_t s) {
   // two key blocks in flight per wave where the registers allow
   constexpr int kGB = NDT <= (sizeof(T) == 2 ? 6 : 4) ? 2 : 1;
-  if (kw == 2) launch_g<T, NDC, NDT, kGB, QT, 2>(a, grid, s);
-  else if (kw == 4) launch_g<T, NDC, NDT, kGB, QT, 4>(a, grid, s);
-  else launch_g<T, NDC, NDT, kGB, QT, 8>(a, grid, s);
+  if (kw == 2) launch_g<T, NDC, NDT, NDTU, kGB, QT, 2>(a, grid, s);
+  else if (kw == 4) launch_g<T, NDC, NDT, NDTU, kGB, QT, 4>(a, grid, s);
+  else launch_g<T, NDC, NDT, NDTU, kGB, QT, 8>(a, grid, s);
 }
 
+// head dims in 32-wide K chunks (NDC) and 16-wide V tiles (NDT stored, NDTU
+// used: d_h = 72 stores 96 dims and uses 80)
 template <class T, int QT>
 static void launch_dh(const AttnArgs& a, int kw, dim3 grid, hipStream_t s) {
   const int dh = a.sh.dh;
-  if (dh <= 32) launch_t<T, 1, 2, QT>(a, kw, grid, s);
-  else if (dh <= 64) launch_t<T, 2, 4, QT>(a, kw, grid, s);
-  else if (dh <= 96) launch_t<T, 3, 6, QT>(a, kw, grid, s);
-  else launch_t<T, 4, 8, QT>(a, kw, grid, s);
+  if (dh <= 32) launch_t<T, 1, 2, 2, QT>(a, kw, grid, s);
+  else if (dh <= 64) launch_t<T, 2, 4, 4, QT>(a, kw, grid, s);
+  else if (dh <= 80) launch_t<T, 3, 6, 5, QT>(a, kw, grid, s);
+  else if (dh <= 96) launch_t<T, 3, 6, 6, QT>(a, kw, grid, s);
+  else launch_t<T, 4, 8, 8, QT>(a, kw, grid, s);
 }
 
 // qtiles: 16-query tiles per workgroup (1 or 2).  One tile per workgroup
