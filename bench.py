@@ -82,6 +82,25 @@ def stored_traffic(workload: str, kind: str):
     return vals.get(kind)
 
 
+def quantile(xs_sorted, q: float) -> float:
+    """Linear-interpolation quantile of an ascending list."""
+    if not xs_sorted:
+        return float("nan")
+    pos = q * (len(xs_sorted) - 1)
+    i = int(pos)
+    j = min(i + 1, len(xs_sorted) - 1)
+    return xs_sorted[i] + (xs_sorted[j] - xs_sorted[i]) * (pos - i)
+
+
+def rows_dist(k) -> dict:
+    """Distribution of the refreshed rows: per step (summed over the streams)
+    min / median / p90 / max, and the mean per stream."""
+    tot = sorted(float(x) for x in k.sum(axis=1))
+    return {"per_step": {"min": tot[0], "median": quantile(tot, 0.5), "p90": round(quantile(tot, 0.9), 2),
+                         "max": tot[-1]},
+            "per_stream_mean": [round(float(x), 2) for x in k.mean(axis=0)]}
+
+
 def ksplit(m) -> int:
     """K split of the MLP down projection (the library's rule)."""
     nblocks = m.dim // 16
@@ -768,6 +787,39 @@ def main() -> int:
         enc.drop_graph(gstep)
     approx = approx_vs_full(enc, caches, frames[total - 1])
 
+    # the same stream again on fresh caches, each step bracketed by its own
+    # events (outside the timed region above): the median and p90 of a step
+    buf3, caches3 = enc.new_caches(B)
+    enc.full_encode(frames[0], caches3)
+    g3 = enc.step_graph(inp, caches3, wl.tau, wl.caps, out) if args.graph else None
+
+    def step3(t):
+        inp.copy_(frames[t])
+        if g3 is not None:
+            enc.launch(g3)
+        else:
+            enc.step(inp, caches3, wl.tau, wl.caps, out=out)
+
+    for t in range(1, args.warmup + 1):
+        step3(t)
+    torch.cuda.synchronize()
+    evs = []
+    for t in range(args.warmup + 1, total):
+        inp.copy_(frames[t])
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record()
+        if g3 is not None:
+            enc.launch(g3)
+        else:
+            enc.step(inp, caches3, wl.tau, wl.caps, out=out)
+        a1.record()
+        evs.append((a0, a1))
+    torch.cuda.synchronize()
+    each_ms = sorted(a0.elapsed_time(a1) for a0, a1 in evs)
+    if g3 is not None:
+        enc.drop_graph(g3)
+    del buf3, caches3
+
     # same frames again, eagerly, with per-kernel events on the launch stream
     buf2, caches2 = enc.new_caches(B)
     enc.full_encode(frames[0], caches2)
@@ -800,6 +852,10 @@ def main() -> int:
         "full_encode_frames_per_s": round(B * 1e3 / full_med, 2),
         "speedup_vs_full_encode": round(full_med / step_ms, 3),
         "approx_cos_vs_full": approx,
+        "step_ms_dist": {"median": round(statistics.median(each_ms), 5), "p90": round(quantile(each_ms, 0.9), 5),
+                         "min": round(each_ms[0], 5), "max": round(each_ms[-1], 5)},
+        "full_encode_ms_dist": {"median": round(full_med, 5), "p90": round(quantile(sorted(full_ms), 0.9), 5)},
+        "rows_dist": rows_dist(k),
     }
     if not args.no_torch_full:
         tms, tmode = torch_full_forward(m, wl.weights(), frames[0], max(5, args.full_repeats // 2))

@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     ("incvit::sim_kernel(incvit::SimArgs)", "sim"),
     ("incvit::select_kernel(incvit::SelectArgs)", "select"),
     ("void incvit::attn_kernel<unsigned short, 3, 6, 2, 1, 4>(incvit::AttnArgs)", "attn"),
+    ("void incvit::attn_kernel<unsigned short, 3, 6, 5, 2, 1, 4>(incvit::AttnArgs)", "attn"),
     ("__amd_rocclr_copyBuffer", None),
     ("void at::native::vectorized_elementwise_kernel<4, at::native::FillFunctor<unsigned char>>", None),
 ])
@@ -94,3 +95,16 @@ def test_counter_summary(tmp_path):
     assert float(lines["sim"][0]) == 4.0    # mean of rounds 1, 2
     assert float(lines["fc1"][0]) == 50.0   # the last round only
     assert lines["source_hash"] == [bench.source_hash()]
+
+
+def test_quantile_and_rows_distribution():
+    """The p90 and the refreshed-row distribution the bench line reports."""
+    import numpy as np
+    assert bench.quantile([1.0], 0.9) == 1.0
+    assert bench.quantile([0.0, 10.0], 0.9) == pytest.approx(9.0)
+    xs = sorted(float(i) for i in range(11))  # 0..10
+    assert bench.quantile(xs, 0.5) == 5.0 and bench.quantile(xs, 0.9) == pytest.approx(9.0)
+    k = np.array([[3, 1], [5, 2], [0, 0], [10, 4]])  # steps x streams
+    d = bench.rows_dist(k)
+    assert d["per_step"] == {"min": 0.0, "median": 5.5, "p90": pytest.approx(11.9), "max": 14.0}
+    assert d["per_stream_mean"] == [4.5, 1.75]
