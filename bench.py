@@ -82,6 +82,38 @@ def stored_traffic(workload: str, kind: str):
     return vals.get(kind)
 
 
+def run_env(torch) -> dict:
+    """Versions and clocks of the run (best effort: fields that cannot be read
+    are left out)."""
+    env = {"torch": torch.__version__, "hip": getattr(torch.version, "hip", None)}
+    try:
+        p = torch.cuda.get_device_properties(0)
+        env.update({"device": p.name, "arch": getattr(p, "gcnArchName", None),
+                    "compute_units": p.multi_processor_count, "hbm_gib": round(p.total_memory / 2**30, 1)})
+    except Exception:
+        pass
+    try:
+        with open("/sys/module/amdgpu/version") as f:
+            env["amdgpu_driver"] = f.read().strip()
+    except OSError:
+        pass
+    # current DPM levels (the line marked '*') of the first card that has them
+    for dev in sorted(glob.glob("/sys/class/drm/card*/device")):
+        clocks = {}
+        for name in ("pp_dpm_sclk", "pp_dpm_mclk", "pp_dpm_fclk"):
+            try:
+                with open(os.path.join(dev, name)) as f:
+                    cur = [ln.split(":", 1)[1].replace("*", "").strip() for ln in f if ln.rstrip().endswith("*")]
+                if cur:
+                    clocks[name[7:]] = cur[0]
+            except (OSError, IndexError):
+                pass
+        if clocks:
+            env["clocks"] = clocks
+            break
+    return env
+
+
 def quantile(xs_sorted, q: float) -> float:
     """Linear-interpolation quantile of an ascending list."""
     if not xs_sorted:
@@ -914,6 +946,7 @@ def main() -> int:
         n_cpu = min(len(frames_np), 64)
         result["cpu_baseline"] = cpu_baseline(wl, frames_np[:n_cpu], args.cpu_seconds)
 
+    result["env"] = run_env(torch)
     print(json.dumps(result), flush=True)
     return 0
 
