@@ -264,7 +264,8 @@ int cols_of(const int* tuned, const GemmGeom& g, int kind, int rgroups, int rows
 
 // Row groups of one GEMM launch, from the call's row groups R (rows known on
 // the host, or the caller's expected count).  While R is small (at most 6
-// blocks of 32 rows: steps, not full encodes) each GEMM keeps only as many
+// blocks of 32 rows, as in the steps; full encodes of 256 or more rows have
+// 8, and keep them) each GEMM keeps only as many
 // groups as its workgroups fill the chip once; the groups then loop over the
 // remaining row blocks with their weights still in registers:
 //   QKV with four-block workgroups: at most one workgroup per CU (more put two

@@ -38,7 +38,8 @@ constexpr int kMaxDT = kMaxHeadDim / 16;  // 16-wide d tiles
 // kilobyte.  Dims past d_h are zeroed in the K operand (the matching Q values
 // are in-bounds data of the same row); the lanes that hold them read the
 // position of lane group 0 instead (lines the wave fetches anyway), so a
-// padded chunk moves a quarter of its bytes.  Keys past N are masked in the
+// padded chunk moves only the bytes of its real dims (a quarter of the chunk
+// at d_h = 72).  Keys past N are masked in the
 // scores and zeroed in the V operand (their cache entries are never written).
 template <class T, int NDC>
 __device__ __forceinline__ void load_kblock(V8<T> (&kop)[2][NDC], const T* kbase, int kb, int dh, int g, int lane) {
