@@ -26,33 +26,45 @@ in the paper; they are the readings taken here.
 
 What the cosine compares (``Model.score``): "embed" scores the layer-1 input
 token (patch embedding + position) against its value at the token's last
-refresh; "key" scores the first layer's key projection of that token, as eq. 3
-states it ("cosine similarity between current and previously cached keys").
+refresh; "key" scores the first layer's key projection of that token, which is
+what eq. 3 compares (the current key of a token against its cached key).
 Either way the vector is kept per token as the reference for later frames.
 
 The paper's odd/even chunk schedule (a full forward on odd chunks whose keys
 become the reference, incremental encoding on even chunks) is
 ``run_schedule`` with period 2; other periods generalise it.
 
-What "all tokens are processed by the MLP layer" means (``Model.mlp``):
-"reuse" (default) reads it exactly: a reused row's MLP input is its cached
-state, so its MLP output is its cached output and only the rows U need
-computing.  "all" is the non-exact reading: every frame, every row starts from
-this frame's embedded token, reused rows add their cached attention-branch
-output (attention + output projection, per layer) to their current residual
-stream, and the MLP runs over all rows, so reused rows follow the new frame
-without their attention being recomputed (their K and V stay cached).
+How the MLP sentence of §III-B is read (``Model.mlp``; the paper says every
+token goes through the MLP): "reuse" (default) reads it exactly: a reused
+row's MLP input is its cached state, so its MLP output is its cached output
+and only the rows U need computing.  "all" is the non-exact reading: every
+frame, every row starts from this frame's embedded token, reused rows add
+their cached attention-branch output (attention + output projection, per
+layer) to their current residual stream, and the MLP runs over all rows, so
+reused rows follow the new frame without their attention being recomputed
+(their K and V stay cached).
 
 Arithmetic: everything is float64 except the patch embedding, the key score
 and the cosine, which follow a fixed fp32 order (``pinned.c``) so that the
-selection is reproducible bit for bit. ``S(.)`` rounds to the storage precision (bf16 with
-ties to even, fp32, or nothing for the "f64" mode used by the pins) at the
-points where a value between two operations is formed, as a half-precision
-inference pipeline stores every tensor between its operations (the paper runs
-its encoder in FP16 under PyTorch, Appendix A, hardware table): Q/K/V, the LN
-outputs fed to a GEMM, the attention output, the residual H after the
-attention, the GELU output, each layer's output rows, the final output and the
-layer-0 input rows.
+selection is reproducible bit for bit.
+
+Storage rounding, one reading applied everywhere: the paper runs its encoder
+in half precision under PyTorch (Appendix A, hardware table), where every
+operation reads stored tensors, computes internally at higher precision and
+stores its result in the storage type.  ``S(.)`` (round to nearest, ties to
+even, to bf16 or fp32; nothing in the "f64" mode of the pins) is therefore
+applied to the output of every operation of the layer and nowhere else:
+
+    A  = S(LN1(X))            Q|K|V = S(A W_qkv + b_qkv)
+    O  = S(Attn(Q, K, V))     B     = S(O W_o + b_o)       H = S(X + B)
+    A2 = S(LN2(H))            F     = S(A2 W_1 + b_1)      G = S(GELU(F))
+    M  = S(G W_2 + b_2)       X'    = S(H + M)             Y = S(LN_f(X^L))
+
+and X^0 = S(T^0).  A linear layer with its bias is one operation, as is the
+attention.  The two MLP readings share this block exactly (the "all" reading
+caches B per layer), so their full encodes are identical.  The test
+``tests/test_oracle_rounding.py`` pins these points against PyTorch's own
+bf16 modules.
 
 Parity: pinned (see tests/test_oracle_*.py) by library routines (torch fp64
 functional ops), closed forms, brute-force selection, and the invariants the
@@ -240,54 +252,56 @@ def score_vectors(model: Model, t0: np.ndarray) -> np.ndarray:
     return t0
 
 
-def layer_rows(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
-               trace: Optional[dict] = None) -> np.ndarray:
-    """Layer l for the rows U, whose inputs are Z ([|U|][D]); K, V are the
-    layer's full [N][D] key/value caches.  The new K/V rows of U are written
-    into K, V before the attention, so the updated queries see the new keys of
-    U and the cached keys of the other rows.  Returns the layer's output rows."""
+def attn_branch(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
+                trace: Optional[dict] = None) -> np.ndarray:
+    """Attention branch of layer l for the rows U (inputs Z, [|U|][D]):
+    B = S(S(Attn(Q, K, V)) W_o + b_o).  The new K/V rows of U are written into
+    the layer's full [N][D] caches K, V before the attention (eq. 5), so the
+    updated queries see the new keys of U and the cached keys of the rest."""
     m, dt = model.shape, model.dtype
     D = m.dim
     A = S(layer_norm(Z, model.p(l, "ln1_g"), model.p(l, "ln1_b"), model.eps), dt)
-    qkv = S(A @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)
-    q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
-    K[U] = k
-    V[U] = v
-    O = S(attention(q, K, V, m.heads), dt)
-    Hres = S(Z + (O @ model.p(l, "w_o") + model.p(l, "b_o")), dt)
+    qkv = S(A @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)     # eq. 4
+    K[U] = qkv[:, D:2 * D]
+    V[U] = qkv[:, 2 * D:]
+    O = S(attention(qkv[:, :D], K, V, m.heads), dt)
     if trace is not None:
         trace.setdefault("O", []).append(O)
+    return S(O @ model.p(l, "w_o") + model.p(l, "b_o"), dt)
+
+
+def mlp_block(model: Model, l: int, X: np.ndarray, Bo: np.ndarray, trace: Optional[dict] = None) -> np.ndarray:
+    """Residual add of the attention branch, then the MLP with its residual:
+    H = S(X + B), X' = S(H + S(S(GELU(S(S(LN2(H)) W_1 + b_1))) W_2 + b_2))."""
+    dt = model.dtype
+    Hres = S(X + Bo, dt)
+    if trace is not None:
         trace.setdefault("H", []).append(Hres)
     A2 = S(layer_norm(Hres, model.p(l, "ln2_g"), model.p(l, "ln2_b"), model.eps), dt)
-    G = S(gelu_tanh(A2 @ model.p(l, "w_1") + model.p(l, "b_1")), dt)
-    return S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
+    F1 = S(A2 @ model.p(l, "w_1") + model.p(l, "b_1"), dt)
+    G = S(gelu_tanh(F1), dt)
+    M2 = S(G @ model.p(l, "w_2") + model.p(l, "b_2"), dt)
+    return S(Hres + M2, dt)
+
+
+def layer_rows(model: Model, l: int, Z: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
+               trace: Optional[dict] = None) -> np.ndarray:
+    """Layer l for the rows U, whose inputs are Z ([|U|][D]); K, V are the
+    layer's full [N][D] key/value caches (updated in place).  Returns the
+    layer's output rows."""
+    return mlp_block(model, l, Z, attn_branch(model, l, Z, U, K, V, trace), trace)
 
 
 def layer_all(model: Model, l: int, X: np.ndarray, U: np.ndarray, K: np.ndarray, V: np.ndarray,
               A: np.ndarray, trace: Optional[dict] = None) -> np.ndarray:
-    """Layer l in the "all" reading: attention for the rows U only (new K/V
-    rows scattered first), their attention-branch outputs S(O W_o + b_o) into
-    A; every row then adds its A row (new for U, cached for the rest) to its
-    current input and goes through the MLP.  X: [N][D] inputs of all rows;
-    returns the [N][D] outputs."""
-    m, dt = model.shape, model.dtype
-    D = m.dim
+    """Layer l in the "all" reading: the attention branch for the rows U only
+    (new K/V rows scattered first) goes into the branch cache A; every row then
+    adds its A row (new for U, cached for the rest) to its current input and
+    goes through the MLP.  X: [N][D] inputs of all rows; returns the [N][D]
+    outputs."""
     if U.size:
-        Z = X[U]
-        A1 = S(layer_norm(Z, model.p(l, "ln1_g"), model.p(l, "ln1_b"), model.eps), dt)
-        qkv = S(A1 @ model.p(l, "w_qkv") + model.p(l, "b_qkv"), dt)
-        K[U] = qkv[:, D:2 * D]
-        V[U] = qkv[:, 2 * D:]
-        O = S(attention(qkv[:, :D], K, V, m.heads), dt)
-        A[U] = S(O @ model.p(l, "w_o") + model.p(l, "b_o"), dt)
-        if trace is not None:
-            trace.setdefault("O", []).append(O)
-    Hres = S(X + A, dt)
-    if trace is not None:
-        trace.setdefault("H", []).append(Hres)
-    A2 = S(layer_norm(Hres, model.p(l, "ln2_g"), model.p(l, "ln2_b"), model.eps), dt)
-    G = S(gelu_tanh(A2 @ model.p(l, "w_1") + model.p(l, "b_1")), dt)
-    return S(Hres + (G @ model.p(l, "w_2") + model.p(l, "b_2")), dt)
+        A[U] = attn_branch(model, l, X[U], U, K, V, trace)
+    return mlp_block(model, l, X, A, trace)
 
 
 def final_rows(model: Model, Z: np.ndarray) -> np.ndarray:

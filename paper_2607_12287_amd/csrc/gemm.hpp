@@ -3,8 +3,8 @@
 // refreshed rows of the call (rows padded to a multiple of 64):
 //   QKV : [Q K V] = S(LN1(Z_l) W_qkv + b); Q -> workspace, K and V rows
 //         scattered into the cached K^l, V^l of each stream (eq. 5);
-//   RES : the output projection with its residual, H = S(Z_l + (O W_o + b_o));
-//   FC1 : G = S(GELU(LN2(H) W_1 + b_1));
+//   RES : the output projection with its residual, H = S(Z_l + S(O W_o + b_o));
+//   FC1 : G = S(GELU(S(LN2(H) W_1 + b_1)));
 //   PART: raw partial sums of A W over one share of K (the MLP down
 //         projection); a row kernel adds the bias, the residual and the
 //         next LayerNorm;
@@ -12,8 +12,11 @@
 //         cache's A^l rows (the all-rows MLP reading, whose residual is
 //         formed for every row by a row kernel);
 //   DOWN: the MLP down projection over the whole K with its residual,
-//         Z_{l+1} = S(H + (G W_2 + b_2)) into the compact Z and the cache's
+//         Z_{l+1} = S(H + S(G W_2 + b_2)) into the compact Z and the cache's
 //         X^{l+1} (one kernel instead of split-K partials and a row kernel).
+// Every operation's result is rounded to the storage type once, as a
+// half-precision pipeline stores it: the linear output with its bias, then the
+// residual sum, and the MLP's up projection before its GELU.
 // Z, O, H and G are kept in MFMA operand order (frag_off).
 //
 // LayerNorm folded into the GEMM (QKV, FC1): the weights are packed as
@@ -24,7 +27,13 @@
 // product: x * ones gives the row sums and x * x^T (the A fragment is also a
 // valid B fragment of x^T) the sums of squares on its diagonal.  The waves'
 // partial sums meet in LDS with the partial tiles and are combined in wave
-// order in the epilogue (mean = sum / D, var = sumsq / D - mean^2).
+// order in the epilogue (mean = sum / D, var = sumsq / D - mean^2).  This
+// one-pass variance loses about (mean / spread)^2 * 2^-24 of its relative
+// precision, harmless against bf16 storage (1e-3 at a mean 130 times the
+// spread); fp32 models, whose results are held to fp32 precision, take the
+// sums of the shifted values x - x_0 (x_0: the row's first element, so the
+// differences are exact) on the vector units instead, which leaves no
+// cancellation when the row's mean is large against its spread.
 //
 // With M a few dozen rows these are weight-streaming problems whose time is set
 // by memory latency, so a workgroup of the first row group issues every load
@@ -82,11 +91,11 @@ __host__ __device__ constexpr int gemm_red_bytes() {
   return NW * 2 * NB * 64 * 16;
 }
 // LDS: the wave partial tiles; with LayerNorm folding, then the waves' row
-// partials [NW][32] (sum, sum of squares)
+// partials [NW][32] (sum, sum of squares) and the rows' shifts [32]
 template <int EPI, int NB>
 __host__ __device__ constexpr int gemm_lds_bytes() {
   constexpr int NW = gemm_waves<EPI>();
-  return gemm_red_bytes<NB, NW>() + (ln_on_load<EPI>() ? NW * kGemmRB * 8 : 0);
+  return gemm_red_bytes<NB, NW>() + (ln_on_load<EPI>() ? NW * kGemmRB * 8 + kGemmRB * 4 : 0);
 }
 
 // an operand fragment of all ones (B of the row-sum product)
@@ -104,6 +113,8 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   extern __shared__ __align__(16) char smem[];
   f32x4_t* red = reinterpret_cast<f32x4_t*>(smem);                          // [NW][2][NB][64]
   float2* s_ps = reinterpret_cast<float2*>(smem + gemm_red_bytes<NB, NW>());  // [NW][32] (sum, sumsq)
+  float* s_shift = reinterpret_cast<float*>(s_ps + NW * kGemmRB);              // [32] (fp32 models)
+  constexpr bool SHIFT = LNA && std::is_same<T, float>::value;  // shifted row statistics
 
   const int tid = threadIdx.x, lane = tid & 63;
   // w lives in a scalar register, so every guard that depends on it is a
@@ -145,12 +156,19 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   const Rsrc rA = make_rsrc(a.A, (uint32_t)a.mpad * a.lda * sizeof(T));
   const Rsrc rW = make_rsrc(a.W, (uint32_t)(a.Nout / 16) * a.kchunks * kChunkElems * sizeof(T));
   const uint32_t voff = lane * 8 * sizeof(T);
+  float shv[2] = {0.0f, 0.0f};  // SHIFT: the first element of row 16 r + n of the block
   auto load_a = [&](int m0, int round) {
 #pragma unroll
     for (int c = 0; c < CPW; ++c)
 #pragma unroll
       for (int r = 0; r < 2; ++r)
         ab[c][r].bload(rA, voff, (uint32_t)(((m0 >> 4) + r) * akc + kc_of(round, c)) * kChunkElems * sizeof(T));
+    if constexpr (SHIFT) {
+      if (round == 0) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) shv[r] = static_cast<const float*>(a.A)[frag_off(m0 + 16 * r + n, 0, akc)];
+      }
+    }
   };
   auto load_w = [&](int round) {
 #pragma unroll
@@ -196,6 +214,7 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       if constexpr (has_resid<EPI>()) load_res(m0);
     }
     f32x4_t acc[2][NB], accs[2], accq[2];  // accs, accq: row sums and sums of squares (LNA)
+    float vsu[2] = {0.0f, 0.0f}, vsq[2] = {0.0f, 0.0f};  // SHIFT: this lane's sums of x - x_0
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       accs[r] = accq[r] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -218,7 +237,16 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
           for (int r = 0; r < 2; ++r) {
 #pragma unroll
             for (int b = 0; b < NB; ++b) mma(acc[r][b], ab[c][r], wb[c][b]);
-            if constexpr (LNA) {
+            if constexpr (SHIFT) {  // lane (g, n): row n, k = 8g..8g+7 of the chunk, in k order
+              const float xv[8] = {ab[c][r].a.x, ab[c][r].a.y, ab[c][r].a.z, ab[c][r].a.w,
+                                   ab[c][r].b.x, ab[c][r].b.y, ab[c][r].b.z, ab[c][r].b.w};
+#pragma unroll
+              for (int j = 0; j < 8; ++j) {
+                const float d = xv[j] - shv[r];
+                vsu[r] += d;
+                vsq[r] = fmaf(d, d, vsq[r]);
+              }
+            } else if constexpr (LNA) {
               mma(accs[r], ab[c][r], one);
               mma(accq[r], ab[c][r], ab[c][r]);
             }
@@ -228,7 +256,9 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
     }
     // One round: the weights stay in registers and the A fragments are free
     // once the products are issued, so the group's next row block loads its A
-    // now, behind this block's reduction and epilogue (uniform branch).
+    // now, behind this block's reduction and epilogue (uniform branch).  The
+    // shifts of this block are kept first (the preload replaces them).
+    const float shcur[2] = {shv[0], shv[1]};
     if (rounds == 1 && m0 + mstep < M) load_a(m0 + mstep, 0);
 
     // ---- sum the waves' partial tiles in wave order
@@ -236,7 +266,20 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
     for (int r = 0; r < 2; ++r)
 #pragma unroll
       for (int b = 0; b < NB; ++b) red[((w * 2 + r) * NB + b) * 64 + lane] = acc[r][b];
-    if constexpr (LNA) {
+    if constexpr (SHIFT) {
+      // the four lanes of row n (g = 0..3) combined in a fixed order
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        vsu[r] += __shfl_xor(vsu[r], 16, 64);
+        vsq[r] += __shfl_xor(vsq[r], 16, 64);
+        vsu[r] += __shfl_xor(vsu[r], 32, 64);
+        vsq[r] += __shfl_xor(vsq[r], 32, 64);
+        if (g == 0) {
+          s_ps[w * kGemmRB + 16 * r + n] = make_float2(vsu[r], vsq[r]);
+          if (w == 0) s_shift[16 * r + n] = shcur[r];
+        }
+      }
+    } else if constexpr (LNA) {
       // lane (g, n) holds rows 4g..4g+3 of column n: row n's sum (any column)
       // and its sum of squares (the diagonal) sit in element n - 4g
       const int i = n - 4 * g;
@@ -260,8 +303,9 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
         su += p.x;
         sq += p.y;
       }
-      const float mean = su / (float)D;
+      float mean = su / (float)D;
       const float var = fmaxf(sq / (float)D - mean * mean, 0.0f);
+      if constexpr (SHIFT) mean += s_shift[16 * re + 4 * g + ie];  // the sums were of x - x_0
       rstd = 1.0f / sqrtf(var + a.sh.eps);
       nmr = -mean * rstd;
     }
@@ -274,11 +318,11 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       for (int ww = 0; ww < NW; ++ww) x += redf[(((ww * 2 + re) * NB + b) * 64 + lane) * 4 + ie];
       if constexpr (EPI == EPI_PART) {
         if (ok) static_cast<float*>(a.out)[((size_t)ks * a.mpad + row) * a.ldo + col] = x;
-      } else if constexpr (EPI == EPI_RES) {  // H = S(Z + (O W_o + b_o))
-        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resv[b] + (x + biasv[b]));
-      } else if constexpr (EPI == EPI_DOWN) {  // Z_{l+1} = S(H + (G W_2 + b_2))
+      } else if constexpr (EPI == EPI_RES) {  // H = S(Z + S(O W_o + b_o))
+        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resv[b] + Elem<T>::rnd(x + biasv[b]));
+      } else if constexpr (EPI == EPI_DOWN) {  // Z_{l+1} = S(H + S(G W_2 + b_2))
         if (ok) {
-          const T z = Elem<T>::cv(resv[b] + (x + biasv[b]));
+          const T z = Elem<T>::cv(resv[b] + Elem<T>::rnd(x + biasv[b]));
           static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = z;
           gbl(x_row<T>(rinfo.cache, a.cl, a.sh, a.layer + 1, rinfo.tok))[col] = z;
         }
@@ -301,9 +345,9 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
             gbl(reinterpret_cast<T*>(base))[e] = o;
           }
         }
-      } else {  // EPI_FC1
+      } else {  // EPI_FC1: G = S(GELU(S(LN2(H) W_1 + b_1)))
         x = fmaf(rstd, x, fmaf(nmr, c1v[b], biasv[b]));
-        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(gelu_tanh(x));
+        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(gelu_tanh(Elem<T>::rnd(x)));
       }
     }
     __syncthreads();  // red and the row partials are reused by the next row block

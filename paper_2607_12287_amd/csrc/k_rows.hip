@@ -1,13 +1,14 @@
 // Row kernel that finishes the split-K MLP down projection of a layer (paper
 // §III-B: the residual addition after the MLP), one workgroup per compact row:
 //
-//   Z' = S(H + ((P_0 + P_1 + ...) + b_2))   (X^{l+1} rows, and the next
+//   Z' = S(H + S((P_0 + P_1 + ...) + b_2))  (X^{l+1} rows, and the next
 //                                           layer's input in operand order)
 //   after the last layer also Y = S(LN_f(Z')) into the cache and the caller's
 //   `refreshed` rows.
 //
-// The partial sums are added in split order, then the bias, then the residual,
-// which is the order the unsplit product would use.  LayerNorm: two passes
+// The partial sums are added in split order, then the bias; the MLP output is
+// rounded to the storage type before the residual add, whose sum is rounded
+// again (each operation stores its result, as in a half-precision pipeline).  LayerNorm: two passes
 // (mean, then mean squared deviation) over the row in fp32, thread partials
 // summed in index order and combined across the workgroup in a fixed order.
 // Every load is issued before M is known (the compact buffers are padded past
@@ -92,7 +93,7 @@ __global__ __launch_bounds__(256) void res_kernel(ResArgs a) {
     float4 x = p[0][j];
 #pragma unroll
     for (int s = 1; s < S; ++s) x = add4(x, p[s][j]);
-    x = add4(x, bias[j]);
+    x = rnd4(add4(x, bias[j]), static_cast<T*>(nullptr));
     v[j] = rnd4(add4(res[j], x), static_cast<T*>(nullptr));
     if (tid + 256 * j < D4) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
   }

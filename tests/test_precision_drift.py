@@ -9,8 +9,8 @@ deep hidden states grows past 2e-2 with no mistake anywhere.
 
 This test shows it on the CPU with no GPU code at all: the same layers as the
 oracle (same rounding points, fp64 LayerNorm, softmax and GELU), with only the
-GEMM accumulation switched to fp32, drift from the oracle by more than 1e-2
-and stay inside the free-running bound the GPU tests use (4e-2).  The per-layer
+GEMM accumulation switched to fp32, drift from the oracle past the per-layer
+bar (2e-2) and stay inside the free-running bound the GPU tests use (4e-2).  The per-layer
 (teacher-forced) GPU checks keep the strict 2e-2 bar, since one layer alone
 does not compound.
 """
@@ -39,10 +39,10 @@ def _encode_fp32_gemms(model, t0):
         A = S(vit.layer_norm(Z, p("ln1_g"), p("ln1_b"), m.ln_eps))
         qkv = S(mm(A, p("w_qkv")) + p("b_qkv"))
         O = S(vit.attention(qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], H))
-        Hr = S(Z + (mm(O, p("w_o")) + p("b_o")))
+        Hr = S(Z + S(mm(O, p("w_o")) + p("b_o")))
         A2 = S(vit.layer_norm(Hr, p("ln2_g"), p("ln2_b"), m.ln_eps))
-        G = S(vit.gelu_tanh(mm(A2, p("w_1")) + p("b_1")))
-        Z = S(Hr + (mm(G, p("w_2")) + p("b_2")))
+        G = S(vit.gelu_tanh(S(mm(A2, p("w_1")) + p("b_1"))))
+        Z = S(Hr + S(mm(G, p("w_2")) + p("b_2")))
         xs.append(Z)
     return xs
 
@@ -58,5 +58,6 @@ def test_fp32_accumulation_alone_drifts_past_the_per_layer_bar():
     errs = [float(np.abs(xs[l] - cache.X[l]).max() / np.abs(cache.X[l]).max()) for l in range(m.depth + 1)]
     assert errs[0] == 0.0                       # same embedding, same rounding
     assert errs[1] <= TOL["bf16"]               # one layer: inside the strict bar
-    assert max(errs) > 0.5 * TOL["bf16"]        # depth: the drift is real
+    print("fp32-accumulation drift per layer:", " ".join(f"{e:.2e}" for e in errs))
+    assert max(errs) > TOL["bf16"]              # depth: the drift passes the per-layer bar
     assert max(errs) <= FREE_TOL["bf16"]        # and inside the free-running bound
