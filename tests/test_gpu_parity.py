@@ -47,6 +47,9 @@ def test_small_models_stream(name):
 
 
 def _workload_run(name, steps, oracle_views=None, rho=0.10, row_groups=0):
+    """Full encode, then `steps` steps of the workload's stream, each checked
+    per layer (teacher-forced) and free-running; prints the worst error of
+    each step so that any growth over the stream shows."""
     wl = synth.workload(name, rho=rho)
     m = wl.model
     say(f"[{name}] rho={rho} views={wl.views} steps={steps} row_groups={row_groups}")
@@ -60,37 +63,45 @@ def _workload_run(name, steps, oracle_views=None, rho=0.10, row_groups=0):
     tf = p.check_layers(None, f"{name} full")
     worst = p.check_caches(f"{name} full")
     say(f"  full encode: per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
+    hist = []
     for t in range(1, steps + 1):
         idx, count, refreshed, res = p.step(frames[t], wl.tau, wl.caps)
         p.check_step(idx, count, refreshed, res, f"{name} step {t}")
         tf = p.check_layers(lambda v: idx[v, :count[v]], f"{name} step {t}")
         worst = p.check_caches(f"{name} step {t}")
+        hist.append((tf, worst))
         say(f"  step {t}: count={count.tolist()} per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
+    if hist:
+        say(f"  over {steps} steps: per-layer worst {max(h[0] for h in hist):.2e}, "
+            f"free-running worst {max(h[1] for h in hist):.2e}")
+    return hist
 
 
 def test_tiny_workload():
     _workload_run("tiny", 8)
 
 
-def test_so400m_workload():
-    _workload_run("so400m", 3)
+def test_so400m_full_stream():
+    """The 64-frame stream of the So400m workload: a full encode and all 63 steps."""
+    _workload_run("so400m", 63)
 
 
-@pytest.mark.parametrize("row_groups", [0, 4])
-def test_so400m_three_views(row_groups):
-    """row_groups 4: the threshold steps' GEMM row groups that a caller expecting
-    about a hundred rows sets (each GEMM then takes its own share of them)."""
-    _workload_run("so400m_x3", 2, row_groups=row_groups)
+@pytest.mark.parametrize("row_groups,steps", [(0, 32), (4, 2)])
+def test_so400m_three_views(row_groups, steps):
+    """32 frames of the three-stream workload; row_groups 4 (two steps): the
+    threshold steps' GEMM row groups that a caller expecting about a hundred
+    rows sets (each GEMM then takes its own share of them)."""
+    _workload_run("so400m_x3", steps, row_groups=row_groups)
 
 
-@pytest.mark.parametrize("rho", [0.02, 0.10, 1.0])
+@pytest.mark.parametrize("rho", [0.02, 0.05, 0.10, 0.25, 0.50, 1.0])
 def test_so400m_448_top_k(rho):
     _workload_run("so400m_448", 1, rho=rho)
 
 
-@pytest.mark.parametrize("row_groups", [0, 6])
-def test_vitl_eight_streams_sampled(row_groups):
-    _workload_run("vitl_x8", 2, oracle_views=[0, 5], row_groups=row_groups)
+@pytest.mark.parametrize("row_groups,steps", [(0, 32), (6, 2)])
+def test_vitl_eight_streams_sampled(row_groups, steps):
+    _workload_run("vitl_x8", steps, oracle_views=[0, 5], row_groups=row_groups)
 
 
 @pytest.mark.parametrize("waves", [2, 4, 8])

@@ -1,0 +1,88 @@
+"""The edge-case inputs do what they are built for, on the oracle alone."""
+import numpy as np
+import pytest
+
+from oracle import vit
+from paper_2607_12287_amd import synth
+from tests import edge_cases
+
+
+@pytest.mark.parametrize("img", [64, 80])
+def test_tie_group_has_equal_similarities_below_the_rest(img):
+    m, w = edge_cases.tie_model(img)
+    frames, grp, mov = edge_cases.tie_frames(m, 2300 + img)
+    model = vit.Model(m, w)
+    cache = vit.full_encode(model, frames[0][0])
+    t0 = vit.embed(model, frames[1][0])
+    sim = vit.pinned.cosine_f32(t0, cache.ref)
+    assert len(set(sim[grp].tolist())) == 1            # the group ties exactly
+    static = np.setdiff1d(np.arange(m.n_tokens), np.concatenate([grp, mov]))
+    assert sim[grp][0] < sim[static].min()             # and sits below every static token
+    # a cap inside the group keeps the moved tokens below it and the group's lowest indices
+    below = mov[sim[mov] < sim[grp][0]]
+    cap = below.size + 5
+    U = vit.select(sim, np.inf, cap)
+    assert set(U.tolist()) == set(below.tolist()) | set(grp[:5].tolist())
+    # a threshold equal to the tied value excludes the whole group (strict <)
+    assert not set(vit.select(sim, float(sim[grp][0]), m.n_tokens).tolist()) & set(grp.tolist())
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_large_mean_rows_are_large_mean(dtype):
+    m, w = edge_cases.large_mean_model(dtype)
+    if dtype == "bf16":
+        assert np.array_equal(w["b_pe"], vit.round_bf16(w["b_pe"]))
+    x = synth.random_patches(m, 2201)[0]
+    cache = vit.full_encode(vit.Model(m, w), x)
+    for l in range(m.depth + 1):
+        X = cache.X[l]
+        ratio = np.abs(X.mean(axis=1)) / X.std(axis=1)
+        assert ratio.min() >= 15.0, (l, ratio.min())
+
+
+def _fold_layer(model, l, Z, U, K, V):
+    """One layer as the oracle computes it except for the LayerNorm folding of
+    the GPU kernels: LN(x) W + b = rstd (x W') - rstd mean c1 + beta^T W + b
+    with W' = S(gamma W), in fp64 (the departure alone, no fp32 arithmetic)."""
+    m, S, D = model.shape, vit.round_bf16, model.shape.dim
+
+    def lin_fold(X, g, b, W, bias):
+        Wp = S(g[:, None] * W)
+        mean = X.mean(1, keepdims=True)
+        rstd = 1.0 / np.sqrt(((X - mean) ** 2).mean(1, keepdims=True) + model.eps)
+        return rstd * (X @ Wp) - rstd * mean * Wp.sum(0) + (b @ W + bias)
+
+    p = lambda n: model.p(l, n)  # noqa: E731
+    qkv = S(lin_fold(Z, p("ln1_g"), p("ln1_b"), p("w_qkv"), p("b_qkv")))
+    K[U], V[U] = qkv[:, D:2 * D], qkv[:, 2 * D:]
+    O = S(vit.attention(qkv[:, :D], K, V, m.heads))
+    H = S(Z + S(O @ p("w_o") + p("b_o")))
+    G = S(vit.gelu_tanh(S(lin_fold(H, p("ln2_g"), p("ln2_b"), p("w_1"), p("b_1")))))
+    return S(H + S(G @ p("w_2") + p("b_2")))
+
+
+def test_fold_alone_drifts_on_large_mean_bf16_rows():
+    """Why the bf16 large-mean GPU test checks K, V and Y per layer only: on
+    these rows the folding departure by itself, in fp64, drifts past the
+    free-running bar on the second layer's K and V and on Y while each layer
+    stays inside the per-layer bar."""
+    m, w = edge_cases.large_mean_model("bf16")
+    model = vit.Model(m, w)
+    x = synth.patchify(next(synth.RefillRectStream(m, 2210, 0, 15, 19).frames(1)), m.patch)
+    cache = vit.full_encode(model, x)
+    U = np.arange(m.n_tokens)
+    Z = cache.X[0].copy()
+    free, per_layer = [], []
+    for l in range(m.depth):
+        K, V = np.zeros_like(cache.K[l]), np.zeros_like(cache.V[l])
+        Kt, Vt = np.zeros_like(K), np.zeros_like(V)
+        Zt = _fold_layer(model, l, cache.X[l], U, Kt, Vt)        # teacher-forced
+        Z = _fold_layer(model, l, Z, U, K, V)                     # free-running
+        rel = lambda a, b: float(np.abs(a - b).max() / np.abs(b).max())  # noqa: E731
+        per_layer += [rel(Zt, cache.X[l + 1]), rel(Kt, cache.K[l]), rel(Vt, cache.V[l])]
+        free += [rel(K, cache.K[l]), rel(V, cache.V[l])]
+    Y = vit.final_rows(model, Z)
+    free.append(float(np.abs(Y - cache.Y).max() / np.abs(cache.Y).max()))
+    assert max(per_layer) <= 2e-2, per_layer
+    assert max(free) > 4e-2, free
+    assert free[-1] > 4e-2, free          # the final LayerNorm's output too
