@@ -19,7 +19,10 @@ _lib = None
 
 
 def build(force: bool = False) -> str:
-    """Compile pinned.c with gcc (contraction off, so only the written fmaf fuse)."""
+    """Compile pinned.c with gcc (contraction off, so only the written fmaf fuse).
+    ORACLE_PINNED_LIB names a prebuilt copy instead (the sanitizer build)."""
+    if os.environ.get("ORACLE_PINNED_LIB"):
+        return os.environ["ORACLE_PINNED_LIB"]
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-O3", "-mavx2", "-mfma", "-ffp-contract=off", "-fno-fast-math",

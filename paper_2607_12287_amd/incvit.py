@@ -14,7 +14,9 @@ from typing import Dict, List, Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libincvit.so")
+# INCVIT_LIB may name another build of the same library (the tests' sanitizer
+# build of the host code); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("INCVIT_LIB") or os.path.join(_HERE, "libincvit.so")
 
 INCVIT_OK, INCVIT_ERR_ARG, INCVIT_ERR_SHAPE, INCVIT_ERR_UNSUPPORTED, INCVIT_ERR_STATE, INCVIT_ERR_HIP = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "INCVIT_OK", -1: "INCVIT_ERR_ARG", -2: "INCVIT_ERR_SHAPE", -3: "INCVIT_ERR_UNSUPPORTED",
