@@ -435,6 +435,29 @@ def rho_sweep(steps: int, full_repeats: int) -> dict:
                         f"{steps} steps per ratio", "sweep": rows, "break_even_rho": even}
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo) and its logical CPU count."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return f"{name} ({os.cpu_count()} logical CPUs visible)"
+
+
+# The paper's own figures for this path (context, not the target): ViT latency
+# of the pi0.5 pipeline without and with temporal token reuse, Table III, on
+# the hardware of Appendix A.
+PAPER_CONTEXT = {"vit_latency_ms_without_reuse": 40.1, "vit_latency_ms_with_token_reuse": 28.5,
+                 "vit_speedup_from_reuse": 1.41, "hardware": "1x NVIDIA A100, FP16, PyTorch",
+                 "workload": "LIBERO 224x224 observations inside the full VLA pipeline",
+                 "source": "Table III; hardware in Appendix A"}
+
+
 def cpu_baseline(wl, frames, seconds: float):
     """The oracle as it is, on this host: full encode of frame 0, then steps of
     the same stream until about `seconds` of step time have been spent."""
@@ -457,7 +480,9 @@ def cpu_baseline(wl, frames, seconds: float):
         spent += time.perf_counter() - t
         steps += 1
     out = {"value": round(steps * wl.views / spent, 4), "unit": "frames/s", "cores": int(threads),
-           "kind": "oracle",
+           "kind": "oracle", "cpu_model": cpu_model(),
+           "oracle": "oracle/ as committed: numpy float64 layers (BLAS threads) and the fixed-order fp32 "
+                     "embedding and cosine in C (OpenMP over tokens); not tuned for speed",
            "sample": f"{wl.name}: oracle full encode of frame 0, then {steps} incremental steps "
                      f"(frames 1..{steps}) of the same stream; value = frames / summed step time"}
     # the same steps on one thread, from a copy of the encoded caches, for
@@ -907,6 +932,7 @@ def main() -> int:
                          "min": round(each_ms[0], 5), "max": round(each_ms[-1], 5)},
         "full_encode_ms_dist": {"median": round(full_med, 5), "p90": round(quantile(sorted(full_ms), 0.9), 5)},
         "rows_dist": rows_dist(k),
+        "paper_context": PAPER_CONTEXT,
     }
     if not args.no_torch_full:
         tms, tmode = torch_full_forward(m, wl.weights(), frames[0], max(5, args.full_repeats // 2))

@@ -21,14 +21,14 @@
  *     the reference, incremental encoding on even chunks) are
  *     incvit_encode_frame with period 2; between full passes every refreshed
  *     token's vector becomes its new reference;
- *   - "all tokens are processed by the MLP layer" is read exactly by default
+ *   - the statement that every token goes through the MLP is read exactly by default
  *     (a reused row's MLP input is its cached state, so only U is computed);
  *     cfg.mlp_all = 1 selects the non-exact reading: every frame, every row
  *     starts from this frame's embedded token, reused rows add their cached
  *     attention-branch output S(O W_o + b_o) of each layer to their current
  *     residual stream, and the MLP runs over all rows (their K and V stay
  *     cached; their outputs follow the new frame);
- *   - "top rho*N lowest similarities" is generalised to: U = {i : sim_i < tau}
+ *   - the rule of refreshing the rho*N least similar tokens is generalised to: U = {i : sim_i < tau}
  *     (strict), and if |U| > cap only the cap lowest similarities are kept,
  *     equal similarities going to the lower token index.  tau = +INFINITY with
  *     cap = round(rho*N) is the paper's top-rho*N rule;

@@ -1,5 +1,5 @@
-"""Pins of the oracle's non-exact reading of "all tokens are processed by the
-MLP layer" (paper §III-B): reused rows add their cached attention-branch output
+"""Pins of the oracle's non-exact reading of the MLP statement of §III-B
+(every token goes through the MLP): reused rows add their cached attention-branch output
 to their current residual stream, and the MLP runs over every row.
 
 * 100% refresh is the plain full forward of the same reading;
