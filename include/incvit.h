@@ -199,6 +199,27 @@ incvit_status incvit_encode_frame(incvit_handle* h, int32_t B, const float* patc
                                   float tau, const int32_t* cap, int32_t* idx, int32_t* count,
                                   void* refreshed, void* workspace, void* stream);
 
+/* Incremental encode without any allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): incvit_step with the workspace taken from
+ * a static device array of INCVIT_NOALLOC_SCRATCH_BYTES (64 MiB) that the
+ * library holds on each GPU it runs on until the process ends (its address is
+ * resolved on the first call on a device).  Arguments, results, errors and
+ * kernels are those of incvit_step; the caller still passes inputs, caches and
+ * outputs.  A call whose workspace (incvit_workspace_bytes(h, B)) exceeds the
+ * array returns INCVIT_ERR_ARG before anything is enqueued (64 MiB holds up to
+ * seven streams of a So400m-shaped model at 224x224, 8.9 MiB each, one at
+ * 448x448, 35.5 MiB, or four ViT-L streams at 224x224, 36 MiB).
+ * No part of the array needs to start at zero: every call writes what it
+ * reads.  Every call on one GPU shares that GPU's array: calls that overlap in
+ * time on one GPU (other host threads, other streams) race and must be
+ * serialised by the caller.  Per-kernel profiling is not recorded. */
+#define INCVIT_NOALLOC_SCRATCH_BYTES (64 << 20)
+incvit_status incvit_step_noalloc(incvit_handle* h, int32_t B, const float* patches,
+                                  void* const* caches, float tau, const int32_t* cap,
+                                  int32_t* idx, int32_t* count, void* refreshed,
+                                  void* stream);
+
 /* ----------------------------------------------------------- cache state -- */
 
 /* Copy a cache into the canonical layout (incvit_cache_canonical_bytes). */

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -571,9 +572,9 @@ incvit_status check_views(incvit_handle* h, int32_t B, void* const* caches, View
     views.p[v] = static_cast<char*>(caches[v]);
   }
   // each stream's step writes its whole cache: two streams sharing bytes would race
-  std::vector<uintptr_t> base(B);
+  uintptr_t base[kMaxViews];
   for (int v = 0; v < B; ++v) base[v] = reinterpret_cast<uintptr_t>(caches[v]);
-  std::sort(base.begin(), base.end());
+  std::sort(base, base + B);
   for (int v = 1; v < B; ++v)
     if (base[v] - base[v - 1] < h->cl.total) return fail(h, INCVIT_ERR_ARG, "caches of one call must not overlap");
   return INCVIT_OK;
@@ -874,6 +875,64 @@ incvit_status incvit_encode_frame(incvit_handle* h, int32_t B, const float* patc
     return full_impl(h, B, patches, caches, idx, count, refreshed, workspace, stream);
   }
   return incvit_step(h, B, patches, caches, tau, cap, idx, count, refreshed, workspace, stream);
+}
+
+}  // extern "C"
+
+// Workspace of incvit_step_noalloc: one file-scope device array.  Each GPU the
+// library runs on holds its own copy (at its own address) until the process
+// ends.  Host code never uses the array's name as an address: its device
+// address is resolved once per device with hipGetSymbolAddress and kept.
+static __device__ __align__(256) char scratch[INCVIT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, resolved on its first use.
+incvit_status scratch_of_current_device(incvit_handle* h, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(h, INCVIT_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(h, INCVIT_ERR_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(h, INCVIT_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return INCVIT_OK;
+}
+}  // namespace
+
+extern "C" {
+
+incvit_status incvit_step_noalloc(incvit_handle* h, int32_t B, const float* patches, void* const* caches, float tau,
+                                  const int32_t* cap, int32_t* idx, int32_t* count, void* refreshed, void* stream) {
+  if (!h) return fail(nullptr, INCVIT_ERR_ARG, "null handle");
+  if (B < 1 || B > h->cfg.max_streams) return fail(h, INCVIT_ERR_ARG, "B must be in [1, max_streams]");
+  const size_t need = ws_layout(h->sh, B).total;
+  if (need > (size_t)INCVIT_NOALLOC_SCRATCH_BYTES) {
+    char buf[256];
+    snprintf(buf, sizeof buf,
+             "a step of %d stream(s) needs %zu bytes of workspace, beyond the %d-byte static scratch of "
+             "incvit_step_noalloc: call incvit_step with a workspace",
+             B, need, INCVIT_NOALLOC_SCRATCH_BYTES);
+    return fail(h, INCVIT_ERR_ARG, buf);
+  }
+  void* ws = nullptr;
+  incvit_status st = scratch_of_current_device(h, &ws);
+  if (st != INCVIT_OK) return st;
+  // no per-kernel profiling events here: creating one may allocate
+  const bool prof = h->prof;
+  h->prof = false;
+  st = incvit_step(h, B, patches, caches, tau, cap, idx, count, refreshed, ws, stream);
+  h->prof = prof;
+  return st;
 }
 
 incvit_status incvit_flow_two_anchor(int32_t S, int64_t n, const float* x0, const float* v0, const float* v7,

@@ -35,7 +35,8 @@ EXPORTS = ("incvit_canonical_weights_bytes", "incvit_packed_weights_bytes", "inc
            "incvit_cache_import", "incvit_cache_status", "incvit_last_error", "incvit_profile_enable",
            "incvit_profile_read", "incvit_step_graph_create", "incvit_full_graph_create",
            "incvit_graph_launch", "incvit_graph_destroy", "incvit_set_tuning", "incvit_encode_frame",
-           "incvit_flow_two_anchor")
+           "incvit_flow_two_anchor", "incvit_step_noalloc")
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class incvit_config(ctypes.Structure):
@@ -92,6 +93,7 @@ def lib() -> ctypes.CDLL:
             "incvit_set_tuning": (I32, [P, ctypes.POINTER(incvit_tuning)]),
             "incvit_encode_frame": (I32, [P, I32, P, P, ctypes.c_int64, I32, F32, P, P, P, P, P, P]),
             "incvit_flow_two_anchor": (I32, [I32, ctypes.c_int64, P, P, P, P, P, P, P, P]),
+            "incvit_step_noalloc": (I32, [P, I32, P, P, F32, P, P, P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -156,6 +158,13 @@ def incvit_step(h, B: int, patches: int, caches: Sequence[int], tau: float, cap:
     caps = (ctypes.c_int32 * B)(*[int(c) for c in cap])
     return lib().incvit_step(h, B, patches, _ptr_array(caches), float(tau), caps, idx, count,
                              refreshed, workspace, stream)
+
+
+def incvit_step_noalloc(h, B: int, patches: int, caches: Sequence[int], tau: float, cap: Sequence[int], idx: int,
+                        count: int, refreshed: int, stream: int = 0) -> int:
+    caps = (ctypes.c_int32 * B)(*[int(c) for c in cap])
+    return lib().incvit_step_noalloc(h, B, patches, _ptr_array(caches), float(tau), caps, idx, count, refreshed,
+                                     stream)
 
 
 def incvit_encode_frame(h, B: int, patches: int, caches: Sequence[int], frame_index: int, period: int, tau: float,

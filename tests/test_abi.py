@@ -91,3 +91,22 @@ def test_null_arguments_are_rejected():
     st, h = incvit.incvit_create(cfg, 0)
     assert st == incvit.INCVIT_ERR_ARG and not h.value
     assert incvit.lib().incvit_full_encode(None, 1, None, None, None, None) == incvit.INCVIT_ERR_ARG
+
+
+def test_noalloc_step_beyond_the_static_scratch_is_rejected_on_the_host():
+    """incvit_step_noalloc refuses a call whose workspace exceeds its static
+    scratch before touching the device (eight ViT-L streams need 72 MiB)."""
+    m = synth.VIT_L
+    st, h = incvit.incvit_create(incvit.make_config(m, 8), 1 << 20)
+    assert st == incvit.INCVIT_OK
+    try:
+        assert incvit.incvit_workspace_bytes(h, 8) > incvit.NOALLOC_SCRATCH_BYTES
+        assert incvit.incvit_workspace_bytes(h, 4) <= incvit.NOALLOC_SCRATCH_BYTES
+        caches = [(1 << 40) + i * (1 << 30) for i in range(8)]
+        st = incvit.incvit_step_noalloc(h, 8, 1 << 36, caches, 0.98, [256] * 8, 1 << 37, 1 << 38, 0, 0)
+        assert st == incvit.INCVIT_ERR_ARG
+        assert "static scratch" in incvit.incvit_last_error(h)
+        assert incvit.incvit_step_noalloc(h, 9, 1 << 36, caches, 0.98, [256] * 9, 1 << 37, 1 << 38, 0, 0) \
+            == incvit.INCVIT_ERR_ARG
+    finally:
+        incvit.lib().incvit_destroy(h)
