@@ -747,6 +747,8 @@ def main() -> int:
     ap.add_argument("--row-groups", type=int, default=0,
                     help="GEMM row groups of threshold steps (0 = ceil(mean rows / 32) of 8 calibration steps)")
     ap.add_argument("--attn-waves", type=int, default=0, help="waves per attention workgroup (0 = automatic)")
+    ap.add_argument("--tiled", type=int, default=0, help="large-row GEMM for calls of 256+ known rows: "
+                    "0 automatic, 1 never")
     ap.add_argument("--fc2-mode", type=int, default=0, help="MLP down projection: 1 split-K + row kernel, "
                                                             "2 unsplit with the residual in the epilogue (0 = default)")
     args = ap.parse_args()
@@ -801,10 +803,10 @@ def main() -> int:
             seen.append(int(enc.step(frames[t], ccaches, wl.tau, wl.caps)[1].sum()))
         row_groups = max(1, min(8, math.ceil(statistics.mean(seen) / 32)))
         del cbuf, ccaches
-    if args.cols or args.attn_qtiles or row_groups > 1 or args.attn_waves or args.fc2_mode:
+    if args.cols or args.attn_qtiles or row_groups > 1 or args.attn_waves or args.fc2_mode or args.tiled:
         cols = [int(x) for x in args.cols.split(",")] if args.cols else None
         incvit._check(incvit.incvit_set_tuning(enc.h, cols, args.attn_qtiles, row_groups, args.attn_waves,
-                                               args.fc2_mode), enc.h)
+                                               args.fc2_mode, args.tiled), enc.h)
     buf, caches = enc.new_caches(B)
     out = (torch.empty((B, m.n_tokens), dtype=torch.int32, device=dev),
            torch.empty((B,), dtype=torch.int32, device=dev),

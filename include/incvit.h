@@ -311,6 +311,12 @@ void incvit_graph_destroy(incvit_graph* g);
  * workgroups: one per CU; MLP up projection: two per CU; K-split MLP down
  * projection: one per CU; output projection: all), the rest looping over the
  * row blocks.
+ * tiled: the large-row GEMM of bf16 models (output tiles of 64 or 128 rows
+ * by 128 columns, K staged through LDS), used where the call's row count is
+ * known on the host and at least 512 (full encodes of several streams or of
+ * 448x448 frames, pure top-k steps of that many rows, the all-rows MLP):
+ * 0 = automatic (used there), 1 = never (the weight-streaming GEMM above).
+ * The cols, row_groups and fc2_mode fields do not apply to its launches.
  * A NULL pointer restores the defaults. */
 typedef struct {
   int32_t cols[4];
@@ -318,6 +324,7 @@ typedef struct {
   int32_t row_groups;
   int32_t attn_waves;
   int32_t fc2_mode;
+  int32_t tiled;
 } incvit_tuning;
 
 incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t);

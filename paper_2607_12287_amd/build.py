@@ -16,7 +16,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libincvit.so")
 DRIVE = os.path.join(HERE, "incvit_drive")
 SOURCES = ["incvit_api.hip", "k_embed.hip", "k_select.hip", "k_gemm.hip", "k_gemm_qkv.hip",
-           "k_gemm_fc1.hip", "k_gemm_part.hip", "k_gemm_res.hip", "k_gemm_att.hip", "k_gemm_down.hip", "k_rows.hip", "k_attn.hip", "k_misc.hip", "k_flow.hip"]
+           "k_gemm_fc1.hip", "k_gemm_part.hip", "k_gemm_res.hip", "k_gemm_att.hip", "k_gemm_down.hip", "k_gemm_tiled.hip", "k_rows.hip", "k_attn.hip", "k_misc.hip", "k_flow.hip"]
 # the fixed-order fp32 embedding and cosine must not be contracted beyond the
 # explicit fma intrinsics
 NO_CONTRACT = {"k_embed.hip"}

@@ -22,6 +22,9 @@ constexpr int kStatusNonFinite = -1;           // a step saw a NaN similarity
 // 16-column block is one 16-byte (bf16) or 32-byte (fp32) load per lane,
 // already in MFMA operand order.
 constexpr int kGemmRows = 64;
+// Calls of bf16 models with at least this many rows known on the host run
+// the large-row GEMM (gemm_tiled.hpp) instead of the weight-streaming one.
+constexpr int kTiledMinRows = 512;
 constexpr int kChunkElems = 512;  // 64 lanes x 8 elements
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
@@ -319,6 +322,8 @@ hipError_t launch_sim(const SimArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_commit(const RowsArgs& a, int mmax, hipStream_t s);
 hipError_t launch_gemm(int epi, int cols, const GemmArgs& a, hipStream_t s);
+// the large-row GEMM (gemm_tiled.hpp): bf16, whole K, rows = the call's M
+hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int rows, hipStream_t s);
 hipError_t launch_res(const ResArgs& a, int mmax, hipStream_t s);
 hipError_t launch_hsum(const HsumArgs& a, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, int max_rows_per_view, int qtiles, int waves, hipStream_t s);
@@ -480,6 +485,48 @@ __host__ __device__ __forceinline__ size_t v_elem(const Shape& sh, int h, int to
   const int kb = tok >> 5, r = tok & 31;
   const int g = r >> 3, j = r & 7, dt = d >> 4, n = d & 15;
   return ((((size_t)h * (sh.Npad >> 5) + kb) * (2 * sh.ndc) + dt) * 64 + (16 * g + n)) * 8 + j;
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (gfx9 encoding: vmcnt split over bits 3:0 and
+// 15:14; expcnt and lgkmcnt left at their no-wait maxima).
+__host__ __device__ constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// 16 bytes of LDS at byte address addr + off (off a compile-time constant)
+// into a register quad, without a wait: the caller waits for lgkmcnt.
+__device__ __forceinline__ void lds_read16(u32x4_t& out, uint32_t addr, int off) {
+  switch (off) {  // the offset is an immediate of the instruction
+#define INCVIT_DSR(o) \
+    case o: asm volatile("ds_read_b128 %0, %1 offset:" #o : "=v"(out) : "v"(addr)); break;
+    INCVIT_DSR(0) INCVIT_DSR(1024) INCVIT_DSR(2048) INCVIT_DSR(3072) INCVIT_DSR(4096) INCVIT_DSR(5120)
+    INCVIT_DSR(6144) INCVIT_DSR(7168) INCVIT_DSR(8192) INCVIT_DSR(9216) INCVIT_DSR(10240) INCVIT_DSR(11264)
+    INCVIT_DSR(12288) INCVIT_DSR(13312) INCVIT_DSR(14336) INCVIT_DSR(15360)
+#undef INCVIT_DSR
+    default: asm volatile("ds_read_b128 %0, %1" : "=v"(out) : "v"(addr + off)); break;
+  }
+}
+
+// The offsets above separate into a row (token) part and a column (dim) part,
+// so an epilogue that writes many rows of the same columns forms each part
+// once: frag_off = frag_row + frag_col, k_elem = k_tok + k_col, v_elem =
+// v_tok + v_col.
+__host__ __device__ __forceinline__ size_t frag_row(int r, int kc) { return ((size_t)(r >> 4) * kc * 64 + (r & 15)) * 8; }
+__host__ __device__ __forceinline__ size_t frag_col(int k) {
+  return ((size_t)(k >> 5) * 64 + (((k & 31) >> 3) << 4)) * 8 + (k & 7);
+}
+__host__ __device__ __forceinline__ size_t k_tok(const Shape& sh, int tok) {
+  const int r = tok & 31;
+  return (size_t)(tok >> 5) * 2 * sh.ndc * 512 + ((r & 7) >> 2) * sh.ndc * 512 + 8 * (4 * (r >> 3) + (r & 3));
+}
+__host__ __device__ __forceinline__ size_t k_col(const Shape& sh, int h, int d) {
+  return (size_t)h * (sh.Npad >> 5) * 2 * sh.ndc * 512 + (d >> 5) * 512 + 128 * ((d >> 3) & 3) + (d & 7);
+}
+__host__ __device__ __forceinline__ size_t v_tok(const Shape& sh, int tok) {
+  const int r = tok & 31;
+  return (size_t)(tok >> 5) * 2 * sh.ndc * 512 + 128 * (r >> 3) + (r & 7);
+}
+__host__ __device__ __forceinline__ size_t v_col(const Shape& sh, int h, int d) {
+  return (size_t)h * (sh.Npad >> 5) * 2 * sh.ndc * 512 + (d >> 4) * 512 + 8 * (d & 15);
 }
 
 }  // namespace incvit

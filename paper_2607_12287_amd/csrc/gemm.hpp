@@ -65,9 +65,13 @@ namespace incvit {
 constexpr int kGemmWaves = 8;
 constexpr int kGemmRB = 32;                       // rows per block: two 16-row MFMA tiles
 
+// GELU, tanh form, with tanh(u) = 1 - 2 / (1 + e^(2u)) on the hardware
+// exponential (error a few fp32 ulps, far below the bf16 rounding that
+// follows; the limits u -> +-inf give +-1).
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.0f + tanhf(u));
+  const float t = 1.0f - __fdividef(2.0f, 1.0f + __expf(2.0f * u));
+  return 0.5f * x * (1.0f + t);
 }
 
 template <int EPI>
@@ -104,6 +108,44 @@ __device__ __forceinline__ void ones(V8<float>& v) { v.a = make_float4(1.0f, 1.0
 
 __device__ __forceinline__ float elem4(const f32x4_t& v, int i) {
   return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
+}
+
+// One output element of a GEMM, x = the fp32 product over the whole K (or,
+// for PART, over this workgroup's share of K) at (row, col) with row < M:
+// bias, the folded LayerNorm (rstd, nmr = -mean * rstd of the row; QKV, FC1),
+// the residual element (RES, DOWN), the row's map entry (QKV, ATT, DOWN), and
+// the K split (PART).  Every operation's result is rounded to the storage type
+// once, as a half-precision pipeline stores it.
+template <class T, int EPI>
+__device__ __forceinline__ void epilogue_store(const GemmArgs& a, int row, int col, float x, float bias, float c1,
+                                               float resid, float rstd, float nmr, const RowInfo& rinfo, int ks) {
+  const int D = a.sh.D;
+  if constexpr (EPI == EPI_PART) {
+    static_cast<float*>(a.out)[((size_t)ks * a.mpad + row) * a.ldo + col] = x;
+  } else if constexpr (EPI == EPI_RES) {  // H = S(Z + S(O W_o + b_o))
+    static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resid + Elem<T>::rnd(x + bias));
+  } else if constexpr (EPI == EPI_DOWN) {  // Z_{l+1} = S(H + S(G W_2 + b_2))
+    const T z = Elem<T>::cv(resid + Elem<T>::rnd(x + bias));
+    static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = z;
+    gbl(x_row<T>(rinfo.cache, a.cl, a.sh, a.layer + 1, rinfo.tok))[col] = z;
+  } else if constexpr (EPI == EPI_ATT) {  // A^l[tok] = S(O W_o + b_o)
+    T* arow = reinterpret_cast<T*>(rinfo.cache + a.cl.a + (size_t)a.layer * a.cl.x_layer);
+    gbl(arow)[(size_t)rinfo.tok * D + col] = Elem<T>::cv(x + bias);
+  } else if constexpr (EPI == EPI_QKV) {  // [Q K V] = S(LN1(Z) W_qkv + b), K and V into the cache
+    const T o = Elem<T>::cv(fmaf(rstd, x, fmaf(nmr, c1, bias)));
+    const int which = col / D, c = col - which * D;
+    if (which == 0) {
+      static_cast<T*>(a.out)[(size_t)row * a.ldo + c] = o;
+    } else {
+      const int hh = c / a.sh.dh, d = c - hh * a.sh.dh;
+      char* base = rinfo.cache + (which == 1 ? a.cl.k : a.cl.v) + (size_t)a.layer * a.cl.kv_layer;
+      const size_t e = which == 1 ? k_elem(a.sh, hh, rinfo.tok, d) : v_elem(a.sh, hh, rinfo.tok, d);
+      gbl(reinterpret_cast<T*>(base))[e] = o;
+    }
+  } else {  // EPI_FC1: G = S(GELU(S(LN2(H) W_1 + b_1)))
+    const float f = fmaf(rstd, x, fmaf(nmr, c1, bias));
+    static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(gelu_tanh(Elem<T>::rnd(f)));
+  }
 }
 
 template <class T, int EPI, int NB, int CPW>
@@ -316,39 +358,7 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
       float x = 0.0f;
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) x += redf[(((ww * 2 + re) * NB + b) * 64 + lane) * 4 + ie];
-      if constexpr (EPI == EPI_PART) {
-        if (ok) static_cast<float*>(a.out)[((size_t)ks * a.mpad + row) * a.ldo + col] = x;
-      } else if constexpr (EPI == EPI_RES) {  // H = S(Z + S(O W_o + b_o))
-        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(resv[b] + Elem<T>::rnd(x + biasv[b]));
-      } else if constexpr (EPI == EPI_DOWN) {  // Z_{l+1} = S(H + S(G W_2 + b_2))
-        if (ok) {
-          const T z = Elem<T>::cv(resv[b] + Elem<T>::rnd(x + biasv[b]));
-          static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = z;
-          gbl(x_row<T>(rinfo.cache, a.cl, a.sh, a.layer + 1, rinfo.tok))[col] = z;
-        }
-      } else if constexpr (EPI == EPI_ATT) {  // A^l[tok] = S(O W_o + b_o)
-        if (ok) {
-          T* arow = reinterpret_cast<T*>(rinfo.cache + a.cl.a + (size_t)a.layer * a.cl.x_layer);
-          gbl(arow)[(size_t)rinfo.tok * D + col] = Elem<T>::cv(x + biasv[b]);
-        }
-      } else if constexpr (EPI == EPI_QKV) {
-        x = fmaf(rstd, x, fmaf(nmr, c1v[b], biasv[b]));
-        const int which = col / D, c = col - which * D;
-        const T o = Elem<T>::cv(x);
-        if (ok) {
-          if (which == 0) {
-            static_cast<T*>(a.out)[(size_t)row * a.ldo + c] = o;
-          } else {
-            const int hh = c / a.sh.dh, d = c - hh * a.sh.dh;
-            char* base = rinfo.cache + (which == 1 ? a.cl.k : a.cl.v) + (size_t)a.layer * a.cl.kv_layer;
-            const size_t e = which == 1 ? k_elem(a.sh, hh, rinfo.tok, d) : v_elem(a.sh, hh, rinfo.tok, d);
-            gbl(reinterpret_cast<T*>(base))[e] = o;
-          }
-        }
-      } else {  // EPI_FC1: G = S(GELU(S(LN2(H) W_1 + b_1)))
-        x = fmaf(rstd, x, fmaf(nmr, c1v[b], biasv[b]));
-        if (ok) static_cast<T*>(a.out)[frag_off(row, col, a.ldo / 32)] = Elem<T>::cv(gelu_tanh(Elem<T>::rnd(x)));
-      }
+      if (ok) epilogue_store<T, EPI>(a, row, col, x, biasv[b], c1v[b], resv[b], rstd, nmr, rinfo, ks);
     }
     __syncthreads();  // red and the row partials are reused by the next row block
   };

@@ -354,6 +354,7 @@ struct incvit_handle {
   int attn_waves = 0;          // 0 = automatic
   int fc2_mode = 0;            // 1: split-K + row kernel, 2: unsplit with the residual in the epilogue, 0: by M
   int row_groups = 1;          // GEMM row groups of threshold steps
+  int tiled = 0;               // 0: the large-row GEMM where it applies, 1: never
 };
 
 struct incvit_graph {
@@ -439,6 +440,11 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
   const Meta* mmeta = all ? reinterpret_cast<const Meta*>(ws + wl.meta_all) : meta;
   const int mlp_rows = all ? mall : mmax;
   const int mgroups = all ? groups_for(mall, true) : rgroups;
+  // the large-row GEMM: bf16 models, the rows of the call known on the host
+  // and at least kTiledMinRows (full encodes, pure top-k steps, the all-rows
+  // MLP); it runs every product over the whole K
+  const bool tiled_att = h->tiled == 0 && sh.dtype && exact_m && mmax >= kTiledMinRows;
+  const bool tiled_mlp = h->tiled == 0 && sh.dtype && (exact_m || all) && mlp_rows >= kTiledMinRows;
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
     // the MLP down projection of every layer but the last (whose row kernel
@@ -449,11 +455,12 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
     // sums of every row no longer go through memory), so by default only when
     // M is known on the host and at least 192
     const bool down = !all && l + 1 < sh.L &&
-                      (h->fc2_mode == 2 || (h->fc2_mode == 0 && exact_m && mmax >= 192));
+                      (tiled_mlp || h->fc2_mode == 2 || (h->fc2_mode == 0 && exact_m && mmax >= 192));
     auto gemm = [&](int kind, int kernel_kind) -> incvit_status {
       GemmGeom g = gemm_geom(sh, kind);
-      if (kind == G_FC2 && down) g.ksplit = 1;
       const bool mlp = kind == G_FC1 || kind == G_FC2;
+      const bool tiled = mlp ? tiled_mlp : tiled_att;
+      if (kind == G_FC2 && (down || tiled)) g.ksplit = 1;
       GemmArgs a;
       memset(&a, 0, sizeof a);
       a.rows = mlp ? mrows : rows;
@@ -500,6 +507,8 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
           }
           break;
       }
+      if (tiled)
+        return run(h, kernel_kind, s, [&] { return launch_gemm_tiled(epi, a, mlp ? mlp_rows : mmax, s); });
       const int cols = cols_of(h->cols, g, kind, a.rgroups, mlp ? mlp_rows : mmax, exact_m || (mlp && all));
       return run(h, kernel_kind, s, [&] { return launch_gemm(epi, cols, a, s); });
     };
@@ -513,7 +522,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       r.sh = sh;
       r.layer = l;
       r.part = reinterpret_cast<const float*>(ws + wl.part);
-      r.ksplit = g.ksplit;
+      r.ksplit = tiled_mlp ? 1 : g.ksplit;
       r.mpad = wl.Mpad;
       r.N = sh.N;
       r.res = ws + wl.h;
@@ -1019,11 +1028,14 @@ incvit_status incvit_set_tuning(incvit_handle* h, const incvit_tuning* t) {
   if (aw != 0 && aw != 2 && aw != 4 && aw != 8) return fail(h, INCVIT_ERR_ARG, "attn_waves must be 0, 2, 4 or 8");
   const int fm = t ? t->fc2_mode : 0;
   if (fm < 0 || fm > 2) return fail(h, INCVIT_ERR_ARG, "fc2_mode must be 0, 1 or 2");
+  const int tl = t ? t->tiled : 0;
+  if (tl < 0 || tl > 1) return fail(h, INCVIT_ERR_ARG, "tiled must be 0 or 1");
   for (int k = 0; k < 4; ++k) h->cols[k] = t ? t->cols[k] : 0;
   h->attn_qtiles = q;
   h->row_groups = rg > 0 ? rg : 1;
   h->attn_waves = aw;
   h->fc2_mode = fm;
+  h->tiled = tl;
   return INCVIT_OK;
 }
 

@@ -49,7 +49,7 @@ class incvit_config(ctypes.Structure):
 
 class incvit_tuning(ctypes.Structure):
     _fields_ = [("cols", ctypes.c_int32 * 4), ("attn_qtiles", ctypes.c_int32), ("row_groups", ctypes.c_int32),
-                ("attn_waves", ctypes.c_int32), ("fc2_mode", ctypes.c_int32)]
+                ("attn_waves", ctypes.c_int32), ("fc2_mode", ctypes.c_int32), ("tiled", ctypes.c_int32)]
 
 
 class IncvitError(RuntimeError):
@@ -249,11 +249,11 @@ def incvit_graph_destroy(g) -> None:
 
 
 def incvit_set_tuning(h, cols: Optional[Sequence[int]] = None, attn_qtiles: int = 0, row_groups: int = 0,
-                      attn_waves: int = 0, fc2_mode: int = 0) -> int:
-    if cols is None and not attn_qtiles and not row_groups and not attn_waves and not fc2_mode:
+                      attn_waves: int = 0, fc2_mode: int = 0, tiled: int = 0) -> int:
+    if cols is None and not attn_qtiles and not row_groups and not attn_waves and not fc2_mode and not tiled:
         return lib().incvit_set_tuning(h, None)
     t = incvit_tuning((ctypes.c_int32 * 4)(*[int(k) for k in (cols or (0, 0, 0, 0))]), int(attn_qtiles),
-                      int(row_groups), int(attn_waves), int(fc2_mode))
+                      int(row_groups), int(attn_waves), int(fc2_mode), int(tiled))
     return lib().incvit_set_tuning(h, ctypes.byref(t))
 
 
