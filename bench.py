@@ -54,6 +54,8 @@ def kernel_kind(name: str):
         return None
     if m.group(1) == "gemm":
         return GEMM_KIND.get(m.group(2).split(",")[1].strip())
+    if m.group(1) == "gemm_tiled":  # template <EPI, BM, NS>
+        return GEMM_KIND.get(m.group(2).split(",")[0].strip())
     if m.group(1) == "res":
         return "res_ln1"
     return {"keyln": "key_ln", "keyproj": "key_proj"}.get(m.group(1), m.group(1))
@@ -646,6 +648,50 @@ def summarize_mfma(directory: str, drive_log: str, out: str, command: str) -> No
     print("\n".join(lines))
 
 
+def summarize_full(trace_dir: str, pmc_dir: str, drive_log: str, out: str, command: str) -> None:
+    """Full encodes of the native driver (its third argument repeats them):
+    per kernel kind the mean dispatch duration of the last encode's dispatches
+    (kernel trace), the matrix cores' busy fraction from the MfmaUtil counter
+    pass, and for the four GEMMs the algorithmic FLOP (2 M K N, M = views x
+    tokens) per launch over that duration against the dense bf16 peak."""
+    b = _bench_json(drive_log)
+    reps, L = b["full_encodes"], b["depth"]
+    M, D, F = b["views"] * b["tokens"], b["dim"], b["mlp"]
+    flop = {"qkv": 2.0 * M * D * 3 * D, "oproj": 2.0 * M * D * D, "fc1": 2.0 * M * D * F, "fc2": 2.0 * M * F * D}
+    rows = sorted(_csv_rows(trace_dir, "kernel_trace.csv"), key=lambda r: int(r["Dispatch_Id"]))
+    dur = {}
+    for r, k in zip(rows, kinds_in_order([r["Kernel_Name"] for r in rows])):
+        if k:
+            dur.setdefault(k, []).append(((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3, r["Kernel_Name"]))
+    util = {}
+    disp = _pmc_per_dispatch(pmc_dir, "MfmaUtil")
+    for (_, n, v), k in zip(disp, kinds_in_order([n for _, n, _ in disp])):
+        if k:
+            util.setdefault(k, []).append(v)
+    for k in ("pack", "fold", "conv"):  # weight packing before the encodes
+        dur.pop(k, None)
+    lines = [f"# full encodes of {b['config']['workload']}: {b['views']} stream(s) x {b['tokens']} tokens = {M} rows, "
+             f"D={D}, F={F}, {L} layers; last of {reps} encodes",
+             f"# command: {command}",
+             "# per kind: mean over the last encode's dispatches; us from the kernel trace; mfma_util_pct from the",
+             "# MfmaUtil pass (busy cycles / active cycles x SIMDs); tflops = algorithmic 2 M K N / us; frac = / 2500",
+             f"source_hash {source_hash()}",
+             f"{'kind':8s} {'n':>4s} {'us':>9s} {'mfma_util_pct':>14s} {'tflops':>9s} {'frac':>7s}  kernel"]
+    total = 0.0
+    for k, d in dur.items():
+        last = d[-max(1, len(d) // reps):]  # every encode launches the same kernels
+        us = statistics.mean(x[0] for x in last)
+        total += sum(x[0] for x in last)
+        u = util.get(k, [])[-len(last):]
+        tf = flop[k] / (us * 1e-6) / 1e12 if k in flop else float("nan")
+        lines.append(f"{k:8s} {len(last):4d} {us:9.2f} {statistics.mean(u) if u else float('nan'):14.2f} "
+                     f"{tf:9.1f} {tf / 2500.0:7.3f}  {last[-1][1][:70]}")
+    lines.append(f"# summed kernel time of the last encode: {total:.1f} us")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_counters(directory: str, drive_log: str, out: str, command: str) -> None:
     """Every counter of one rocprofv3 --pmc pass, per kernel kind: the mean per
     dispatch over the last n dispatches of each kind (the incremental steps of
@@ -722,6 +768,7 @@ def main() -> int:
     ap.add_argument("--summarize-trace", nargs=5, metavar=("TRACE_DIR", "TRACED_BENCH_LOG", "PLAIN_BENCH_LOG", "OUT",
                                                            "COMMAND"))
     ap.add_argument("--summarize-mfma", nargs=4, metavar=("PMC_DIR", "DRIVE_LOG", "OUT", "COMMAND"))
+    ap.add_argument("--summarize-full", nargs=5, metavar=("TRACE_DIR", "PMC_DIR", "DRIVE_LOG", "OUT", "COMMAND"))
     ap.add_argument("--summarize-counters", nargs=4, metavar=("PMC_DIR", "DRIVE_LOG", "OUT", "COMMAND"))
     ap.add_argument("--summarize-pmc", nargs=8, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
                                                          "COPY_WRITE_DIR", "BENCH_LOG", "COPY_LOG", "OUT", "COMMANDS"))
@@ -763,6 +810,9 @@ def main() -> int:
         return 0
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters)
+        return 0
+    if args.summarize_full:
+        summarize_full(*args.summarize_full)
         return 0
     if args.dump_workload:
         return dump_workload(args.workload, args.rho, args.dump_workload, args.steps + 1)

@@ -4,7 +4,8 @@
 // process.  Also does a plain device-to-device copy of known size, the
 // calibration for the memory counters.
 //
-//   incvit_drive <dir> <steps>     dir holds config.txt, weights.bin, frames.bin
+//   incvit_drive <dir> <steps> [full]  dir holds config.txt, weights.bin, frames.bin;
+//                                     full: further full encodes of frame 0 after the first
 //   incvit_drive --copy <MiB>
 //
 // config.txt: "img_h img_w channels patch dim depth heads mlp_dim dtype ln_eps
@@ -87,12 +88,17 @@ int copy_mode(int mib) {
 
 int main(int argc, char** argv) {
   if (argc == 3 && std::string(argv[1]) == "--copy") return copy_mode(atoi(argv[2]));
-  if (argc != 3) {
-    fprintf(stderr, "usage: incvit_drive <dir> <steps> | incvit_drive --copy <MiB>\n");
+  if (argc != 3 && argc != 4) {
+    fprintf(stderr, "usage: incvit_drive <dir> <steps> [full] | incvit_drive --copy <MiB>\n");
     return 2;
   }
   const std::string dir = argv[1];
   const int steps = atoi(argv[2]);
+  const int full_more = argc > 3 ? atoi(argv[3]) : 0;
+  if (full_more < 0 || full_more > 1000) {
+    fprintf(stderr, "full must be in [0, 1000]\n");
+    return 2;
+  }
 
   incvit_config cfg;
   memset(&cfg, 0, sizeof cfg);
@@ -167,6 +173,7 @@ int main(int argc, char** argv) {
 
   auto frame = [&](int t) { return reinterpret_cast<const float*>(static_cast<char*>(frames_d) + frame_bytes * t); };
   CHECK_IV(incvit_full_encode(h, views, frame(0), caches.data(), ws, nullptr), h);
+  for (int r = 0; r < full_more; ++r) CHECK_IV(incvit_full_encode(h, views, frame(0), caches.data(), ws, nullptr), h);
   std::vector<int32_t> cnt(views);
   std::vector<long> rows;
   for (int t = 1; t <= steps; ++t) {
@@ -195,9 +202,10 @@ int main(int argc, char** argv) {
   const long L = cfg.depth;
   printf("{\"steps\": %d, \"rows_mean\": %.3f, \"kernel_launches\": {\"embed\": %d, \"sim\": %d, \"select\": %d, "
          "\"commit\": %ld, \"qkv\": %ld, \"attn\": %ld, \"oproj\": %ld, \"fc1\": %ld, \"fc2\": %ld, "
-         "\"res_ln1\": %ld}, \"config\": {\"workload\": \"%s\", \"rows_mean\": %.3f}}\n",
+         "\"res_ln1\": %ld}, \"full_encodes\": %d, \"views\": %d, \"tokens\": %d, \"dim\": %d, \"depth\": %d, "
+         "\"mlp\": %d, \"config\": {\"workload\": \"%s\", \"rows_mean\": %.3f}}\n",
          steps, mean, steps, steps, steps, active, active * L, active * L, active * L, active * L, active * L,
-         active * L, dir.c_str(), mean);
+         active * L, full_more + 1, views, N, cfg.dim, cfg.depth, cfg.mlp_dim, dir.c_str(), mean);
   incvit_destroy(h);
   return 0;
 }

@@ -21,6 +21,9 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     ("void incvit::gemm_kernel<unsigned short, 4, 1, 5>(incvit::GemmArgs)", "oproj"),
     ("void incvit::gemm_kernel<unsigned short, 5, 2, 8>(incvit::GemmArgs)", "fc2"),
     ("void incvit::gemm_kernel<float, 0, 1, 2>(incvit::GemmArgs)", "qkv"),
+    ("void incvit::gemm_tiled_kernel<0, 128, 4>(incvit::GemmArgs)", "qkv"),
+    ("void incvit::gemm_tiled_kernel<5, 64, 6>(incvit::GemmArgs)", "fc2"),
+    ("void incvit::gemm_tiled_kernel<3, 64, 6>(incvit::GemmArgs)", "oproj"),
     ("void incvit::res_kernel<unsigned short, 3, 2>(incvit::ResArgs)", "res_ln1"),
     ("void incvit::embed_kernel<unsigned short, 0, 3, 2>(incvit::EmbedArgs)", "embed"),
     ("void incvit::keyproj_kernel<unsigned short, 0, 3, 2>(incvit::EmbedArgs)", "key_proj"),
