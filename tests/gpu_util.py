@@ -27,7 +27,7 @@ from paper_2607_12287_amd import incvit, synth
 
 TOL = {"bf16": 2e-2, "f32": 1e-4}
 GUARD_BYTE = 0xA5
-FREE_TOL = {"bf16": 4e-2, "f32": 1e-4}
+FREE_TOL = {"bf16": 5e-2, "f32": 1e-4}
 
 
 def say(*a):

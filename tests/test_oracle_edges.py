@@ -5,6 +5,7 @@ import pytest
 from oracle import vit
 from paper_2607_12287_amd import synth
 from tests import edge_cases
+from tests.gpu_util import FREE_TOL
 
 
 @pytest.mark.parametrize("img", [64, 80])
@@ -84,5 +85,5 @@ def test_fold_alone_drifts_on_large_mean_bf16_rows():
     Y = vit.final_rows(model, Z)
     free.append(float(np.abs(Y - cache.Y).max() / np.abs(cache.Y).max()))
     assert max(per_layer) <= 2e-2, per_layer
-    assert max(free) > 4e-2, free
-    assert free[-1] > 4e-2, free          # the final LayerNorm's output too
+    assert max(free) > FREE_TOL["bf16"], free
+    assert free[-1] > FREE_TOL["bf16"], free  # the final LayerNorm's output too
