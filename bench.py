@@ -794,7 +794,7 @@ def main() -> int:
     ap.add_argument("--row-groups", type=int, default=0,
                     help="GEMM row groups of threshold steps (0 = ceil(mean rows / 32) of 8 calibration steps)")
     ap.add_argument("--attn-waves", type=int, default=0, help="waves per attention workgroup (0 = automatic)")
-    ap.add_argument("--tiled", type=int, default=0, help="large-row GEMM for calls of 256+ known rows: "
+    ap.add_argument("--tiled", type=int, default=0, help="large-row GEMM for calls of 512+ known rows: "
                     "0 automatic, 1 never")
     ap.add_argument("--fc2-mode", type=int, default=0, help="MLP down projection: 1 split-K + row kernel, "
                                                             "2 unsplit with the residual in the epilogue (0 = default)")

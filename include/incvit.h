@@ -316,7 +316,9 @@ void incvit_graph_destroy(incvit_graph* g);
  * known on the host and at least 512 (full encodes of several streams or of
  * 448x448 frames, pure top-k steps of that many rows, the all-rows MLP):
  * 0 = automatic (used there), 1 = never (the weight-streaming GEMM above).
- * The cols, row_groups and fc2_mode fields do not apply to its launches.
+ * The cols and row_groups fields do not apply to its launches; its MLP down
+ * projection follows fc2_mode (1: split over K with the row kernel, 2:
+ * unsplit; 0: split while its 64-row tiles give fewer than 256 workgroups).
  * A NULL pointer restores the defaults. */
 typedef struct {
   int32_t cols[4];

@@ -90,6 +90,10 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(GemmArgs a) {
   const int M = a.meta->m;
   if (m0 >= M) return;  // uniform: no rows in this tile
   const int nblocks = a.Nout / 16, kchunks = a.kchunks, akc = a.lda / 32;
+  // K split (partial sums only): split ks takes chunks kbeg .. kbeg + nk - 1
+  const int ks = blockIdx.z;
+  const int kper = (kchunks + (int)gridDim.z - 1) / (int)gridDim.z;
+  const int kbeg = ks * kper, nk = min(kchunks - kbeg, kper);
 
   // operand fragments of chunk kc: A row tile t is kilobyte (m0/16 + t) * akc + kc
   // of the compact rows, W column block b is kilobyte (cb0 + b) * kchunks + kc
@@ -102,8 +106,9 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(GemmArgs a) {
   const char* gA = static_cast<const char*>(a.A);
   const char* gW = static_cast<const char*>(a.W);
   const uint32_t a_frags = (uint32_t)(a.mpad / 16) * akc;  // kilobytes of A
-  auto issue = [&](int kc) {
-    char* slot = ring + (kc % NS) * FPC * 1024;
+  auto issue = [&](int i) {  // chunk kbeg + i into ring slot i % NS
+    const int kc = kbeg + i;
+    char* slot = ring + (i % NS) * FPC * 1024;
 #pragma unroll
     for (int j = 0; j < LPW; ++j) {
       const int f = w + 4 * j;  // uniform
@@ -177,22 +182,23 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(GemmArgs a) {
     }
   };
 
-  // The K loop: chunk c sits in ring slot c % NS; NS - 1 chunks are in
+  // The K loop over the split's chunks (kc counts from kbeg): chunk kc sits
+  // in ring slot kc % NS; NS - 1 chunks are in
   // flight while one is multiplied, one barrier per chunk (two chunks per
   // barrier with NS - 2 in flight measured slower: the loads' latency, not
   // the barriers, sets the pace).
 #pragma unroll
   for (int c = 0; c < NS - 1; ++c)
-    if (c < kchunks) issue(c);
-  for (int kc = 0; kc < kchunks; ++kc) {
+    if (c < nk) issue(c);
+  for (int kc = 0; kc < nk; ++kc) {
     // chunk kc has landed once at most the loads of the chunks issued after
     // it are outstanding (loads complete in issue order)
-    if (kc + NS - 2 < kchunks) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPW * (NS - 2)));
+    if (kc + NS - 2 < nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPW * (NS - 2)));
     else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     // every wave's fragments of chunk kc are in LDS; every wave is done with
     // chunk kc - 1, whose slot the next issue refills
     __builtin_amdgcn_s_barrier();
-    if (kc + NS - 1 < kchunks) issue(kc + NS - 1);
+    if (kc + NS - 1 < nk) issue(kc + NS - 1);
     compute(ring_lds + (uint32_t)(kc % NS) * FPC * 1024);
   }
   __syncthreads();
@@ -275,7 +281,8 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(GemmArgs a) {
       const size_t rpart = frag_row(row, ldk);
       float o[8];
       if constexpr (EPI == EPI_PART) {
-        float4* dst = reinterpret_cast<float4*>(static_cast<float*>(a.out) + (size_t)row * a.ldo + cpart);
+        float4* dst =
+            reinterpret_cast<float4*>(static_cast<float*>(a.out) + ((size_t)ks * a.mpad + row) * a.ldo + cpart);
         dst[0] = lo;
         dst[1] = hi;
         continue;
@@ -343,17 +350,21 @@ hipError_t launch_tiled_cfg(const GemmArgs& a, int rows, hipStream_t s) {
   int gm = 1;
   while ((gm + 1) * (gm + 1) <= per_xcd) ++gm;
   b.rgroups = std::max(1, std::min(gm, mt));
-  return launch_k(gemm_tiled_kernel<EPI, BM, NS>, dim3(mt, nt), dim3(256), (size_t)lds, s, b);
+  return launch_k(gemm_tiled_kernel<EPI, BM, NS>, dim3(mt, nt, a.ksplit), dim3(256), (size_t)lds, s, b);
 }
 
-// rows: the call's row count M (known on the host); bf16 only, whole K
-// (a.ksplit == 1).  128-row tiles once they give a workgroup per CU or more,
-// 64-row tiles below.
+// rows: the call's row count M (known on the host); bf16 only.  The K split
+// (a.ksplit > 1) only for partial sums, each split at least one chunk.
+// 128-row tiles once they give a workgroup per CU or more, 64-row tiles below.
 template <int EPI>
 hipError_t launch_tiled_epi(const GemmArgs& a, int rows, hipStream_t s) {
-  if (!a.sh.dtype || a.ksplit != 1 || a.sh.dh % 8) return hipErrorInvalidValue;
+  if (!a.sh.dtype || a.ksplit < 1 || a.sh.dh % 8) return hipErrorInvalidValue;
+  if (a.ksplit > 1) {
+    const int kper = (a.kchunks + a.ksplit - 1) / a.ksplit;
+    if (EPI != EPI_PART || kper * (a.ksplit - 1) >= a.kchunks) return hipErrorInvalidValue;
+  }
   const int ntile = (a.Nout / 16 + kTiledBN / 16 - 1) / (kTiledBN / 16);
-  if ((rows + 127) / 128 * ntile >= 256) return launch_tiled_cfg<EPI, 128, 4>(a, rows, s);
+  if ((rows + 127) / 128 * ntile * a.ksplit >= 256) return launch_tiled_cfg<EPI, 128, 4>(a, rows, s);
   return launch_tiled_cfg<EPI, 64, 6>(a, rows, s);
 }
 

@@ -445,6 +445,17 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
   // MLP); it runs every product over the whole K
   const bool tiled_att = h->tiled == 0 && sh.dtype && exact_m && mmax >= kTiledMinRows;
   const bool tiled_mlp = h->tiled == 0 && sh.dtype && (exact_m || all) && mlp_rows >= kTiledMinRows;
+  // the large-row MLP down projection runs over K = F: its workgroup's chunks
+  // follow one another, so while its tiles give fewer than one workgroup per
+  // CU it is split over K like the small-M form (partial sums added by the
+  // row kernel): So400m at 768 and 1024 rows, 36-37 us for the whole K in
+  // one workgroup
+  int fc2_split = 1;
+  if (tiled_mlp) {
+    const GemmGeom g2 = gemm_geom(sh, G_FC2);
+    const int tiles = (mlp_rows + 63) / 64 * ((g2.nblocks + 7) / 8);
+    if (h->fc2_mode == 1 || (h->fc2_mode == 0 && tiles < 256)) fc2_split = g2.ksplit;
+  }
   for (int l = 0; l < sh.L; ++l) {
     const PackedLayer& P = h->pl.layers[l];
     // the MLP down projection of every layer but the last (whose row kernel
@@ -453,14 +464,23 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
     // slower for a few dozen rows (the whole K of 16 columns per workgroup
     // against a third of it), faster once M is in the hundreds (the partial
     // sums of every row no longer go through memory), so by default only when
-    // M is known on the host and at least 192
+    // M is known on the host and at least 192; the large-row form whenever it
+    // is not split over K (above)
     const bool down = !all && l + 1 < sh.L &&
-                      (tiled_mlp || h->fc2_mode == 2 || (h->fc2_mode == 0 && exact_m && mmax >= 192));
+                      (tiled_mlp ? fc2_split == 1
+                                 : h->fc2_mode == 2 || (h->fc2_mode == 0 && exact_m && mmax >= 192));
     auto gemm = [&](int kind, int kernel_kind) -> incvit_status {
       GemmGeom g = gemm_geom(sh, kind);
       const bool mlp = kind == G_FC1 || kind == G_FC2;
-      const bool tiled = mlp ? tiled_mlp : tiled_att;
-      if (kind == G_FC2 && (down || tiled)) g.ksplit = 1;
+      // the output projection (N = D) takes the large-row form only once its
+      // 64-row tiles fill the chip: with fewer its workgroups each run the
+      // whole K while most CUs idle (So400m at 512 / 768 / 1024 rows: 13.6 /
+      // 14.0 / 13.5 us against 8.3 / 10.9 / 12.7 us for the small-M form; 8
+      // ViT-L streams, 2048 rows and 256 tiles: 13.0 against 14.1 us)
+      const bool tiled = mlp ? tiled_mlp
+                             : tiled_att && (kind != G_OPROJ || (mmax + 63) / 64 * ((g.nblocks + 7) / 8) >= 256);
+      if (kind == G_FC2 && down) g.ksplit = 1;
+      else if (kind == G_FC2 && tiled) g.ksplit = fc2_split;
       GemmArgs a;
       memset(&a, 0, sizeof a);
       a.rows = mlp ? mrows : rows;
@@ -522,7 +542,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       r.sh = sh;
       r.layer = l;
       r.part = reinterpret_cast<const float*>(ws + wl.part);
-      r.ksplit = tiled_mlp ? 1 : g.ksplit;
+      r.ksplit = tiled_mlp ? fc2_split : g.ksplit;
       r.mpad = wl.Mpad;
       r.N = sh.N;
       r.res = ws + wl.h;
