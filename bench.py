@@ -36,9 +36,11 @@ GEMM_KIND = {"0": "qkv", "1": "fc1", "2": "fc2", "3": "oproj", "4": "oproj", "5"
 
 
 def source_hash() -> str:
-    """Hash of every kernel and ABI source: stored counters are used only while it matches."""
+    """Hash of every kernel and ABI source (not the native driver that only runs
+    them): stored counters are used only while it matches."""
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(ROOT, "paper_2607_12287_amd", "csrc", "*")) +
+    files = sorted([f for f in glob.glob(os.path.join(ROOT, "paper_2607_12287_amd", "csrc", "*"))
+                    if os.path.basename(f) != "incvit_drive.cpp"] +
                    glob.glob(os.path.join(ROOT, "include", "*.h")))
     for f in files:
         h.update(os.path.basename(f).encode())

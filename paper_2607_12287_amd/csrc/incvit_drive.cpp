@@ -88,8 +88,8 @@ int copy_mode(int mib) {
 
 int main(int argc, char** argv) {
   if (argc == 3 && std::string(argv[1]) == "--copy") return copy_mode(atoi(argv[2]));
-  if (argc != 3 && argc != 4) {
-    fprintf(stderr, "usage: incvit_drive <dir> <steps> [full] | incvit_drive --copy <MiB>\n");
+  if (argc < 3 || argc > 5) {
+    fprintf(stderr, "usage: incvit_drive <dir> <steps> [full] [attn_qtiles] | incvit_drive --copy <MiB>\n");
     return 2;
   }
   const std::string dir = argv[1];
@@ -97,6 +97,12 @@ int main(int argc, char** argv) {
   const int full_more = argc > 3 ? atoi(argv[3]) : 0;
   if (full_more < 0 || full_more > 1000) {
     fprintf(stderr, "full must be in [0, 1000]\n");
+    return 2;
+  }
+  // query tiles per attention workgroup (0 = the library's choice)
+  const int qtiles = argc > 4 ? atoi(argv[4]) : 0;
+  if (qtiles < 0 || qtiles > 2) {
+    fprintf(stderr, "attn_qtiles must be 0, 1 or 2\n");
     return 2;
   }
 
@@ -158,6 +164,12 @@ int main(int argc, char** argv) {
   CHECK_HIP(hipFree(canon));
   incvit_handle* h = nullptr;
   CHECK_IV(incvit_create(&cfg, packed, &h), nullptr);
+  if (qtiles) {
+    incvit_tuning t;
+    memset(&t, 0, sizeof t);
+    t.attn_qtiles = qtiles;
+    CHECK_IV(incvit_set_tuning(h, &t), h);
+  }
 
   CHECK_HIP(hipMalloc(&frames_d, fr.size()));
   CHECK_HIP(hipMemcpy(frames_d, fr.data(), fr.size(), hipMemcpyHostToDevice));
