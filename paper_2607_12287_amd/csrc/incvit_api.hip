@@ -295,9 +295,14 @@ int gemm_rgroups(const Shape& sh, const GemmGeom& g, int kind, int R) {
 // Query tiles per attention workgroup: one tile per workgroup while two-tile
 // workgroups would leave most CUs idle (few streams and heads), otherwise
 // two, which halves the K/V reads when a stream has many refreshed rows.
-int attn_qtiles_of(int tuned, int B, int H, int max_rows_per_view) {
+// With the rows known on the host and long streams (N >= 512) every query
+// tile's workgroup reads the head's whole K/V (295 KB at N = 1024, d_h = 72),
+// so two tiles per workgroup as soon as their workgroups still cover the CUs:
+// the 448x448 full encode, 1024 rows, 26.9 -> 21.3 us per launch.
+int attn_qtiles_of(int tuned, int B, int H, int N, int max_rows_per_view, bool exact) {
   if (tuned > 0) return tuned;
   const int groups2 = (max_rows_per_view + 31) / 32;
+  if (exact && N >= 512 && groups2 * B * H >= 256) return 2;
   return std::min(groups2, 2) * B * H < 128 ? 1 : 2;
 }
 
@@ -576,7 +581,7 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
       aa.o = ws + wl.o;
       aa.qmax = wl.Mpad - 1;
       aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)sh.dh));
-      const int qtiles = attn_qtiles_of(h->attn_qtiles, B, sh.H, max_rows_per_view);
+      const int qtiles = attn_qtiles_of(h->attn_qtiles, B, sh.H, sh.N, max_rows_per_view, exact_m);
       if ((st = run(h, INCVIT_K_ATTN, s, [&] { return launch_attn(aa, max_rows_per_view, qtiles, h->attn_waves, s); })) != INCVIT_OK)
         return st;
       if ((st = gemm(G_OPROJ, INCVIT_K_OPROJ)) != INCVIT_OK) return st;
