@@ -41,6 +41,29 @@ def _compile(src: str) -> str:
     return obj
 
 
+def objects(sources=SOURCES) -> list:
+    """Object files of the given sources, compiling only those older than their
+    source or any header (the sanitizer test links its own library from them
+    and leaves libincvit.so as it is)."""
+    os.makedirs(BUILD, exist_ok=True)
+    headers = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hpp")]
+    headers += [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))]
+    newest = max(os.path.getmtime(h) for h in headers)
+
+    def obj(src):
+        return os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+
+    def fresh(src):
+        o = obj(src)
+        return os.path.exists(o) and os.path.getmtime(o) >= max(newest, os.path.getmtime(os.path.join(CSRC, src)))
+
+    stale = [src for src in sources if not fresh(src)]
+    if stale:
+        with cf.ThreadPoolExecutor(max_workers=min(10, os.cpu_count() or 1)) as ex:
+            list(ex.map(_compile, stale))
+    return [obj(src) for src in sources]
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source for gfx950 and link libincvit.so; returns its path."""
     os.makedirs(BUILD, exist_ok=True)

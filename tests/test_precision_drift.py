@@ -65,25 +65,10 @@ def _encode_fp32_gemms(model, t0, mm_down=_mm32):
 
 
 @pytest.mark.slow
-def test_fp32_accumulation_alone_drifts_past_the_per_layer_bar():
-    wl = synth.workload("so400m")
-    m = wl.model
-    model = vit.Model(m, wl.weights())
-    frame = next(iter(wl.patch_frames(1)))[0]
-    cache = vit.full_encode(model, frame)
-    xs = _encode_fp32_gemms(model, cache.ref.astype(np.float64))
-    errs = [float(np.abs(xs[l] - cache.X[l]).max() / np.abs(cache.X[l]).max()) for l in range(m.depth + 1)]
-    assert errs[0] == 0.0                       # same embedding, same rounding
-    assert errs[1] <= TOL["bf16"]               # one layer: inside the strict bar
-    print("fp32-accumulation drift per layer:", " ".join(f"{e:.2e}" for e in errs))
-    assert max(errs) > TOL["bf16"]              # depth: the drift passes the per-layer bar
-    assert max(errs) <= FREE_TOL["bf16"]        # and inside the free-running bound
-
-
-@pytest.mark.slow
-def test_fp32_split_k_drift_on_the_448_frame_needs_the_free_running_bound():
+def test_fp32_accumulation_drifts_past_the_per_layer_bar_and_inside_the_free_running_bound():
     """1024 tokens, 27 layers: fp32 accumulation with the down projection's K
-    split in three drifts past 4e-2 and stays inside the free-running bound."""
+    split in three stays inside the per-layer bar for one layer, drifts past
+    it (and past 4e-2) with depth, and stays inside the free-running bound."""
     wl = synth.workload("so400m_448")
     m = wl.model
     model = vit.Model(m, wl.weights())
@@ -92,6 +77,8 @@ def test_fp32_split_k_drift_on_the_448_frame_needs_the_free_running_bound():
     xs = _encode_fp32_gemms(model, cache.ref.astype(np.float64), mm_down=_mm32_split3)
     errs = [float(np.abs(xs[l] - cache.X[l]).max() / np.abs(cache.X[l]).max()) for l in range(m.depth + 1)]
     print("fp32 split-K drift per layer:", " ".join(f"{e:.2e}" for e in errs))
-    assert errs[1] <= TOL["bf16"]
-    assert max(errs) > 4e-2
-    assert max(errs) <= FREE_TOL["bf16"]
+    assert errs[0] == 0.0                       # same embedding, same rounding
+    assert errs[1] <= TOL["bf16"]               # one layer: inside the per-layer bar
+    assert max(errs) > TOL["bf16"]              # depth: past the per-layer bar
+    assert max(errs) > 4e-2                     # and past the earlier 4e-2 free-running bar
+    assert max(errs) <= FREE_TOL["bf16"]        # inside the free-running bound

@@ -39,17 +39,16 @@ def test_host_code_is_clean_under_asan_and_ubsan(tmp_path):
     subprocess.check_call([os.path.join(LLVM, "bin/clang"), *san, "-mavx2", "-mfma", "-ffp-contract=off",
                            "-fPIC", "-shared", "-o", pinned, os.path.join(ROOT, "oracle", "pinned.c"), "-lm"])
 
-    # every other object of the library as built; incvit_api.hip with its host
-    # pass instrumented (each sanitizer flag applies to the host pass only)
-    hip_build.build()
+    # every other object of the library as built (compiled here only if stale);
+    # incvit_api.hip with its host pass instrumented (each sanitizer flag
+    # applies to the host pass only)
+    objs = hip_build.objects([s for s in hip_build.SOURCES if s != "incvit_api.hip"])
     host_san = []
     for f in san:
         host_san += ["-Xarch_host", f]
     api_obj = str(tmp_path / "incvit_api_san.o")
     subprocess.check_call([HIPCC, *hip_build.COMMON, *host_san, "-c",
                            os.path.join(hip_build.CSRC, "incvit_api.hip"), "-o", api_obj])
-    objs = [os.path.join(hip_build.BUILD, os.path.splitext(s)[0] + ".o") for s in hip_build.SOURCES
-            if s != "incvit_api.hip"]
     lib = str(tmp_path / "libincvit_san.so")
     subprocess.check_call([HIPCC, "--offload-arch=" + hip_build.ARCH, "-shared", "-fPIC", "-shared-libsan",
                            "-fsanitize=address,undefined", api_obj, *objs, "-o", lib])
