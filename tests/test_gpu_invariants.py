@@ -69,6 +69,47 @@ def test_step_graph_replays_match_eager_steps(score, mlp_mode, row_groups):
         enc.drop_graph(g)
 
 
+@pytest.mark.parametrize("name,row_groups", [("so400m", 1), ("vitl_x8", 6), ("so400m_448", 0)])
+def test_workload_graph_replays_match_eager_steps(name, row_groups):
+    """The launch configuration the benchmark times: the full-size workload's
+    step captured in a HIP graph (the bench's GEMM row groups) and replayed on
+    consecutive frames gives bit for bit the outputs and caches of the eager
+    steps, which the oracle parity tests check."""
+    wl = synth.workload(name)
+    m = wl.model
+    B = wl.views
+    enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=B)
+    if row_groups > 1:
+        incvit._check(incvit.incvit_set_tuning(enc.h, row_groups=row_groups), enc.h)
+    fr = [torch.from_numpy(f).cuda() for f in wl.patch_frames(4)]
+    bufa, ca = enc.new_caches(B)
+    bufb, cb = enc.new_caches(B)
+    enc.full_encode(fr[0], ca)
+    enc.full_encode(fr[0], cb)
+    inp = torch.empty_like(fr[0])
+    out_g = (torch.empty((B, m.n_tokens), dtype=torch.int32, device="cuda"),
+             torch.empty((B,), dtype=torch.int32, device="cuda"),
+             torch.empty((B, m.n_tokens, m.dim), dtype=enc.dtype, device="cuda"))
+    g = enc.step_graph(inp, ca, wl.tau, wl.caps, out_g)
+    try:
+        for t in range(1, 4):
+            inp.copy_(fr[t])
+            enc.launch(g)
+            idx, count, refreshed = enc.step(fr[t], cb, wl.tau, wl.caps)
+            torch.cuda.synchronize()
+            say(f"[{name} graph] frame {t}: count={count.tolist()}")
+            assert torch.equal(out_g[1], count)
+            for v in range(B):
+                k = int(count[v])
+                assert torch.equal(out_g[0][v, :k], idx[v, :k])
+                assert torch.equal(out_g[2][v, :k], refreshed[v, :k])
+            for x, y in zip(_raw(enc, ca), _raw(enc, cb)):
+                assert torch.equal(x, y)
+    finally:
+        enc.drop_graph(g)
+        enc.close()
+
+
 @pytest.mark.parametrize("score,mlp_mode", [("embed", "reuse"), ("key", "all")])
 def test_full_graph_matches_eager(score, mlp_mode):
     m, w, enc, fr = _setup(B=1, score=score, mlp_mode=mlp_mode)
