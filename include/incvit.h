@@ -295,7 +295,10 @@ void incvit_graph_destroy(incvit_graph* g);
  * has more than 1024 rows known on the host, two for the
  * output projection and the K-split down projection, and for the MLP up
  * projection from 1536 rows.
- * attn_qtiles: 16-query tiles per attention workgroup: 1 or 2; 0 = automatic.
+ * attn_qtiles: 16-query tiles per attention workgroup: 1 or 2; 0 = automatic
+ * (two when many streams and heads would still fill the CUs, or when the rows
+ * are known on the host, the stream has 512 tokens or more and two-tile
+ * workgroups still number 256 or more).
  * attn_waves: waves per attention workgroup, splitting the stream's keys: 2, 4
  * or 8; 0 = automatic (about two 32-key blocks per wave).
  * fc2_mode: the MLP down projection of every layer but the last: 1 = K split
@@ -315,7 +318,8 @@ void incvit_graph_destroy(incvit_graph* g);
  * by 128 columns, K staged through LDS), used where the call's row count is
  * known on the host and at least 512 (full encodes of several streams or of
  * 448x448 frames, pure top-k steps of that many rows, the all-rows MLP):
- * 0 = automatic (used there), 1 = never (the weight-streaming GEMM above).
+ * 0 = automatic (used there; the output projection only once its 64-row
+ * tiles number 256 or more), 1 = never (the weight-streaming GEMM above).
  * The cols and row_groups fields do not apply to its launches; its MLP down
  * projection follows fc2_mode (1: split over K with the row kernel, 2:
  * unsplit; 0: split while its 64-row tiles give fewer than 256 workgroups).

@@ -2,8 +2,10 @@
 // projection and MLP products, eqs. 4-5), for calls whose row count M is known
 // on the host and large: full encodes, top-k steps of several hundred rows and
 // the all-rows MLP.  The small-M kernel (gemm.hpp) streams the weights once
-// and re-reads the few A rows per 16-64 columns; here the product is
-// compute-bound, so the A and W operands are shared through LDS:
+// and re-reads the few A rows per 16-64 columns; here each workgroup stages a
+// tile of A rows and of W columns through LDS once per K chunk and all its
+// waves multiply from there (the staging, at 13-26 bytes per clock per CU
+// from L2, sets the pace):
 //
 //   * output tile BM x 128 per workgroup, 4 waves in a WR x WC grid, each
 //     wave owning (BM / WR) x (128 / WC) outputs as 16x16 MFMA accumulators
@@ -24,7 +26,11 @@
 //     every address split into a row part and a column part formed once;
 //   * each XCD takes a compact block of about sqrt(tiles / 8) row tiles by as
 //     many column tiles, so its workgroups share their A and W tiles in its
-//     L2 (the hardware deals workgroups to the XCDs round robin).
+//     L2 (the hardware deals workgroups to the XCDs round robin);
+//   * partial sums (the MLP down projection while its tiles are fewer than
+//     the CUs) may split K over the grid's third dimension: split z takes a
+//     contiguous range of chunks and writes its fp32 partial sums, which the
+//     row kernel adds in split order.
 //
 // bf16 models only (fp32 models use the small-M kernel).  Results do not
 // depend on the tile shape beyond the fp32 order of the MFMA accumulation,

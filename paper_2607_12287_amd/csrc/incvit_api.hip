@@ -447,7 +447,8 @@ incvit_status run_layers(incvit_handle* h, const Views& views, int B, const WsLa
   const int mgroups = all ? groups_for(mall, true) : rgroups;
   // the large-row GEMM: bf16 models, the rows of the call known on the host
   // and at least kTiledMinRows (full encodes, pure top-k steps, the all-rows
-  // MLP); it runs every product over the whole K
+  // MLP); the output projection only once its tiles fill the chip, and the
+  // MLP down projection split over K while they do not (below)
   const bool tiled_att = h->tiled == 0 && sh.dtype && exact_m && mmax >= kTiledMinRows;
   const bool tiled_mlp = h->tiled == 0 && sh.dtype && (exact_m || all) && mlp_rows >= kTiledMinRows;
   // the large-row MLP down projection runs over K = F: its workgroup's chunks
