@@ -168,15 +168,20 @@ __global__ __launch_bounds__(gemm_waves<EPI>() * 64) void gemm_kernel(GemmArgs a
   // (column group, K split, row group) of this workgroup, XCD-major; the
   // grid's shape comes from the arguments (no load of the dispatch packet)
   const int nz = a.rgroups, ny = a.ksplit, nx = a.Nout / 16 / NB;
-  int zg = 0, ks = blockIdx.y, cg = blockIdx.x;  // one row group: launch order
-  if (nz > 1) {                                   // uniform
+  int zg = 0, ks = blockIdx.y, cg = blockIdx.x;  // one row group, one K range: launch order
+  if (nz > 1 || ny > 1) {                         // uniform
     const int total = nx * ny * nz;
     const int lin = blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z);
     const int xcd = lin % 8, per = total / 8, rem = total % 8;
     const int pos = xcd * per + min(xcd, rem) + lin / 8;
-    zg = pos % nz;
-    ks = (pos / nz) % ny;
-    cg = pos / (nz * ny);
+    if (nz > 1) {  // the row groups of a column block together: its weights once per XCD
+      zg = pos % nz;
+      ks = (pos / nz) % ny;
+      cg = pos / (nz * ny);
+    } else {  // K ranges apart: an XCD reads about one range of A (nothing else is shared)
+      ks = pos / nx;
+      cg = pos % nx;
+    }
   }
   if (zg > 0) {  // a later row group reads M first and leaves when it has no rows (uniform)
     if (zg * kGemmRB >= *static_cast<const volatile int*>(&a.meta->m)) return;
