@@ -69,6 +69,46 @@ def test_all_rows_workloads(name, steps):
         say(f"  step {t}: count={count.tolist()} per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
 
 
+def test_all_rows_large_row_gemm():
+    """600 rows per call (6 streams of 100 tokens): the MLP of every call runs
+    the large-row GEMM, its down projection split over K into partial sums for
+    the row kernel, in full encodes and in threshold steps alike."""
+    m = synth.small_model(dim=256, depth=2, heads=4, mlp=520, img=40, patch=4, dtype="bf16")
+    B = 6
+    w = synth.make_weights(m, 2610)
+    say(f"[mlp all, large-row GEMM] N={m.n_tokens} B={B} rows={B * m.n_tokens}")
+    frames = frames_of(m, B, 3, 2620)
+    p = Pair(m, w, B, mlp="all")
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    p.check_caches("full")
+    for t, (tau, caps) in enumerate([(0.98, [m.n_tokens] * B), (np.inf, [30, 0, 100, 7, 64, 1])], start=1):
+        idx, count, refreshed, res = p.step(frames[t], tau, caps)
+        say(f"  step {t}: count={count.tolist()}")
+        p.check_step(idx, count, refreshed, res, f"step {t}")
+        p.check_layers(lambda v: idx[v, :count[v]], f"step {t}")
+        p.check_caches(f"step {t}")
+
+
+def test_all_rows_eight_vitl_streams_sampled():
+    """8 ViT-L streams, 2048 rows: the full encode's output projection writes
+    the attention branch through the large-row GEMM (its 64-row tiles fill the
+    chip); checked on streams 0 and 5."""
+    wl = synth.workload("vitl_x8")
+    m = wl.model
+    say("[mlp all vitl_x8] views 8, oracle views [0, 5]")
+    p = Pair(m, wl.weights(), wl.views, oracle_views=[0, 5], mlp="all")
+    frames = list(wl.patch_frames(2))
+    p.full_encode(frames[0])
+    p.check_layers(None, "full")
+    p.check_caches("full")
+    idx, count, refreshed, res = p.step(frames[1], wl.tau, wl.caps)
+    p.check_step(idx, count, refreshed, res, "step 1")
+    tf = p.check_layers(lambda v: idx[v, :count[v]], "step 1")
+    worst = p.check_caches("step 1")
+    say(f"  step 1: count={count.tolist()} per-layer worst {tf:.2e}, free-running worst {worst:.2e}")
+
+
 def test_all_rows_identical_frame_is_a_fixed_point_and_invalid_stream_untouched():
     m = synth.small_model(dim=256, depth=2, heads=4, mlp=200, img=40, patch=4, dtype="bf16")
     w = synth.make_weights(m, 431)
