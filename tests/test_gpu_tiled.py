@@ -18,17 +18,21 @@ CASES = {
 }
 
 
-@pytest.mark.parametrize("tiled", [0, 1])
+@pytest.mark.parametrize("tiled,fc2_mode", [(0, 0), (0, 2), (1, 0)])
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_large_row_gemm(name, tiled):
+def test_large_row_gemm(name, tiled, fc2_mode):
+    """fc2_mode 0: the down projection split over K (its tiles are fewer than
+    the CUs here); 2: unsplit, the residual and the cache write in its
+    epilogue."""
     dim, depth, heads, mlp, img, patch, B, caps = CASES[name]
     m = synth.small_model(dim=dim, depth=depth, heads=heads, mlp=mlp, img=img, patch=patch, dtype="bf16")
     w = synth.make_weights(m, 2500 + dim)
-    say(f"[large-row GEMM {name} tiled={tiled}] N={m.n_tokens} B={B} rows={B * m.n_tokens} D={dim} F={mlp}")
+    say(f"[large-row GEMM {name} tiled={tiled} fc2_mode={fc2_mode}] N={m.n_tokens} B={B} rows={B * m.n_tokens} "
+        f"D={dim} F={mlp}")
     its = [synth.RefillRectStream(m, 2510 + v, v, 3 * patch + 1, 5 * patch).frames(3) for v in range(B)]
     frames = [np.stack([synth.patchify(next(it), patch) for it in its]) for _ in range(3)]
     p = Pair(m, w, B)
-    incvit._check(incvit.incvit_set_tuning(p.enc.h, tiled=tiled), p.enc.h)
+    incvit._check(incvit.incvit_set_tuning(p.enc.h, tiled=tiled, fc2_mode=fc2_mode), p.enc.h)
     p.full_encode(frames[0])
     tf = p.check_layers(None, "full")
     fr = p.check_caches("full")
