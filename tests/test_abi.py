@@ -110,3 +110,24 @@ def test_noalloc_step_beyond_the_static_scratch_is_rejected_on_the_host():
             == incvit.INCVIT_ERR_ARG
     finally:
         incvit.lib().incvit_destroy(h)
+
+
+@pytest.mark.parametrize("field,value", [
+    ("cols", (3, 0, 0, 0)), ("cols", (0, 0, 0, 8)), ("cols", (-1, 0, 0, 0)),
+    ("attn_qtiles", 3), ("attn_qtiles", -1), ("row_groups", 9), ("attn_waves", 6),
+    ("fc2_mode", 3), ("tiled", 2),
+])
+def test_invalid_tunings_are_rejected(field, value):
+    """incvit_set_tuning validates every field on the host (no device work)."""
+    cfg = incvit.make_config(synth.small_model(dtype="bf16"), 2)
+    st, h = incvit.incvit_create(cfg, 1 << 20)
+    assert st == incvit.INCVIT_OK
+    try:
+        assert incvit.incvit_set_tuning(h, **{field: value}) == incvit.INCVIT_ERR_ARG
+        assert field.split("_")[0] in incvit.incvit_last_error(h)
+        # valid settings and the defaults are accepted
+        assert incvit.incvit_set_tuning(h, cols=(1, 2, 4, 0), attn_qtiles=2, row_groups=8, attn_waves=4,
+                                        fc2_mode=1, tiled=1) == incvit.INCVIT_OK
+        assert incvit.lib().incvit_set_tuning(h, None) == incvit.INCVIT_OK
+    finally:
+        incvit.lib().incvit_destroy(h)
