@@ -248,6 +248,28 @@ def test_full_refresh_step_matches_full_encode():
             assert rel_err(a[name], b[name]) <= TOL[m.dtype], name
 
 
+def test_448_full_refresh_equals_full_encode_on_every_frame():
+    """The 448x448 stream at rho = 100% (top-k of all 1024 tokens): every step
+    equals a full encode of the same frame bit for bit -- same rows, same row
+    order, same kernels -- on each of four frames."""
+    wl = synth.workload("so400m_448", rho=1.0)
+    m = wl.model
+    enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=1)
+    fr = [torch.from_numpy(f).cuda() for f in wl.patch_frames(5)]
+    bufa, ca = enc.new_caches(1)
+    bufb, cb = enc.new_caches(1)
+    enc.full_encode(fr[0], ca)
+    for t in range(1, 5):
+        idx, count, refreshed = enc.step(fr[t], ca, wl.tau, wl.caps)
+        enc.full_encode(fr[t], cb)
+        torch.cuda.synchronize()
+        say(f"[448 rho 100%] frame {t}: count={count.tolist()}")
+        assert count.tolist() == [m.n_tokens]
+        assert idx[0].tolist() == list(range(m.n_tokens))
+        assert torch.equal(_raw(enc, ca)[0], _raw(enc, cb)[0])
+    enc.close()
+
+
 def test_uninitialised_cache_and_nan_frame_are_no_ops():
     m, w, enc, fr = _setup()
     buf, c = enc.new_caches(2)           # zero-filled: never encoded
