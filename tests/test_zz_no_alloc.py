@@ -72,3 +72,29 @@ def test_noalloc_step_equals_step(name):
         _same(enc, ref, got, f"call {t}")
         assert torch.equal(buf_a, buf_b), f"call {t}: caches differ"
     enc.close()
+
+
+def test_noalloc_large_row_gemm():
+    """The 448x448 frame (1024 tokens) top-k: 512 rows (the large-row GEMM,
+    its down projection's partial sums in the static scratch), then 102 rows
+    (the weight-streaming GEMM) -- both equal incvit_step bit for bit."""
+    wl = synth.workload("so400m_448", rho=0.5)
+    m = wl.model
+    say(f"[noalloc 448] N={m.n_tokens} D={m.dim}")
+    enc = incvit.Encoder(m, synth.flatten_weights(m, wl.weights()), max_streams=1)
+    assert incvit.incvit_workspace_bytes(enc.h, 1) <= incvit.NOALLOC_SCRATCH_BYTES
+    frames = [torch.from_numpy(f).cuda() for f in wl.patch_frames(3)]
+    buf_a, ca = enc.new_caches(1)
+    buf_b, cb = enc.new_caches(1)
+    enc.full_encode(frames[0], ca)
+    enc.full_encode(frames[0], cb)
+    torch.cuda.synchronize()
+    for t, cap in enumerate([512, 102], start=1):
+        ref = enc.step(frames[t], ca, wl.tau, [cap])
+        got = _step_noalloc(enc, frames[t], cb, wl.tau, [cap])
+        torch.cuda.synchronize()
+        say(f"  call {t}: cap {cap} count {got[1].tolist()}")
+        assert got[1].tolist() == [cap]
+        _same(enc, ref, got, f"call {t}")
+        assert torch.equal(buf_a, buf_b), f"call {t}: caches differ"
+    enc.close()
